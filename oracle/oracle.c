@@ -1,0 +1,134 @@
+/*
+ * CPU oracle for C = A . B  (TEST INFRASTRUCTURE ONLY).
+ *
+ * Only tests, the smoke check and the bench's CPU-baseline leg may load this
+ * library; the product path never does.  It shares no code with the HIP
+ * library.
+ *
+ * What it computes.  The paper's kernels (MatMul and BatchMatMul, written as
+ * [M,K,N] in its kernel table, Table 3) are schedules of one loop nest: a
+ * candidate is a sequence of primitives (tiling, reorder, unroll, ...) applied
+ * to the same computation (Sec. 2, "kernel generation pipeline"; Fig. 10 tiles
+ * only re-block it).  Every candidate therefore reaches, up to rounding order,
+ * the plain product
+ *
+ *     R[b][i][j] = sum_{k=0}^{K-1} A[b][i][k] * B[b][k][j]
+ *
+ * and that definition is what this file evaluates: every product and every
+ * partial sum in fp64, k ascending, starting from 0.  fp32 and fp16 inputs
+ * convert to fp64 exactly, and the product of two such values is exact in fp64
+ * (at most 48 significand bits), so the only rounding is in the additions.
+ *
+ * Layout: row-major with leading dimensions (lda >= K, ldb >= N, ldr >= N) and
+ * batch strides in elements.  R is fp64.
+ *
+ * Loop order: each output row i is accumulated in place, k outer, j inner.
+ * For every single element this is the same k-ascending sum as the i-j-k
+ * triple loop, so the result is bit-identical to it and does not depend on the
+ * number of OpenMP threads (work is split over (b, i, column block) only).
+ */
+#include <stdint.h>
+#include <string.h>
+
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* IEEE 754 binary16 -> binary64, exact: 1 sign bit, 5 exponent bits (bias
+ * 15), 10 fraction bits; exponent 0 encodes zero/subnormals (no implicit 1,
+ * scale 2^-14), exponent 31 encodes inf/NaN. */
+double oracle_f16_to_f64(uint16_t h)
+{
+    const int sign = (h >> 15) & 1;
+    const int e = (h >> 10) & 0x1f;
+    const int f = h & 0x3ff;
+    double v;
+    if (e == 0) {
+        v = (double)f / 1024.0 / 16384.0; /* f * 2^-10 * 2^-14 */
+    } else if (e == 31) {
+        if (f == 0) {
+            v = 1.0 / 0.0;
+        } else {
+            uint64_t nan_bits = 0x7ff8000000000000ull;
+            memcpy(&v, &nan_bits, sizeof v);
+        }
+    } else {
+        v = 1.0 + (double)f / 1024.0;
+        int p = e - 15;
+        while (p > 0) { v *= 2.0; --p; }
+        while (p < 0) { v *= 0.5; ++p; }
+    }
+    return sign ? -v : v;
+}
+
+enum { ORACLE_F32 = 0, ORACLE_F16 = 1 };
+enum { COLS_PER_TASK = 512 };
+
+static inline double load_elt(const void *p, int64_t idx, int dtype)
+{
+    if (dtype == ORACLE_F32)
+        return (double)((const float *)p)[idx];
+    return oracle_f16_to_f64(((const uint16_t *)p)[idx]);
+}
+
+/* Batched product in fp64; see the file comment for the definition. */
+int oracle_matmul(int64_t batch, int64_t M, int64_t N, int64_t K,
+                  const void *A, int64_t lda, int64_t strideA,
+                  const void *B, int64_t ldb, int64_t strideB,
+                  double *R, int64_t ldr, int64_t strideR,
+                  int dtype, int nthreads)
+{
+    if (batch < 0 || M < 0 || N < 0 || K < 0)
+        return -1;
+    if (dtype != ORACLE_F32 && dtype != ORACLE_F16)
+        return -2;
+    if (batch == 0 || M == 0 || N == 0)
+        return 0;
+    if (lda < K || ldb < N || ldr < N)
+        return -1;
+
+    const int64_t col_tasks = (N + COLS_PER_TASK - 1) / COLS_PER_TASK;
+    const int64_t ntasks = batch * M * col_tasks;
+#ifdef _OPENMP
+    if (nthreads <= 0)
+        nthreads = omp_get_max_threads();
+#pragma omp parallel for schedule(dynamic, 1) num_threads(nthreads)
+#endif
+    for (int64_t t = 0; t < ntasks; ++t) {
+        const int64_t b = t / (M * col_tasks);
+        const int64_t i = (t / col_tasks) % M;
+        const int64_t j0 = (t % col_tasks) * COLS_PER_TASK;
+        const int64_t j1 = (j0 + COLS_PER_TASK < N) ? j0 + COLS_PER_TASK : N;
+        double *r = R + b * strideR + i * ldr;
+        for (int64_t j = j0; j < j1; ++j)
+            r[j] = 0.0;
+        for (int64_t k = 0; k < K; ++k) {
+            const double a = load_elt(A, b * strideA + i * lda + k, dtype);
+            const int64_t brow = b * strideB + k * ldb;
+            for (int64_t j = j0; j < j1; ++j)
+                r[j] += a * load_elt(B, brow + j, dtype);
+        }
+    }
+    (void)nthreads;
+    return 0;
+}
+
+/* One output element R[b][i][j], k ascending: the same sum oracle_matmul
+ * forms, for sampled checks at sizes where the full product is too slow. */
+double oracle_element(int64_t K, const void *A, int64_t a_off, const void *B,
+                      int64_t b_off, int64_t ldb, int dtype)
+{
+    double s = 0.0;
+    for (int64_t k = 0; k < K; ++k)
+        s += load_elt(A, a_off + k, dtype) * load_elt(B, b_off + k * ldb, dtype);
+    return s;
+}
+
+int oracle_max_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
