@@ -1,0 +1,212 @@
+/*
+ * nnjit.h -- C-ABI of the lite-space, per-shape tuned MatMul / BatchMatMul /
+ * GEMV library for MI355X (gfx950, CDNA4).
+ *
+ * The operation is the paper's MatMul and BatchMatMul (kernel table, Table 3:
+ * "MatMul M,K,N", "BatchMatMul B,M,K,N"): one kernel per operator shape that
+ * computes C = A . B.  Which kernel runs is picked from a small, resource-
+ * driven "lite" space of tiling configurations and tuned just in time per
+ * shape on the device (Sec. 5.2 and its Table 1 formulas and heuristics;
+ * candidates are measured on the device and the fastest is kept, Sec. 3).
+ *
+ * Conventions for every entry point below
+ *   - All matrices are row-major.  Element (i, j) of X lives at
+ *     X[i * ldx + j]; batch b of a batched operand starts at X + b * strideX
+ *     (strides and leading dimensions are in ELEMENTS, not bytes).
+ *   - C[i][j] = sum_k A[i][k] * B[k][j]; C is overwritten (no alpha/beta).
+ *   - Shapes are passed as (M, N, K): A is M x K, B is K x N, C is M x N.
+ *     (The paper writes shapes as [M, K, N]; the order here differs.)
+ *   - dtype NNJIT_F32: A, B, C are fp32; products are accumulated in fp32 on
+ *     the fp32 matrix cores (v_mfma_f32_*_f32), or in fp32 FMAs for GEMV.
+ *     dtype NNJIT_F16: A and B are IEEE binary16, C is fp32, accumulation is
+ *     fp32.
+ *   - A, B, C are DEVICE pointers owned by the caller; the library never
+ *     allocates, frees or retains them beyond the call.
+ *   - stream is a hipStream_t (NULL = the default stream).  Launches are
+ *     asynchronous on that stream; a fault inside a kernel surfaces at the
+ *     caller's next synchronisation, not as a return code.
+ *   - Preconditions: M, N, K >= 0 (and < 2^31); batch >= 0; lda >= max(1, K);
+ *     ldb >= max(1, N); ldc >= max(1, N); strides >= 0; a NULL pointer is
+ *     allowed only for an operand with no elements.  M == 0, N == 0 or
+ *     batch == 0 is a no-op that returns NNJIT_OK without touching the GPU;
+ *     K == 0 writes zeros to C.  Overlap between C and A/B, or between the C
+ *     slices of a batch, is the caller's error and is not detected.
+ *   - Arguments are validated before any HIP call, so a process without a GPU
+ *     gets an error code (NNJIT_EINVAL / NNJIT_EDTYPE for bad arguments,
+ *     NNJIT_EHIP otherwise), never an abort.
+ *   - Operands whose base pointers are not 16-byte aligned, or whose leading
+ *     dimensions, batch strides, K or N are not multiples of 16 bytes' worth
+ *     of elements, run on an element-load fallback configuration (correct,
+ *     slower); this is not an error.
+ *   - Thread safety: all entry points may be called from several host
+ *     threads.  Split-K scratch is kept per (device, stream), so concurrent
+ *     calls on different streams do not share it; calls on one stream are
+ *     ordered by the stream.
+ *   - Errors: a negative return code; nnjit_last_error() gives a message.
+ */
+#ifndef NNJIT_H
+#define NNJIT_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum nnjit_dtype { NNJIT_F32 = 0, NNJIT_F16 = 1 };
+
+/* Operator kinds: the key "t" (kernel type) of the paper's kernel database
+ * (Sec. 5.3).  GEMV is the M == 1, batch == 1 case of MatMul. */
+enum nnjit_kind { NNJIT_KIND_GEMM = 0, NNJIT_KIND_BATCHED = 1, NNJIT_KIND_GEMV = 2 };
+
+#define NNJIT_OK 0
+#define NNJIT_EINVAL (-1)  /* bad dimension, leading dim, stride, NULL pointer, config id */
+#define NNJIT_EDTYPE (-2)  /* dtype is not NNJIT_F32 / NNJIT_F16                         */
+#define NNJIT_ENOCFG (-3)  /* no configuration fits (not expected: fallbacks exist)      */
+#define NNJIT_EHIP (-4)    /* HIP runtime error, including "no GPU"                     */
+#define NNJIT_ENOMEM (-5)  /* device scratch allocation failed                           */
+
+/* C = A . B for one product (MatMul; GEMV when M == 1).  Uses the tuned
+ * configuration of this (kind, M, N, K, dtype) on the current device if
+ * nnjit_tune() ran for it, else the first configuration of the shape's lite
+ * space in evaluation order (the paper's predefined kernel that serves until
+ * just-in-time tuning finds a better one, Sec. 3).  Never tunes implicitly.
+ * Returns NNJIT_OK or a negative error code. */
+int nnjit_matmul(int64_t M, int64_t N, int64_t K,
+                 const void *A, int64_t lda,
+                 const void *B, int64_t ldb,
+                 void *C, int64_t ldc, int dtype, void *stream);
+
+/* C_b = A_b . B_b for b in [0, batch) (BatchMatMul, Table 3).  Operand b
+ * starts at A + b * strideA (elements), likewise B and C.  Same rules as
+ * nnjit_matmul; the tuned configuration is looked up under kind BATCHED
+ * (batch == 1 behaves exactly like nnjit_matmul). */
+int nnjit_batched_matmul(int64_t batch, int64_t M, int64_t N, int64_t K,
+                         const void *A, int64_t lda, int64_t strideA,
+                         const void *B, int64_t ldb, int64_t strideB,
+                         void *C, int64_t ldc, int64_t strideC,
+                         int dtype, void *stream);
+
+/* Just-in-time tuning of one shape (Sec. 3 JIT phase, Sec. 5.2 lite space):
+ * builds the shape's lite space (enumerate the compiled configurations of
+ * the kind and dtype, compute each one's Table 1 resource use on this
+ * device, prune by the heuristics, order by workgroups per CU, most first),
+ * times every survivor on device scratch of this exact shape (1 warm-up + 3
+ * timed launches, median; a candidate whose warm-up is more than 1.5x the
+ * best so far is dropped), keeps the fastest in the per-shape cache and
+ * returns its configuration id (>= 0).  Synchronous; uses its own stream and
+ * a library-owned scratch buffer.  Re-tuning a cached shape replaces the
+ * incumbent only if the new winner is at least 3% faster.  Wall time and
+ * counts: nnjit_last_tune_stats().  Negative return: error code. */
+int nnjit_tune(int64_t M, int64_t N, int64_t K, int dtype);
+
+/* As nnjit_tune, for BatchMatMul shapes (contiguous operands: strideA = M*K,
+ * strideB = K*N, strideC = M*N).  batch == 1 is nnjit_tune. */
+int nnjit_tune_batched(int64_t batch, int64_t M, int64_t N, int64_t K, int dtype);
+
+/* Run one forced configuration `cfg` (test and report helper): any kind's
+ * configuration may be forced as long as it belongs to this dtype; GEMV
+ * configurations additionally need batch == 1 and M == 1; a vector-load
+ * configuration needs the 16-byte alignment described above.  A mismatch is
+ * NNJIT_EINVAL. */
+int nnjit_matmul_config(int cfg, int64_t batch, int64_t M, int64_t N, int64_t K,
+                        const void *A, int64_t lda, int64_t strideA,
+                        const void *B, int64_t ldb, int64_t strideB,
+                        void *C, int64_t ldc, int64_t strideC,
+                        int dtype, void *stream);
+
+/* Number of configurations (ids are 0 .. n-1, fixed for a build). */
+int nnjit_num_configs(void);
+
+/* Writes a one-line description of configuration `cfg` into buf (at most
+ * len bytes including the terminating NUL), e.g.
+ * "id=12 family=gemm_f32 mfma=32x32x2 Mt=128 Nt=64 Kt=16 waves=2x2 stages=2
+ *  vec=16 split=4 threads=256 lds=...".  Returns the full length of the
+ * description, or NNJIT_EINVAL. */
+int nnjit_config_info(int cfg, char *buf, int64_t len);
+
+/* Device description used by the resource model (Table 1's hardware
+ * constants, mapped to one CDNA4 compute unit). */
+typedef struct nnjit_device_limits {
+    int num_cus;             /* compute units (MI355X: 256)                      */
+    int simds_per_cu;        /* 4                                                */
+    int vgprs_per_lane;      /* unified VGPR+AGPR file per SIMD lane (gfx950: 512) */
+    int vgpr_granule;        /* allocation granule (8)                           */
+    int max_waves_per_simd;  /* wave slots per SIMD (8)                          */
+    int wave_size;           /* 64                                               */
+    int64_t lds_per_cu;      /* bytes (gfx950: 163840)                           */
+    int64_t lds_per_wg;      /* bytes a workgroup may allocate (163840)          */
+    int max_threads_per_wg;  /* 1024                                             */
+} nnjit_device_limits;
+
+/* Table 1 quantities of one configuration on a device. */
+typedef struct nnjit_resources {
+    int regs_per_lane;   /* Reg_thread: VGPR+AGPR per lane (measured if available) */
+    int regs_measured;   /* 1 if regs_per_lane came from the compiled kernel      */
+    int64_t lds_per_wg;  /* L1_block: LDS bytes of one workgroup                  */
+    int threads_per_wg;  /* Thread_block                                         */
+    int waves_per_wg;    /* Warp_block                                           */
+    int reg_limit;       /* RegLimit:  workgroups per CU the register file allows */
+    int lds_limit;       /* L1Limit:   workgroups per CU the LDS allows           */
+    int wave_limit;      /* WarpLimit: workgroups per CU the wave slots allow     */
+    int wg_per_cu;       /* Block_core = min(RegLimit, L1Limit, WarpLimit)        */
+} nnjit_resources;
+
+/* Resource use of configuration `cfg` on `dev` (NULL: the current GPU, which
+ * also supplies the compiled kernel's measured register count).  Host-only
+ * when dev != NULL: no HIP call is made. */
+int nnjit_config_resources(int cfg, const nnjit_device_limits *dev, nnjit_resources *out);
+
+/* The lite space of a shape: writes up to `cap` configuration ids, in
+ * evaluation order, into `ids` and returns how many survive pruning (which
+ * may exceed cap).  *n_enumerated (if not NULL) receives the number of
+ * compiled configurations of the kind and dtype that were considered, and
+ * *n_naive the size of the unpruned space over the same parameter axes.
+ * With dev != NULL this is pure host code (no GPU needed) and uses estimated
+ * register counts; with dev == NULL it uses the current GPU's limits and the
+ * compiled kernels' measured registers, as nnjit_tune does. */
+int nnjit_lite_space(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K,
+                     const nnjit_device_limits *dev, int *ids, int cap,
+                     int *n_enumerated, int64_t *n_naive);
+
+/* Statistics of the last nnjit_tune / nnjit_tune_batched call on this thread. */
+typedef struct nnjit_tune_stats {
+    double wall_ms;       /* whole call, including scratch set-up and syncs       */
+    double eval_ms;       /* the candidate evaluation loop only                   */
+    int n_enumerated;     /* compiled configurations of the kind and dtype        */
+    int n_lite;           /* survivors of pruning (the lite space)               */
+    int n_timed;          /* candidates fully timed                              */
+    int n_aborted;        /* dropped after the warm-up (> 1.5x best)             */
+    int n_failed;         /* launch failures (skipped)                           */
+    int chosen;           /* configuration id returned                           */
+    double best_us;       /* its median time                                     */
+    double default_us;    /* median time of the first lite-space candidate        */
+    int cache_hit;        /* 1 if the shape was already tuned (nothing timed)     */
+} nnjit_tune_stats;
+
+int nnjit_last_tune_stats(nnjit_tune_stats *out);
+
+/* Best-so-far curve of the last tune on this thread: for the i-th evaluated
+ * candidate, its id, its median time in us (or -1 if aborted/failed) and the
+ * wall-clock ms since the start of the call.  Returns the number of entries
+ * (may exceed cap). */
+int nnjit_last_tune_trace(int *ids, double *us, double *at_ms, int cap);
+
+/* Configuration id cached for a shape on the current device, or NNJIT_ENOCFG. */
+int nnjit_cached_config(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K);
+
+/* Forget every tuned shape and release the tuner's scratch.  Returns NNJIT_OK. */
+int nnjit_cache_clear(void);
+
+/* Message for the last error on this thread ("" if none).  The pointer stays
+ * valid until the next nnjit_* call on the same thread. */
+const char *nnjit_last_error(void);
+
+/* Library version, (major << 16) | minor. */
+int nnjit_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NNJIT_H */

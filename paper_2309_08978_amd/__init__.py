@@ -1,0 +1,282 @@
+"""Python binding of libnnjit (include/nnjit.h): argument marshalling only.
+
+Every ``nnjit_*`` function here has the name and argument order of the C
+entry point it calls and returns its integer code unchanged; pointer
+arguments accept a ``torch.Tensor`` (its ``data_ptr()``), an int or None, and
+``stream`` accepts a ``torch.cuda.Stream``, an int handle or None.  All the
+work runs in the HIP library; if ``libnnjit.so`` is missing the binding
+raises instead of falling back to anything else.
+
+``matmul`` / ``batched_matmul`` are conveniences that take tensors, derive
+(M, N, K), leading dimensions and batch strides from them, call the entry
+point and raise ``NnjitError`` on a negative code.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+from typing import Optional
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libnnjit.so")
+
+NNJIT_F32, NNJIT_F16 = 0, 1
+NNJIT_KIND_GEMM, NNJIT_KIND_BATCHED, NNJIT_KIND_GEMV = 0, 1, 2
+NNJIT_OK, NNJIT_EINVAL, NNJIT_EDTYPE, NNJIT_ENOCFG, NNJIT_EHIP, NNJIT_ENOMEM = 0, -1, -2, -3, -4, -5
+ERROR_NAMES = {-1: "NNJIT_EINVAL", -2: "NNJIT_EDTYPE", -3: "NNJIT_ENOCFG", -4: "NNJIT_EHIP", -5: "NNJIT_ENOMEM"}
+
+EXPORTED = ["nnjit_matmul", "nnjit_batched_matmul", "nnjit_tune", "nnjit_tune_batched", "nnjit_matmul_config",
+            "nnjit_num_configs", "nnjit_config_info", "nnjit_config_resources", "nnjit_lite_space",
+            "nnjit_last_tune_stats", "nnjit_last_tune_trace", "nnjit_cached_config", "nnjit_cache_clear",
+            "nnjit_last_error", "nnjit_version"]
+
+
+class NnjitError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{ERROR_NAMES.get(code, code)}: {msg}")
+        self.code = code
+
+
+class DeviceLimits(ctypes.Structure):
+    _fields_ = [("num_cus", ctypes.c_int), ("simds_per_cu", ctypes.c_int), ("vgprs_per_lane", ctypes.c_int),
+                ("vgpr_granule", ctypes.c_int), ("max_waves_per_simd", ctypes.c_int), ("wave_size", ctypes.c_int),
+                ("lds_per_cu", ctypes.c_int64), ("lds_per_wg", ctypes.c_int64), ("max_threads_per_wg", ctypes.c_int)]
+
+
+class Resources(ctypes.Structure):
+    _fields_ = [("regs_per_lane", ctypes.c_int), ("regs_measured", ctypes.c_int), ("lds_per_wg", ctypes.c_int64),
+                ("threads_per_wg", ctypes.c_int), ("waves_per_wg", ctypes.c_int), ("reg_limit", ctypes.c_int),
+                ("lds_limit", ctypes.c_int), ("wave_limit", ctypes.c_int), ("wg_per_cu", ctypes.c_int)]
+
+
+class TuneStats(ctypes.Structure):
+    _fields_ = [("wall_ms", ctypes.c_double), ("eval_ms", ctypes.c_double), ("n_enumerated", ctypes.c_int),
+                ("n_lite", ctypes.c_int), ("n_timed", ctypes.c_int), ("n_aborted", ctypes.c_int),
+                ("n_failed", ctypes.c_int), ("chosen", ctypes.c_int), ("best_us", ctypes.c_double),
+                ("default_us", ctypes.c_double), ("cache_hit", ctypes.c_int)]
+
+
+def mi355x_limits() -> DeviceLimits:
+    """MI355X constants for the host-only resource model."""
+    return DeviceLimits(256, 4, 512, 8, 8, 64, 163840, 163840, 1024)
+
+
+_lock = threading.Lock()
+_lib = None
+
+
+def load(build_if_missing: bool = False) -> ctypes.CDLL:
+    """Load libnnjit.so (built in-tree by ``paper_2309_08978_amd.build``)."""
+    global _lib
+    with _lock:
+        if _lib is not None:
+            return _lib
+        if not os.path.exists(LIB_PATH):
+            if not build_if_missing:
+                raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2309_08978_amd.build`")
+            from . import build as _b
+            _b.build()
+        lib = ctypes.CDLL(LIB_PATH)
+        i64, vp, ci = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
+        sig = {
+            "nnjit_matmul": [i64, i64, i64, vp, i64, vp, i64, vp, i64, ci, vp],
+            "nnjit_batched_matmul": [i64, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64, i64, ci, vp],
+            "nnjit_tune": [i64, i64, i64, ci],
+            "nnjit_tune_batched": [i64, i64, i64, i64, ci],
+            "nnjit_matmul_config": [ci, i64, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64, i64, ci, vp],
+            "nnjit_num_configs": [],
+            "nnjit_config_info": [ci, ctypes.c_char_p, i64],
+            "nnjit_config_resources": [ci, ctypes.POINTER(DeviceLimits), ctypes.POINTER(Resources)],
+            "nnjit_lite_space": [ci, ci, i64, i64, i64, i64, ctypes.POINTER(DeviceLimits),
+                                 ctypes.POINTER(ci), ci, ctypes.POINTER(ci), ctypes.POINTER(i64)],
+            "nnjit_last_tune_stats": [ctypes.POINTER(TuneStats)],
+            "nnjit_last_tune_trace": [ctypes.POINTER(ci), ctypes.POINTER(ctypes.c_double),
+                                      ctypes.POINTER(ctypes.c_double), ci],
+            "nnjit_cached_config": [ci, ci, i64, i64, i64, i64],
+            "nnjit_cache_clear": [],
+            "nnjit_last_error": [],
+            "nnjit_version": [],
+        }
+        for name, args in sig.items():
+            f = getattr(lib, name)
+            f.argtypes = args
+            f.restype = ctypes.c_char_p if name == "nnjit_last_error" else ctypes.c_int
+        _lib = lib
+        return lib
+
+
+def _ptr(x) -> Optional[int]:
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return int(x.data_ptr())
+
+
+def _stream(s) -> Optional[int]:
+    if s is None:
+        return None
+    if isinstance(s, int):
+        return s
+    return int(s.cuda_stream)
+
+
+# ------------------------------------------------------ entry points (1:1)
+
+def nnjit_matmul(M, N, K, A, lda, B, ldb, C, ldc, dtype, stream=None) -> int:
+    return load().nnjit_matmul(M, N, K, _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc, dtype, _stream(stream))
+
+
+def nnjit_batched_matmul(batch, M, N, K, A, lda, strideA, B, ldb, strideB, C, ldc, strideC, dtype,
+                         stream=None) -> int:
+    return load().nnjit_batched_matmul(batch, M, N, K, _ptr(A), lda, strideA, _ptr(B), ldb, strideB,
+                                       _ptr(C), ldc, strideC, dtype, _stream(stream))
+
+
+def nnjit_tune(M, N, K, dtype) -> int:
+    return load().nnjit_tune(M, N, K, dtype)
+
+
+def nnjit_tune_batched(batch, M, N, K, dtype) -> int:
+    return load().nnjit_tune_batched(batch, M, N, K, dtype)
+
+
+def nnjit_matmul_config(cfg, batch, M, N, K, A, lda, strideA, B, ldb, strideB, C, ldc, strideC, dtype,
+                        stream=None) -> int:
+    return load().nnjit_matmul_config(cfg, batch, M, N, K, _ptr(A), lda, strideA, _ptr(B), ldb, strideB,
+                                      _ptr(C), ldc, strideC, dtype, _stream(stream))
+
+
+def nnjit_num_configs() -> int:
+    return load().nnjit_num_configs()
+
+
+def nnjit_config_info(cfg) -> str:
+    buf = ctypes.create_string_buffer(512)
+    rc = load().nnjit_config_info(cfg, buf, len(buf))
+    if rc < 0:
+        raise NnjitError(rc, nnjit_last_error())
+    return buf.value.decode()
+
+
+def nnjit_config_resources(cfg, dev: Optional[DeviceLimits] = None) -> dict:
+    out = Resources()
+    rc = load().nnjit_config_resources(cfg, ctypes.byref(dev) if dev is not None else None, ctypes.byref(out))
+    if rc < 0:
+        raise NnjitError(rc, nnjit_last_error())
+    return {f: getattr(out, f) for f, _ in Resources._fields_}
+
+
+def nnjit_lite_space(kind, dtype, batch, M, N, K, dev: Optional[DeviceLimits] = None, cap: int = 4096):
+    """-> (ids in evaluation order, n_surviving, n_enumerated, n_naive)."""
+    ids = (ctypes.c_int * cap)()
+    n_enum = ctypes.c_int(0)
+    n_naive = ctypes.c_int64(0)
+    rc = load().nnjit_lite_space(kind, dtype, batch, M, N, K, ctypes.byref(dev) if dev is not None else None,
+                                 ids, cap, ctypes.byref(n_enum), ctypes.byref(n_naive))
+    if rc < 0:
+        raise NnjitError(rc, nnjit_last_error())
+    return list(ids[:min(rc, cap)]), rc, n_enum.value, n_naive.value
+
+
+def nnjit_last_tune_stats() -> dict:
+    st = TuneStats()
+    load().nnjit_last_tune_stats(ctypes.byref(st))
+    return {f: getattr(st, f) for f, _ in TuneStats._fields_}
+
+
+def nnjit_last_tune_trace(cap: int = 256):
+    ids = (ctypes.c_int * cap)()
+    us = (ctypes.c_double * cap)()
+    at = (ctypes.c_double * cap)()
+    n = load().nnjit_last_tune_trace(ids, us, at, cap)
+    return [(ids[i], us[i], at[i]) for i in range(min(n, cap))]
+
+
+def nnjit_cached_config(kind, dtype, batch, M, N, K) -> int:
+    return load().nnjit_cached_config(kind, dtype, batch, M, N, K)
+
+
+def nnjit_cache_clear() -> int:
+    return load().nnjit_cache_clear()
+
+
+def nnjit_last_error() -> str:
+    r = load().nnjit_last_error()
+    return r.decode() if r else ""
+
+
+def nnjit_version() -> int:
+    return load().nnjit_version()
+
+
+# ------------------------------------------------------------ conveniences
+
+def dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.float32:
+        return NNJIT_F32
+    if t.dtype == torch.float16:
+        return NNJIT_F16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def check(rc: int) -> int:
+    if rc < 0:
+        raise NnjitError(rc, nnjit_last_error())
+    return rc
+
+
+def _ld(t) -> int:
+    # leading dimension of a row-major 2-D view (unit column stride required)
+    if t.stride(-1) != 1 and t.shape[-1] > 1:
+        raise ValueError("operands must have unit stride along the last dimension")
+    return max(int(t.stride(-2)), int(t.shape[-1]), 1)
+
+
+def matmul(A, B, C=None, stream=None, cfg: Optional[int] = None):
+    """C = A . B for 2-D fp32/fp16 CUDA tensors (C fp32, allocated if None)."""
+    import torch
+    M, K = A.shape
+    K2, N = B.shape
+    if K2 != K:
+        raise ValueError(f"inner dimensions differ: {tuple(A.shape)} . {tuple(B.shape)}")
+    if C is None:
+        C = torch.empty((M, N), dtype=torch.float32, device=A.device)
+    dt = dtype_code(A)
+    if cfg is None:
+        check(nnjit_matmul(M, N, K, A, _ld(A), B, _ld(B), C, _ld(C), dt, stream))
+    else:
+        check(nnjit_matmul_config(cfg, 1, M, N, K, A, _ld(A), 0, B, _ld(B), 0, C, _ld(C), 0, dt, stream))
+    return C
+
+
+def batched_matmul(A, B, C=None, stream=None, cfg: Optional[int] = None):
+    """C[b] = A[b] . B[b] for 3-D fp32/fp16 CUDA tensors (C fp32)."""
+    import torch
+    batch, M, K = A.shape
+    _, K2, N = B.shape
+    if K2 != K or B.shape[0] != batch:
+        raise ValueError(f"shape mismatch {tuple(A.shape)} . {tuple(B.shape)}")
+    if C is None:
+        C = torch.empty((batch, M, N), dtype=torch.float32, device=A.device)
+    dt = dtype_code(A)
+    sA, sB, sC = (int(t.stride(0)) for t in (A, B, C))
+    if cfg is None:
+        check(nnjit_batched_matmul(batch, M, N, K, A, _ld(A), sA, B, _ld(B), sB, C, _ld(C), sC, dt, stream))
+    else:
+        check(nnjit_matmul_config(cfg, batch, M, N, K, A, _ld(A), sA, B, _ld(B), sB, C, _ld(C), sC, dt, stream))
+    return C
+
+
+def configs() -> list:
+    """Descriptions of every configuration id."""
+    out = []
+    for i in range(nnjit_num_configs()):
+        d = {}
+        for kv in nnjit_config_info(i).split():
+            k, v = kv.split("=", 1)
+            d[k] = int(v) if v.lstrip("-").isdigit() else v
+        out.append(d)
+    return out

@@ -1,0 +1,320 @@
+// fp16-input / fp32-accumulate MatMul / BatchMatMul on the gfx950 matrix
+// cores (v_mfma_f32_32x32x16_f16, v_mfma_f32_16x16x32_f16).  C is fp32.
+//
+// Same tile hierarchy as the fp32 kernels (Fig. 10, Table 1 of the paper):
+// an Mt x Nt tile per workgroup, a 64-deep K slab staged through LDS, wave
+// sub-tiles in accumulator registers, unrolled inner loop, 128-bit loads.
+//
+// The matrix cores want both operands K-contiguous per lane (8 halves = one
+// 128-bit register quad).  A (row-major M x K) already is; B (row-major
+// K x N) is transposed on its way into LDS: each thread loads an 8 x 8 block
+// of B (eight 128-bit rows), transposes it in registers and stores eight
+// 128-bit columns.  Both LDS slabs are [row][8 chunks of 16 bytes] with the
+// chunk index XOR-swizzled by (row & 7), which keeps the 128-bit LDS reads
+// of the fragments and the 128-bit stores of the loaders free of bank
+// conflicts without padding.
+#include "kcommon.h"
+
+namespace nnjit {
+
+template <int MF> struct Mfma16;
+template <> struct Mfma16<32> {
+    typedef f32x16 acc_t;
+    static constexpr int NR = 16;
+    __device__ static __forceinline__ acc_t mma(f16x8 a, f16x8 b, acc_t c) {
+        return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+    }
+    __device__ static __forceinline__ int row_of(int r, int g) { return 8 * (r >> 2) + 4 * g + (r & 3); }
+};
+template <> struct Mfma16<16> {
+    typedef f32x4 acc_t;
+    static constexpr int NR = 4;
+    __device__ static __forceinline__ acc_t mma(f16x8 a, f16x8 b, acc_t c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+    }
+    __device__ static __forceinline__ int row_of(int r, int g) { return 4 * g + r; }
+};
+
+// Low (even) or high (odd) halves of two dwords, packed low | high << 16.
+__device__ __forceinline__ unsigned pack_lo(unsigned a, unsigned b) { return (a & 0xffffu) | (b << 16); }
+__device__ __forceinline__ unsigned pack_hi(unsigned a, unsigned b) { return (a >> 16) | (b & 0xffff0000u); }
+
+template <int MT, int NT, int WM, int WN, int MF, int ST, bool VEC>
+__global__ void __launch_bounds__(WM * WN * 64)
+gemm_f16_kernel(GemmParams p)
+{
+    typedef Mfma16<MF> I;
+    typedef typename I::acc_t acc_t;
+    constexpr int KT = 64;
+    constexpr int NTHR = WM * WN * 64;
+    constexpr int WTM = MT / WM, WTN = NT / WN;
+    constexpr int FM = WTM / MF, FN = WTN / MF;
+    constexpr int A8 = MT * (KT / 8);          // 16-byte chunks of the A slab
+    constexpr int BB = (KT / 8) * (NT / 8);    // 8x8 blocks of the B slab
+    constexpr int LA = (A8 + NTHR - 1) / NTHR;
+    constexpr int LB = (BB + NTHR - 1) / NTHR;
+    constexpr int KG = 64 / MF;                // lane groups along k (2 or 4)
+    constexpr int NSTEP = KT / (8 * KG);       // instructions per slab and fragment pair
+    static_assert(FM >= 1 && FN >= 1 && WTM % MF == 0 && WTN % MF == 0, "wave tile");
+    static_assert(MT * NT == NTHR * FM * FN * I::NR, "tile / accumulator count");
+
+    __shared__ u32x4 As[ST][MT * 8];
+    __shared__ u32x4 Bt[ST][NT * 8];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / WN, wn = wave % WN;
+    const int li = lane % MF, lg = lane / MF;
+
+    const int tiles = p.tiles_m * p.tiles_n;
+    const int gx = gridDim.x;
+    const int logical = xcd_remap(blockIdx.x + gx * blockIdx.z, gx * gridDim.z);
+    const int z = logical / gx;
+    const int rest = logical - z * gx;
+    const int s = rest / tiles;
+    const int tile = rest - s * tiles;
+    const int tm = tile % p.tiles_m, tn = tile / p.tiles_m;
+    const int m0 = tm * MT, n0 = tn * NT;
+    const int kbeg = s * p.kchunk;
+    const int kend = min(p.K, kbeg + p.kchunk);
+    const int nk = kend > kbeg ? (kend - kbeg + KT - 1) / KT : 0;
+
+    const unsigned short *A = (const unsigned short *)p.A + (long long)z * p.sA;
+    const unsigned short *B = (const unsigned short *)p.B + (long long)z * p.sB;
+    float *C = p.C + (long long)z * p.sC;
+    const int M = p.M, N = p.N;
+    const long long lda = p.lda, ldb = p.ldb;
+
+    u32x4 ra[LA];
+    u32x4 rb[LB][8];
+
+    auto ld8 = [&](const unsigned short *src, int nvalid) -> u32x4 {
+        // 8 halves from src; elements at or beyond nvalid read as +0
+        u32x4 v = {0u, 0u, 0u, 0u};
+        if constexpr (VEC) {
+            if (nvalid >= 8) v = *(const u32x4 *)src;
+        } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                if (e < nvalid) v[e >> 1] |= (unsigned)src[e] << (16 * (e & 1));
+        }
+        return v;
+    };
+
+    auto gload = [&](int k0) {
+#pragma unroll
+        for (int l = 0; l < LA; ++l) {
+            const int f = tid + l * NTHR;
+            const int row = f >> 3, c = f & 7;
+            const int gm = m0 + row, gk = k0 + 8 * c;
+            u32x4 v = {0u, 0u, 0u, 0u};
+            if ((A8 % NTHR == 0 || f < A8) && gm < M && gk < kend)
+                v = ld8(A + (long long)gm * lda + gk, kend - gk);
+            ra[l] = v;
+        }
+#pragma unroll
+        for (int l = 0; l < LB; ++l) {
+            const int f = tid + l * NTHR;
+            const int kb = f & 7, nb = f >> 3;
+            const int gn = n0 + 8 * nb;
+#pragma unroll
+            for (int r = 0; r < 8; ++r) {
+                const int gk = k0 + 8 * kb + r;
+                u32x4 v = {0u, 0u, 0u, 0u};
+                if ((BB % NTHR == 0 || f < BB) && gk < kend && gn < N)
+                    v = ld8(B + (long long)gk * ldb + gn, N - gn);
+                rb[l][r] = v;
+            }
+        }
+    };
+
+    auto sstore = [&](int buf) {
+#pragma unroll
+        for (int l = 0; l < LA; ++l) {
+            const int f = tid + l * NTHR;
+            if (A8 % NTHR == 0 || f < A8) {
+                const int row = f >> 3, c = f & 7;
+                As[buf][row * 8 + (c ^ (row & 7))] = ra[l];
+            }
+        }
+#pragma unroll
+        for (int l = 0; l < LB; ++l) {
+            const int f = tid + l * NTHR;
+            if (BB % NTHR == 0 || f < BB) {
+                const int kb = f & 7, nb = f >> 3;
+                // column c of the 8x8 block: halves k = 0..7 of column n = 8*nb + c
+#pragma unroll
+                for (int c = 0; c < 8; ++c) {
+                    const int d = c >> 1;
+                    u32x4 o;
+#pragma unroll
+                    for (int w = 0; w < 4; ++w)
+                        o[w] = (c & 1) ? pack_hi(rb[l][2 * w][d], rb[l][2 * w + 1][d])
+                                       : pack_lo(rb[l][2 * w][d], rb[l][2 * w + 1][d]);
+                    const int n = 8 * nb + c;
+                    Bt[buf][n * 8 + (kb ^ c)] = o;  // (n & 7) == c
+                }
+            }
+        }
+    };
+
+    acc_t acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int r = 0; r < I::NR; ++r) acc[i][j][r] = 0.f;
+
+    auto compute = [&](int buf) {
+#pragma unroll
+        for (int st = 0; st < NSTEP; ++st) {
+            const int chunk = st * KG + lg;   // k in [8*chunk, 8*chunk + 8)
+            f16x8 a[FM], b[FN];
+#pragma unroll
+            for (int i = 0; i < FM; ++i) {
+                const int row = wm * WTM + i * MF + li;
+                a[i] = __builtin_bit_cast(f16x8, As[buf][row * 8 + (chunk ^ (row & 7))]);
+            }
+#pragma unroll
+            for (int j = 0; j < FN; ++j) {
+                const int col = wn * WTN + j * MF + li;
+                b[j] = __builtin_bit_cast(f16x8, Bt[buf][col * 8 + (chunk ^ (col & 7))]);
+            }
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j) acc[i][j] = I::mma(a[i], b[j], acc[i][j]);
+        }
+    };
+
+    if constexpr (ST == 2) {
+        if (nk > 0) {
+            gload(kbeg);
+            sstore(0);
+        }
+        __syncthreads();
+        for (int it = 0; it < nk; ++it) {
+            const int cur = it & 1;
+            if (it + 1 < nk) gload(kbeg + (it + 1) * KT);
+            compute(cur);
+            if (it + 1 < nk) sstore(cur ^ 1);
+            __syncthreads();
+        }
+    } else {
+        if (nk > 0) gload(kbeg);
+        for (int it = 0; it < nk; ++it) {
+            __syncthreads();
+            sstore(0);
+            __syncthreads();
+            if (it + 1 < nk) gload(kbeg + (it + 1) * KT);
+            compute(0);
+        }
+    }
+
+    const int rbase = m0 + wm * WTM, cbase = n0 + wn * WTN + li;
+    if (p.S == 1) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int r = 0; r < I::NR; ++r) {
+                    const int row = rbase + i * MF + I::row_of(r, lg), col = cbase + j * MF;
+                    if (row < M && col < N) C[(long long)row * p.ldc + col] = acc[i][j][r];
+                }
+        return;
+    }
+
+    const long long tile_id = (long long)z * tiles + tile;
+    float *part = p.ws + (tile_id * p.S + s) * (long long)(MT * NT);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int r = 0; r < I::NR; ++r)
+                part[((i * FN + j) * I::NR + r) * NTHR + tid] = acc[i][j][r];
+    if (!splitk_arrive_last(&p.counters[tile_id], p.S)) return;
+    const float *base = p.ws + tile_id * p.S * (long long)(MT * NT);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int r = 0; r < I::NR; ++r) {
+                const int idx = ((i * FN + j) * I::NR + r) * NTHR + tid;
+                float v = 0.f;
+                for (int t = 0; t < p.S; ++t) {
+                    const float x = (t == s) ? acc[i][j][r] : base[(long long)t * (MT * NT) + idx];
+                    v = (t == 0) ? x : v + x;
+                }
+                const int row = rbase + i * MF + I::row_of(r, lg), col = cbase + j * MF;
+                if (row < M && col < N) C[(long long)row * p.ldc + col] = v;
+            }
+    if (tid == 0) p.counters[tile_id] = 0u;
+}
+
+template <int MT, int NT, int WM, int WN, int MF, int ST, bool VEC>
+static hipError_t launch_gemm_f16(const void *params, dim3 grid, hipStream_t stream)
+{
+    hipLaunchKernelGGL((gemm_f16_kernel<MT, NT, WM, WN, MF, ST, VEC>), grid, dim3(WM * WN * 64), 0, stream,
+                       *(const GemmParams *)params);
+    return hipGetLastError();
+}
+
+// Table 1 register formula for one lane (see est_regs_f32): accumulators,
+// one K step of A and B fragments (4 VGPRs per 8 halves), the staging
+// registers of the global->LDS copy (B needs eight 128-bit rows per 8x8
+// block), and a fixed overhead.
+constexpr int est_regs_f16(int mt, int nt, int wm, int wn, int mf) {
+    return (mt / wm) * (nt / wn) / 64 + 4 * ((mt / wm) / mf) + 4 * ((nt / wn) / mf) +
+           4 * ((mt * 8 + wm * wn * 64 - 1) / (wm * wn * 64)) +
+           32 * ((nt + wm * wn * 64 - 1) / (wm * wn * 64)) + 28;
+}
+constexpr int lds_f16(int mt, int nt, int st) { return st * (mt + nt) * 128; }
+
+#define NNJIT_F16_VARIANT(MT, NT, WM, WN, MF, ST, VEC)                                                      \
+    {"gemm_f16_" #MT "x" #NT "x64_w" #WM "x" #WN "_m" #MF "_s" #ST "_v" #VEC, FAM_GEMM_F16, MF,                \
+     (MF == 32 ? 16 : 32), MT, NT, 64, WM, WN, ST, (VEC ? 16 : 2), 0, 0, WM * WN * 64, lds_f16(MT, NT, ST),   \
+     est_regs_f16(MT, NT, WM, WN, MF), (const void *)&gemm_f16_kernel<MT, NT, WM, WN, MF, ST, VEC>,         \
+     &launch_gemm_f16<MT, NT, WM, WN, MF, ST, VEC>}
+
+// The compiled fp16 configurations (K slab fixed at 64: 128-byte rows).
+#define NNJIT_F16_LIST(X) \
+    X(256, 256, 2, 2, 32, 2, true) \
+    X(256, 128, 2, 2, 32, 2, true) \
+    X(128, 256, 2, 2, 32, 2, true) \
+    X(256, 128, 4, 2, 32, 2, true) \
+    X(128, 256, 2, 4, 32, 2, true) \
+    X(128, 128, 2, 2, 32, 2, true) \
+    X(128, 128, 1, 2, 32, 2, true) \
+    X(128, 128, 2, 1, 32, 2, true) \
+    X(128, 128, 2, 2, 16, 2, true) \
+    X(128, 128, 2, 2, 32, 1, true) \
+    X(128, 64, 2, 1, 32, 2, true) \
+    X(128, 64, 2, 2, 32, 2, true) \
+    X(64, 128, 1, 2, 32, 2, true) \
+    X(64, 128, 2, 2, 32, 2, true) \
+    X(64, 64, 1, 1, 32, 2, true) \
+    X(64, 64, 2, 2, 32, 2, true) \
+    X(64, 64, 2, 2, 16, 2, true) \
+    X(32, 64, 1, 2, 32, 2, true) \
+    X(64, 32, 2, 1, 32, 2, true) \
+    X(32, 32, 1, 1, 32, 2, true) \
+    X(32, 32, 2, 2, 16, 2, true) \
+    X(16, 64, 1, 4, 16, 2, true) \
+    X(64, 64, 2, 2, 32, 2, false) \
+    X(32, 32, 1, 1, 32, 2, false) \
+
+#define NNJIT_F16_INST(MT, NT, WM, WN, MF, ST, VEC) \
+    template __global__ void gemm_f16_kernel<MT, NT, WM, WN, MF, ST, VEC>(GemmParams);
+NNJIT_F16_LIST(NNJIT_F16_INST)
+
+#if !defined(__HIP_DEVICE_COMPILE__)
+#define NNJIT_F16_ENTRY(...) NNJIT_F16_VARIANT(__VA_ARGS__),
+const Variant kGemmF16Variants[] = {NNJIT_F16_LIST(NNJIT_F16_ENTRY)};
+const int kNumGemmF16Variants = sizeof(kGemmF16Variants) / sizeof(kGemmF16Variants[0]);
+#endif
+
+}  // namespace nnjit

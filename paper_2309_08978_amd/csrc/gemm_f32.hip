@@ -1,0 +1,323 @@
+// fp32 MatMul / BatchMatMul on the fp32 matrix cores of gfx950.
+//
+// One workgroup computes an Mt x Nt tile of C for one split of K and one
+// batch slice.  This is the paper's tile hierarchy (Fig. 10, Table 1): the
+// block tile (x1, y1, r1) = (Nt, Mt, Kt) is staged through LDS (the
+// "cache_read" primitive of Table 2), each wave owns a (Mt/WM) x (Nt/WN)
+// sub-tile held in accumulator registers (the thread tile; "cache_write": C
+// is written once, at the end), and the inner loop over the slab is fully
+// unrolled (the "unroll" primitive).  Global loads are 128-bit (heuristic 1).
+//
+// Matrix-core instructions (operands are per lane of a 64-lane wave):
+//   v_mfma_f32_32x32x2_f32:  lane l holds A[i][k], B[k][j] with i = j = l % 32,
+//                            k = l / 32; D[i][j] is register 8*(i/8)... see
+//                            row_of() below.
+//   v_mfma_f32_16x16x4_f32:  i = j = l % 16, k = l / 16.
+// Only the pairing of A and B k-slots matters for the product, so lane group
+// g takes the K-slab's k in [g*KL, (g+1)*KL) one per instruction; A values
+// of a lane are then contiguous in LDS and are read 128 bits at a time.
+#include "kcommon.h"
+
+namespace nnjit {
+
+template <int MF> struct Mfma32;
+template <> struct Mfma32<32> {
+    typedef f32x16 acc_t;
+    static constexpr int NR = 16;
+    __device__ static __forceinline__ acc_t mma(float a, float b, acc_t c) {
+        return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+    }
+    // row of accumulator register r of a lane in lane group g (column = l % 32)
+    __device__ static __forceinline__ int row_of(int r, int g) { return 8 * (r >> 2) + 4 * g + (r & 3); }
+};
+template <> struct Mfma32<16> {
+    typedef f32x4 acc_t;
+    static constexpr int NR = 4;
+    __device__ static __forceinline__ acc_t mma(float a, float b, acc_t c) {
+        return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+    }
+    __device__ static __forceinline__ int row_of(int r, int g) { return 4 * g + r; }
+};
+
+template <int MT, int NT, int KT, int WM, int WN, int MF, int ST, bool VEC>
+__global__ void __launch_bounds__(WM * WN * 64)
+gemm_f32_kernel(GemmParams p)
+{
+    typedef Mfma32<MF> I;
+    typedef typename I::acc_t acc_t;
+    constexpr int NTHR = WM * WN * 64;
+    constexpr int WTM = MT / WM, WTN = NT / WN;
+    constexpr int FM = WTM / MF, FN = WTN / MF;
+    constexpr int SA = KT + 4;           // LDS row stride of the A slab (floats)
+    constexpr int SB = NT + 4;           // LDS row stride of the B slab (floats)
+    constexpr int A4 = MT * KT / 4;      // 16-byte chunks of one A slab
+    constexpr int B4 = KT * NT / 4;
+    constexpr int LA = (A4 + NTHR - 1) / NTHR;
+    constexpr int LB = (B4 + NTHR - 1) / NTHR;
+    constexpr int KG = 64 / MF;          // lane groups along k
+    constexpr int KL = KT / KG;          // k values of one lane group per slab
+    static_assert(FM >= 1 && FN >= 1 && WTM % MF == 0 && WTN % MF == 0, "wave tile");
+    static_assert(KL % 4 == 0, "K-slab too small for 128-bit LDS reads");
+    static_assert(MT * NT == NTHR * FM * FN * I::NR, "tile / accumulator count");
+
+    __shared__ __attribute__((aligned(16))) float As[ST][MT * SA];
+    __shared__ __attribute__((aligned(16))) float Bs[ST][KT * SB];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / WN, wn = wave % WN;
+    const int li = lane % MF, lg = lane / MF;
+
+    // workgroup -> (batch z, split s, tile)
+    const int tiles = p.tiles_m * p.tiles_n;
+    const int gx = gridDim.x;
+    const int logical = xcd_remap(blockIdx.x + gx * blockIdx.z, gx * gridDim.z);
+    const int z = logical / gx;
+    const int rest = logical - z * gx;
+    const int s = rest / tiles;
+    const int tile = rest - s * tiles;
+    const int tm = tile % p.tiles_m, tn = tile / p.tiles_m;
+    const int m0 = tm * MT, n0 = tn * NT;
+    const int kbeg = s * p.kchunk;
+    const int kend = min(p.K, kbeg + p.kchunk);
+    const int nk = kend > kbeg ? (kend - kbeg + KT - 1) / KT : 0;
+
+    const float *A = (const float *)p.A + (long long)z * p.sA;
+    const float *B = (const float *)p.B + (long long)z * p.sB;
+    float *C = p.C + (long long)z * p.sC;
+    const int M = p.M, N = p.N;
+    const long long lda = p.lda, ldb = p.ldb;
+
+    f32x4 ra[LA], rb[LB];
+
+    auto gload = [&](int k0) {
+#pragma unroll
+        for (int l = 0; l < LA; ++l) {
+            const int f = tid + l * NTHR;
+            const int row = f / (KT / 4), c4 = f % (KT / 4);
+            const int gm = m0 + row, gk = k0 + c4 * 4;
+            f32x4 v = {0.f, 0.f, 0.f, 0.f};
+            if ((A4 % NTHR == 0 || f < A4) && gm < M) {
+                const float *src = A + (long long)gm * lda + gk;
+                if constexpr (VEC) {
+                    if (gk < kend) v = *(const f32x4 *)src;
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (gk + e < kend) v[e] = src[e];
+                }
+            }
+            ra[l] = v;
+        }
+#pragma unroll
+        for (int l = 0; l < LB; ++l) {
+            const int f = tid + l * NTHR;
+            const int row = f / (NT / 4), c4 = f % (NT / 4);
+            const int gk = k0 + row, gn = n0 + c4 * 4;
+            f32x4 v = {0.f, 0.f, 0.f, 0.f};
+            if ((B4 % NTHR == 0 || f < B4) && gk < kend) {
+                const float *src = B + (long long)gk * ldb + gn;
+                if constexpr (VEC) {
+                    if (gn < N) v = *(const f32x4 *)src;
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (gn + e < N) v[e] = src[e];
+                }
+            }
+            rb[l] = v;
+        }
+    };
+
+    auto sstore = [&](int buf) {
+#pragma unroll
+        for (int l = 0; l < LA; ++l) {
+            const int f = tid + l * NTHR;
+            if (A4 % NTHR == 0 || f < A4) {
+                const int row = f / (KT / 4), c4 = f % (KT / 4);
+                *(f32x4 *)&As[buf][row * SA + c4 * 4] = ra[l];
+            }
+        }
+#pragma unroll
+        for (int l = 0; l < LB; ++l) {
+            const int f = tid + l * NTHR;
+            if (B4 % NTHR == 0 || f < B4) {
+                const int row = f / (NT / 4), c4 = f % (NT / 4);
+                *(f32x4 *)&Bs[buf][row * SB + c4 * 4] = rb[l];
+            }
+        }
+    };
+
+    acc_t acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int r = 0; r < I::NR; ++r) acc[i][j][r] = 0.f;
+
+    auto compute = [&](int buf) {
+        const float *as = &As[buf][(wm * WTM + li) * SA + lg * KL];
+        const float *bs = &Bs[buf][(lg * KL) * SB + wn * WTN + li];
+#pragma unroll
+        for (int q = 0; q < KL / 4; ++q) {
+            f32x4 a[FM];
+#pragma unroll
+            for (int i = 0; i < FM; ++i) a[i] = *(const f32x4 *)&as[i * MF * SA + 4 * q];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                float b[FN];
+#pragma unroll
+                for (int j = 0; j < FN; ++j) b[j] = bs[(4 * q + e) * SB + j * MF];
+#pragma unroll
+                for (int i = 0; i < FM; ++i)
+#pragma unroll
+                    for (int j = 0; j < FN; ++j) acc[i][j] = I::mma(a[i][e], b[j], acc[i][j]);
+            }
+        }
+    };
+
+    if constexpr (ST == 2) {
+        if (nk > 0) {
+            gload(kbeg);
+            sstore(0);
+        }
+        __syncthreads();
+        for (int it = 0; it < nk; ++it) {
+            const int cur = it & 1;
+            if (it + 1 < nk) gload(kbeg + (it + 1) * KT);
+            compute(cur);
+            if (it + 1 < nk) sstore(cur ^ 1);
+            __syncthreads();
+        }
+    } else {
+        if (nk > 0) gload(kbeg);
+        for (int it = 0; it < nk; ++it) {
+            __syncthreads();
+            sstore(0);
+            __syncthreads();
+            if (it + 1 < nk) gload(kbeg + (it + 1) * KT);
+            compute(0);
+        }
+    }
+
+    const int rbase = m0 + wm * WTM, cbase = n0 + wn * WTN + li;
+    if (p.S == 1) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int r = 0; r < I::NR; ++r) {
+                    const int row = rbase + i * MF + I::row_of(r, lg), col = cbase + j * MF;
+                    if (row < M && col < N) C[(long long)row * p.ldc + col] = acc[i][j][r];
+                }
+        return;
+    }
+
+    // split-K: store the partial tile (coalesced, one register index per
+    // 64-lane row), the last arriving split sums all partials in split order.
+    const long long tile_id = (long long)z * tiles + tile;
+    float *part = p.ws + (tile_id * p.S + s) * (long long)(MT * NT);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int r = 0; r < I::NR; ++r)
+                part[((i * FN + j) * I::NR + r) * NTHR + tid] = acc[i][j][r];
+    if (!splitk_arrive_last(&p.counters[tile_id], p.S)) return;
+    const float *base = p.ws + tile_id * p.S * (long long)(MT * NT);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int r = 0; r < I::NR; ++r) {
+                const int idx = ((i * FN + j) * I::NR + r) * NTHR + tid;
+                float v = 0.f;
+                for (int t = 0; t < p.S; ++t) {
+                    const float x = (t == s) ? acc[i][j][r] : base[(long long)t * (MT * NT) + idx];
+                    v = (t == 0) ? x : v + x;
+                }
+                const int row = rbase + i * MF + I::row_of(r, lg), col = cbase + j * MF;
+                if (row < M && col < N) C[(long long)row * p.ldc + col] = v;
+            }
+    if (tid == 0) p.counters[tile_id] = 0u;
+}
+
+template <int MT, int NT, int KT, int WM, int WN, int MF, int ST, bool VEC>
+static hipError_t launch_gemm_f32(const void *params, dim3 grid, hipStream_t stream)
+{
+    hipLaunchKernelGGL((gemm_f32_kernel<MT, NT, KT, WM, WN, MF, ST, VEC>), grid, dim3(WM * WN * 64), 0,
+                       stream, *(const GemmParams *)params);
+    return hipGetLastError();
+}
+
+// Register estimate of the Table 1 formula Reg_thread = x0*r0 + r0*y0 + x0*y0
+// for one lane: the accumulator tile (x0*y0 over 64 lanes), the A and B
+// fragments of one K step (r0*y0, r0*x0), the global->LDS staging registers,
+// and a fixed overhead for addresses and indices.
+constexpr int est_regs_f32(int mt, int nt, int kt, int wm, int wn, int mf) {
+    return (mt / wm) * (nt / wn) / 64 + 4 * ((mt / wm) / mf) + ((nt / wn) / mf) +
+           (mt * kt + kt * nt) / (wm * wn * 64) + 28;
+}
+constexpr int lds_f32(int mt, int nt, int kt, int st) { return st * (mt * (kt + 4) + kt * (nt + 4)) * 4; }
+
+#define NNJIT_F32_VARIANT(MT, NT, KT, WM, WN, MF, ST, VEC)                                              \
+    {"gemm_f32_" #MT "x" #NT "x" #KT "_w" #WM "x" #WN "_m" #MF "_s" #ST "_v" #VEC, FAM_GEMM_F32, MF,         \
+     (MF == 32 ? 2 : 4), MT, NT, KT, WM, WN, ST, (VEC ? 16 : 4), 0, 0, WM * WN * 64, lds_f32(MT, NT, KT, ST), \
+     est_regs_f32(MT, NT, KT, WM, WN, MF),                                                              \
+     (const void *)&gemm_f32_kernel<MT, NT, KT, WM, WN, MF, ST, VEC>,                                   \
+     &launch_gemm_f32<MT, NT, KT, WM, WN, MF, ST, VEC>}
+
+// The compiled fp32 configurations (the family's full set; the lite space of
+// a shape is a pruned, ordered subset).  Tile edges are powers of two
+// (heuristic 2).  The last entries load element by element, for operands
+// that are not 16-byte aligned.
+#define NNJIT_F32_LIST(X) \
+    X(256, 128, 16, 2, 2, 32, 2, true) \
+    X(128, 256, 16, 2, 2, 32, 2, true) \
+    X(256, 256, 16, 2, 2, 32, 2, true) \
+    X(256, 128, 16, 4, 2, 32, 2, true) \
+    X(128, 128, 16, 2, 2, 32, 2, true) \
+    X(128, 128, 32, 2, 2, 32, 2, true) \
+    X(128, 128, 16, 2, 2, 32, 1, true) \
+    X(128, 128, 16, 1, 2, 32, 2, true) \
+    X(128, 64, 16, 2, 1, 32, 2, true) \
+    X(128, 64, 16, 2, 2, 32, 2, true) \
+    X(128, 64, 32, 2, 2, 32, 2, true) \
+    X(64, 128, 16, 1, 2, 32, 2, true) \
+    X(64, 128, 16, 2, 2, 32, 2, true) \
+    X(64, 128, 32, 2, 2, 32, 2, true) \
+    X(64, 64, 16, 1, 1, 32, 2, true) \
+    X(64, 64, 16, 2, 2, 32, 2, true) \
+    X(64, 64, 32, 2, 2, 32, 2, true) \
+    X(64, 64, 16, 2, 2, 16, 2, true) \
+    X(64, 64, 32, 2, 2, 16, 2, true) \
+    X(64, 64, 16, 2, 2, 32, 1, true) \
+    X(32, 64, 16, 1, 2, 32, 2, true) \
+    X(32, 64, 32, 1, 2, 32, 2, true) \
+    X(64, 32, 16, 2, 1, 32, 2, true) \
+    X(64, 32, 32, 2, 1, 32, 2, true) \
+    X(32, 32, 16, 1, 1, 32, 2, true) \
+    X(32, 32, 32, 1, 1, 32, 2, true) \
+    X(32, 32, 16, 2, 2, 16, 2, true) \
+    X(32, 64, 16, 2, 2, 16, 2, true) \
+    X(64, 32, 16, 2, 2, 16, 2, true) \
+    X(16, 64, 16, 1, 2, 16, 2, true) \
+    X(16, 64, 32, 1, 4, 16, 2, true) \
+    X(64, 64, 16, 2, 2, 32, 2, false) \
+    X(32, 32, 16, 1, 1, 32, 2, false) \
+
+#define NNJIT_F32_INST(MT, NT, KT, WM, WN, MF, ST, VEC) \
+    template __global__ void gemm_f32_kernel<MT, NT, KT, WM, WN, MF, ST, VEC>(GemmParams);
+NNJIT_F32_LIST(NNJIT_F32_INST)
+
+#if !defined(__HIP_DEVICE_COMPILE__)
+#define NNJIT_F32_ENTRY(...) NNJIT_F32_VARIANT(__VA_ARGS__),
+const Variant kGemmF32Variants[] = {NNJIT_F32_LIST(NNJIT_F32_ENTRY)};
+const int kNumGemmF32Variants = sizeof(kGemmF32Variants) / sizeof(kGemmF32Variants[0]);
+#endif
+
+}  // namespace nnjit

@@ -1,0 +1,254 @@
+// y[N] = x[K] . W[K][N] for M == 1 (decode-time linear layers), fp32 or
+// fp16 operands, fp32 accumulation and output.  Bandwidth-bound: every byte
+// of W is read once, 128 bits per lane per load.
+//
+// Workgroup layout.  L lanes span one segment of L*V consecutive columns
+// (V = 4 fp32 or 8 fp16 columns per 128-bit load); the workgroup's other
+// lanes are row slots, so a wave reads 64/L rows of the segment at once and
+// the workgroup NTHR/L rows.  Each lane keeps U row loads in flight.  The
+// K rows of W are split over S workgroups per segment (split-K).
+//
+// Reduction over k, in a fixed order (deterministic):
+//   1. across the row slots of a wave: butterfly over lane xor L, 2L, ...
+//   2. across the waves of the workgroup: through LDS, wave 0 sums in order;
+//   3. across the S workgroups of a segment: partials in device memory, the
+//      last workgroup to arrive sums them in split order.
+#include "kcommon.h"
+
+namespace nnjit {
+
+template <typename T> struct WTraits;
+template <> struct WTraits<float> {
+    static constexpr int V = 4;
+    __device__ static __forceinline__ void fma(float (&acc)[4], float x, u32x4 w) {
+        const f32x4 f = __builtin_bit_cast(f32x4, w);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[e] = __builtin_fmaf(x, f[e], acc[e]);
+    }
+    __device__ static __forceinline__ float load1(const void *p, long long i) { return ((const float *)p)[i]; }
+    __device__ static __forceinline__ unsigned bits1(const void *p, long long i) {
+        return __builtin_bit_cast(unsigned, ((const float *)p)[i]);
+    }
+};
+template <> struct WTraits<_Float16> {
+    static constexpr int V = 8;
+    __device__ static __forceinline__ void fma(float (&acc)[8], float x, u32x4 w) {
+        const f16x8 h = __builtin_bit_cast(f16x8, w);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] = __builtin_fmaf(x, (float)h[e], acc[e]);
+    }
+    __device__ static __forceinline__ float load1(const void *p, long long i) {
+        return (float)((const _Float16 *)p)[i];
+    }
+    __device__ static __forceinline__ unsigned bits1(const void *p, long long i) {
+        return ((const unsigned short *)p)[i];
+    }
+};
+
+template <typename T, int L, int NTHR, int U, bool VEC>
+__global__ void __launch_bounds__(NTHR)
+gemv_kernel(GemvParams p)
+{
+    typedef WTraits<T> W_;
+    constexpr int V = W_::V;
+    constexpr int CW = L * V;         // columns per workgroup
+    constexpr int R = NTHR / L;       // row slots per workgroup
+    constexpr int NW = NTHR / 64;     // waves
+    static_assert(NTHR % 64 == 0 && 64 % L == 0, "layout");
+
+    const int tid = threadIdx.x;
+    const int c = tid % L, rs = tid / L;
+    const int seg = blockIdx.x % p.segs, s = blockIdx.x / p.segs;
+    const int n = seg * CW + c * V;
+    const int kbeg = s * p.kchunk;
+    const int kend = min(p.K, kbeg + p.kchunk);
+    const int N = p.N;
+
+    float acc[V];
+#pragma unroll
+    for (int e = 0; e < V; ++e) acc[e] = 0.f;
+
+    const T *W = (const T *)p.W;
+    auto wload = [&](int k) -> u32x4 {
+        const T *src = W + (long long)k * p.ldw + n;
+        if constexpr (VEC) {
+            return *(const u32x4 *)src;
+        } else {
+            // element loads, columns at or beyond N read as +0
+            u32x4 v = {0u, 0u, 0u, 0u};
+            if constexpr (V == 4) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (n + e < N) v[e] = W_::bits1(src, e);
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    if (n + e < N) v[e >> 1] |= W_::bits1(src, e) << (16 * (e & 1));
+            }
+            return v;
+        }
+    };
+
+    if (n < N) {
+        int k = kbeg + rs;
+        for (; k + (U - 1) * R < kend; k += U * R) {
+            u32x4 w[U];
+            float xv[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) w[u] = wload(k + u * R);
+#pragma unroll
+            for (int u = 0; u < U; ++u) xv[u] = W_::load1(p.x, k + u * R);
+#pragma unroll
+            for (int u = 0; u < U; ++u) W_::fma(acc, xv[u], w[u]);
+        }
+        for (; k < kend; k += R) W_::fma(acc, W_::load1(p.x, k), wload(k));
+    }
+
+    // 1. row slots inside a wave
+#pragma unroll
+    for (int off = L; off < 64; off <<= 1)
+#pragma unroll
+        for (int e = 0; e < V; ++e) acc[e] += __shfl_xor(acc[e], off, 64);
+
+    // 2. waves of the workgroup
+    if constexpr (NW > 1) {
+        __shared__ float red[NW][L][V];
+        const int wave = tid >> 6, lane = tid & 63;
+        if (lane < L)
+#pragma unroll
+            for (int e = 0; e < V; ++e) red[wave][lane][e] = acc[e];
+        __syncthreads();
+        if (tid < L) {
+#pragma unroll
+            for (int e = 0; e < V; ++e) {
+                float v = red[0][tid][e];
+#pragma unroll
+                for (int w = 1; w < NW; ++w) v += red[w][tid][e];
+                acc[e] = v;
+            }
+        }
+    }
+    // threads tid < L now hold the workgroup's sums for columns n .. n+V-1
+
+    if (p.S == 1) {
+        if (tid < L)
+#pragma unroll
+            for (int e = 0; e < V; ++e)
+                if (n + e < N) p.y[n + e] = acc[e];
+        return;
+    }
+
+    // 3. split-K partials, summed in split order by the last arrival
+    if (tid < L)
+#pragma unroll
+        for (int e = 0; e < V; ++e)
+            if (n + e < N) p.ws[(long long)s * N + n + e] = acc[e];
+    if (!splitk_arrive_last(&p.counters[seg], p.S)) return;
+    if (tid < L) {
+#pragma unroll
+        for (int e = 0; e < V; ++e) {
+            if (n + e < N) {
+                float v = 0.f;
+                for (int t = 0; t < p.S; ++t) {
+                    const float x = (t == s) ? acc[e] : p.ws[(long long)t * N + n + e];
+                    v = (t == 0) ? x : v + x;
+                }
+                p.y[n + e] = v;
+            }
+        }
+    }
+    if (tid == 0) p.counters[seg] = 0u;
+}
+
+template <typename T, int L, int NTHR, int U, bool VEC>
+static hipError_t launch_gemv(const void *params, dim3 grid, hipStream_t stream)
+{
+    hipLaunchKernelGGL((gemv_kernel<T, L, NTHR, U, VEC>), grid, dim3(NTHR), 0, stream,
+                       *(const GemvParams *)params);
+    return hipGetLastError();
+}
+
+// Registers: V accumulators, U in-flight 128-bit loads and their x values,
+// plus a fixed overhead.  LDS: the cross-wave reduction buffer.
+constexpr int est_regs_gemv(int v, int u) { return v + 5 * u + 24; }
+constexpr int lds_gemv(int nthr, int l, int v) { return nthr > 64 ? (nthr / 64) * l * v * 4 + 4 : 4; }
+
+#define NNJIT_GEMV_VARIANT(T, FAMV, V, L, NTHR, U, VEC)                                                 \
+    {"gemv_" #T "_L" #L "_t" #NTHR "_u" #U "_v" #VEC, FAMV, 0, 0, 1, L * V, NTHR / L, NTHR / 64, 1, 0,   \
+     (VEC ? 16 : (int)sizeof(T)), L, U, NTHR, lds_gemv(NTHR, L, V), est_regs_gemv(V, U),                \
+     (const void *)&gemv_kernel<T, L, NTHR, U, VEC>, &launch_gemv<T, L, NTHR, U, VEC>}
+
+
+// The compiled GEMV configurations of both dtypes.
+#define NNJIT_GEMV_LIST(X) \
+    X(float, 64, 256, 4, true) \
+    X(float, 64, 256, 8, true) \
+    X(float, 64, 512, 4, true) \
+    X(float, 64, 512, 8, true) \
+    X(float, 64, 128, 8, true) \
+    X(float, 64, 64, 8, true) \
+    X(float, 32, 256, 4, true) \
+    X(float, 32, 256, 8, true) \
+    X(float, 32, 512, 4, true) \
+    X(float, 16, 256, 4, true) \
+    X(float, 16, 256, 8, true) \
+    X(float, 16, 512, 4, true) \
+    X(float, 64, 256, 2, true) \
+    X(float, 64, 1024, 4, true) \
+    X(float, 64, 256, 4, false) \
+    X(_Float16, 64, 256, 4, true) \
+    X(_Float16, 64, 256, 8, true) \
+    X(_Float16, 64, 512, 4, true) \
+    X(_Float16, 64, 512, 8, true) \
+    X(_Float16, 64, 128, 8, true) \
+    X(_Float16, 64, 64, 8, true) \
+    X(_Float16, 32, 256, 4, true) \
+    X(_Float16, 32, 256, 8, true) \
+    X(_Float16, 32, 512, 4, true) \
+    X(_Float16, 16, 256, 4, true) \
+    X(_Float16, 16, 256, 8, true) \
+    X(_Float16, 16, 512, 4, true) \
+    X(_Float16, 64, 256, 2, true) \
+    X(_Float16, 64, 1024, 4, true) \
+    X(_Float16, 64, 256, 4, false) \
+
+#define NNJIT_GEMV_INST(T, L, NTHR, U, VEC) template __global__ void gemv_kernel<T, L, NTHR, U, VEC>(GemvParams);
+NNJIT_GEMV_LIST(NNJIT_GEMV_INST)
+
+#if !defined(__HIP_DEVICE_COMPILE__)
+#define NNJIT_GEMV_ENTRY(T, L, NTHR, U, VEC)                                                                    \
+    NNJIT_GEMV_VARIANT(T, (sizeof(T) == 4 ? FAM_GEMV_F32 : FAM_GEMV_F16), (16 / (int)sizeof(T)), L, NTHR, U, VEC),
+const Variant kGemvVariants[] = {NNJIT_GEMV_LIST(NNJIT_GEMV_ENTRY)};
+const int kNumGemvVariants = sizeof(kGemvVariants) / sizeof(kGemvVariants[0]);
+#endif
+
+// ------------------------------------------------------------------------
+// Scratch fill for the tuner: a counter-based hash of (seed, index) mapped
+// to [-1, 1), written as fp32 or fp16.  Timing candidates does not depend on
+// the values; this only keeps the scratch finite and non-trivial.
+__device__ __forceinline__ unsigned mix32(unsigned x) {
+    x ^= x >> 16; x *= 0x7feb352du; x ^= x >> 15; x *= 0x846ca68bu; x ^= x >> 16;
+    return x;
+}
+
+__global__ void fill_uniform_kernel(void *dst, long long n, int f16, unsigned seed)
+{
+    const long long stride = (long long)gridDim.x * blockDim.x;
+    for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+        const unsigned h = mix32((unsigned)i * 0x9e3779b9u ^ mix32(seed + (unsigned)(i >> 32)));
+        const float v = (float)(h >> 8) * (1.0f / 8388608.0f) - 1.0f;
+        if (f16) ((_Float16 *)dst)[i] = (_Float16)v;
+        else ((float *)dst)[i] = v;
+    }
+}
+
+hipError_t launch_fill_uniform(void *dst, long long n, int dtype, unsigned seed, hipStream_t stream)
+{
+    if (n <= 0) return hipSuccess;
+    long long blocks = (n + 255) / 256;
+    if (blocks > 4096) blocks = 4096;
+    hipLaunchKernelGGL(fill_uniform_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, dst, n, dtype, seed);
+    return hipGetLastError();
+}
+
+}  // namespace nnjit

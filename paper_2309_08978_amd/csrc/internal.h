@@ -1,0 +1,75 @@
+// Internal declarations shared by the kernels, the lite-space builder and
+// the runtime of libnnjit.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+namespace nnjit {
+
+// Kernel families.  A family fixes the operand dtype and the kernel template;
+// the configurations of a family differ in their tiling parameters.
+enum Family { FAM_GEMM_F32 = 0, FAM_GEMM_F16 = 1, FAM_GEMV_F32 = 2, FAM_GEMV_F16 = 3, FAM_COUNT = 4 };
+
+// Arguments of the GEMM / BatchMatMul kernels (one product per grid.z slice).
+struct GemmParams {
+    const void *A;
+    const void *B;
+    float *C;
+    long long lda, ldb, ldc;
+    long long sA, sB, sC;  // batch strides, elements
+    int M, N, K;
+    int S;                 // split-K factor
+    int kchunk;            // K range of one split, a multiple of the K-slab
+    int tiles_m, tiles_n;
+    float *ws;             // S > 1: partial tiles, [batch][tile][S][Mt*Nt]
+    unsigned *counters;    // S > 1: arrivals per (batch, tile); zero between launches
+};
+
+// Arguments of the M == 1 kernels: y[N] = x[K] . W[K][N].
+struct GemvParams {
+    const void *x;
+    const void *W;
+    float *y;
+    long long ldw;
+    int K, N;
+    int S;            // split-K factor
+    int kchunk;       // rows of W per split
+    int segs;         // column segments
+    float *ws;        // S > 1: partial rows, [S][N]
+    unsigned *counters;  // S > 1: arrivals per segment; zero between launches
+};
+
+typedef hipError_t (*LaunchFn)(const void *params, dim3 grid, hipStream_t stream);
+
+// One compiled kernel instantiation (a point of the lite space's parameter
+// axes, before the runtime split-K factor is chosen).
+struct Variant {
+    const char *name;
+    int family;
+    int mfma_m, mfma_k;   // matrix-core instruction shape (0 for GEMV)
+    int mt, nt, kt;       // macro tile (GEMV: mt = 1, nt = columns per WG, kt = rows per pass)
+    int wm, wn;           // wave grid of the workgroup (GEMV: wm = waves, wn = 1)
+    int stages;           // LDS buffers for the K loop (1 or 2; GEMV 0)
+    int vec_bytes;        // bytes per global load of one lane (16, or the element size)
+    int lanes_seg;        // GEMV: lanes across one row segment
+    int unroll;           // GEMV: row loads in flight per lane
+    int threads;          // workgroup size
+    int lds_bytes;        // static LDS of one workgroup
+    int est_regs;         // VGPR+AGPR estimate per lane (the Table 1 register formula)
+    const void *kernel;   // device function (attribute queries)
+    LaunchFn launch;
+};
+
+// Variant tables, one per family (defined in the kernel sources).
+extern const Variant kGemmF32Variants[];
+extern const int kNumGemmF32Variants;
+extern const Variant kGemmF16Variants[];
+extern const int kNumGemmF16Variants;
+extern const Variant kGemvVariants[];
+extern const int kNumGemvVariants;
+
+// Device helper kernels (scratch fill for the tuner).
+hipError_t launch_fill_uniform(void *dst, long long n, int dtype, unsigned seed, hipStream_t stream);
+
+}  // namespace nnjit

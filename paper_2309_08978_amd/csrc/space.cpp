@@ -1,0 +1,235 @@
+// Configurations, the Table 1 resource model and the lite-space builder of
+// the paper's device-guided space building (Sec. 5.2), on one CDNA4 CU.
+// Host-only: no HIP runtime calls.
+#include "space.h"
+
+#include <algorithm>
+#include <climits>
+#include <cmath>
+#include <cstdio>
+
+namespace nnjit {
+
+static const Variant *variant_at(int gi) {
+    if (gi < kNumGemmF32Variants) return &kGemmF32Variants[gi];
+    gi -= kNumGemmF32Variants;
+    if (gi < kNumGemmF16Variants) return &kGemmF16Variants[gi];
+    gi -= kNumGemmF16Variants;
+    return &kGemvVariants[gi];
+}
+
+int total_variants() { return kNumGemmF32Variants + kNumGemmF16Variants + kNumGemvVariants; }
+
+int variant_index(const Variant *v) {
+    if (v >= kGemmF32Variants && v < kGemmF32Variants + kNumGemmF32Variants) return (int)(v - kGemmF32Variants);
+    if (v >= kGemmF16Variants && v < kGemmF16Variants + kNumGemmF16Variants)
+        return kNumGemmF32Variants + (int)(v - kGemmF16Variants);
+    return kNumGemmF32Variants + kNumGemmF16Variants + (int)(v - kGemvVariants);
+}
+
+const std::vector<int> &gemm_splits() {
+    static const std::vector<int> s = {1, 2, 4, 8, 16};
+    return s;
+}
+const std::vector<int> &gemv_splits() {
+    static const std::vector<int> s = {1, 2, 4, 8, 16, 32, 64, 128};
+    return s;
+}
+
+int family_dtype(int family) { return (family == FAM_GEMM_F16 || family == FAM_GEMV_F16) ? NNJIT_F16 : NNJIT_F32; }
+bool family_is_gemv(int family) { return family == FAM_GEMV_F32 || family == FAM_GEMV_F16; }
+int family_of(int kind, int dtype) {
+    if (kind == NNJIT_KIND_GEMV) return dtype == NNJIT_F16 ? FAM_GEMV_F16 : FAM_GEMV_F32;
+    return dtype == NNJIT_F16 ? FAM_GEMM_F16 : FAM_GEMM_F32;
+}
+const char *family_name(int family) {
+    switch (family) {
+    case FAM_GEMM_F32: return "gemm_f32";
+    case FAM_GEMM_F16: return "gemm_f16";
+    case FAM_GEMV_F32: return "gemv_f32";
+    case FAM_GEMV_F16: return "gemv_f16";
+    default: return "?";
+    }
+}
+
+const std::vector<Config> &configs() {
+    static const std::vector<Config> all = [] {
+        std::vector<Config> out;
+        const int nv = total_variants();
+        for (int gi = 0; gi < nv; ++gi) {
+            const Variant *v = variant_at(gi);
+            const std::vector<int> &splits = family_is_gemv(v->family) ? gemv_splits() : gemm_splits();
+            for (int s : splits) out.push_back(Config{(int)out.size(), v, s});
+        }
+        return out;
+    }();
+    return all;
+}
+
+nnjit_device_limits mi355x_limits() {
+    nnjit_device_limits d;
+    d.num_cus = 256;
+    d.simds_per_cu = 4;
+    d.vgprs_per_lane = 512;
+    d.vgpr_granule = 8;
+    d.max_waves_per_simd = 8;
+    d.wave_size = 64;
+    d.lds_per_cu = 163840;
+    d.lds_per_wg = 163840;
+    d.max_threads_per_wg = 1024;
+    return d;
+}
+
+// Table 1 of the paper, on one compute unit ("core"):
+//   Reg_thread   -> VGPR+AGPR per lane (measured from the compiled kernel, or
+//                   the estimate inflated by the relaxation ratio)
+//   L1_block     -> LDS bytes of the workgroup (the C tile lives in registers)
+//   Thread_block -> workgroup size;  Warp_block -> waves of 64 lanes
+//   Block_core   =  min(RegLimit, L1Limit, WarpLimit)
+// RegLimit counts whole waves: a SIMD holds floor(512 / regs) waves (regs
+// rounded up to the allocation granule), at most max_waves_per_simd.
+nnjit_resources resources_of(const Variant &v, const nnjit_device_limits &d, int measured_regs) {
+    nnjit_resources r{};
+    const int regs = measured_regs >= 0 ? measured_regs : (int)std::ceil(v.est_regs / kRelaxation);
+    r.regs_per_lane = regs;
+    r.regs_measured = measured_regs >= 0 ? 1 : 0;
+    r.lds_per_wg = v.lds_bytes;
+    r.threads_per_wg = v.threads;
+    r.waves_per_wg = (v.threads + d.wave_size - 1) / d.wave_size;
+    const int gran = d.vgpr_granule > 0 ? d.vgpr_granule : 1;
+    const int g = ((std::max(regs, 1) + gran - 1) / gran) * gran;
+    const int wps = std::min(d.max_waves_per_simd, d.vgprs_per_lane / g);
+    r.reg_limit = (d.simds_per_cu * wps) / r.waves_per_wg;
+    r.lds_limit = v.lds_bytes > 0 ? (int)std::min<int64_t>(d.lds_per_cu / v.lds_bytes, 1 << 20) : (1 << 20);
+    r.wave_limit = (d.simds_per_cu * d.max_waves_per_simd) / r.waves_per_wg;
+    r.wg_per_cu = std::min(r.reg_limit, std::min(r.lds_limit, r.wave_limit));
+    return r;
+}
+
+static int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+static int64_t pow2ceil(int64_t x) {
+    int64_t p = 1;
+    while (p < x) p <<= 1;
+    return p;
+}
+
+Geometry geometry_of(const Config &c, int64_t batch, int64_t M, int64_t N, int64_t K) {
+    Geometry g;
+    const Variant &v = *c.v;
+    g.split = c.split;
+    if (!family_is_gemv(v.family)) {
+        g.tiles_m = (int)ceil_div(std::max<int64_t>(M, 1), v.mt);
+        g.tiles_n = (int)ceil_div(std::max<int64_t>(N, 1), v.nt);
+        const int64_t per = ceil_div(std::max<int64_t>(K, 1), c.split);
+        g.kchunk = (int)(ceil_div(per, v.kt) * v.kt);
+        const int64_t tiles = batch * g.tiles_m * (int64_t)g.tiles_n;
+        g.wgs = tiles * c.split;
+        g.ws_floats = c.split > 1 ? tiles * c.split * (int64_t)v.mt * v.nt : 0;
+        g.counters = c.split > 1 ? tiles : 0;
+    } else {
+        g.tiles_m = 1;
+        g.tiles_n = (int)ceil_div(std::max<int64_t>(N, 1), v.nt);
+        g.kchunk = (int)std::max<int64_t>(1, ceil_div(std::max<int64_t>(K, 1), c.split));
+        g.wgs = (int64_t)g.tiles_n * c.split;
+        g.ws_floats = c.split > 1 ? (int64_t)c.split * N : 0;
+        g.counters = c.split > 1 ? g.tiles_n : 0;
+    }
+    return g;
+}
+
+namespace {
+struct Cand {
+    int id;
+    nnjit_resources r;
+    double eff;      // fill of the last wave of workgroups
+    int64_t area;    // macro-tile area (GEMM) or columns x rows per pass (GEMV)
+    int split;
+};
+}  // namespace
+
+LiteResult lite_space(const Shape &s, const nnjit_device_limits &d, const std::vector<int> *measured_regs,
+                      const std::vector<int> *spills) {
+    LiteResult out;
+    const int fam = family_of(s.kind, s.dtype);
+    const bool gemv = family_is_gemv(fam);
+    const int V = vec_elems(s.dtype);
+    const bool vec_ok = gemv ? (s.N % V == 0) : (s.K % V == 0 && s.N % V == 0);
+
+    // size of the unpruned parameter space over the same axes
+    if (!gemv) {
+        const int64_t kt_choices = fam == FAM_GEMM_F32 ? 2 : 1;
+        out.n_naive = 2 /*mfma*/ * 5 /*Mt*/ * 5 /*Nt*/ * kt_choices * 3 /*WM*/ * 3 /*WN*/ * 2 /*stages*/ *
+                      (int64_t)gemm_splits().size();
+    } else {
+        out.n_naive = 3 /*L*/ * 5 /*threads*/ * 4 /*U*/ * (int64_t)gemv_splits().size();
+    }
+
+    std::vector<Cand> cands;
+    for (const Config &c : configs()) {
+        const Variant &v = *c.v;
+        if (v.family != fam) continue;
+        ++out.n_enumerated;
+        if ((v.vec_bytes == 16) != vec_ok) continue;  // vector loads only where the shape allows them
+        const int gi = variant_index(&v);
+        if (spills && gi < (int)spills->size() && (*spills)[gi]) continue;
+        const int mregs = (measured_regs && gi < (int)measured_regs->size()) ? (*measured_regs)[gi] : -1;
+        const nnjit_resources r = resources_of(v, d, mregs);
+        if (r.threads_per_wg > std::min(512, d.max_threads_per_wg)) continue;  // heuristic 5
+        if (r.lds_per_wg > d.lds_per_wg) continue;                            // heuristic 6
+        if (r.wg_per_cu < 1) continue;
+
+        const Geometry g = geometry_of(c, s.batch, s.M, s.N, s.K);
+        const int64_t slots = (int64_t)d.num_cus * r.wg_per_cu;
+        if (!gemv) {
+            // shape fit: no macro tile wider than the (power-of-two rounded) matrix
+            if (v.mt > std::max<int64_t>(16, pow2ceil(s.M)) || v.nt > std::max<int64_t>(16, pow2ceil(s.N))) continue;
+            const int64_t tiles = s.batch * g.tiles_m * (int64_t)g.tiles_n;
+            if (c.split > 1) {
+                if (tiles >= slots) continue;               // already fills the chip
+                if (tiles * c.split > 2 * slots) continue;  // over-split
+                if (s.K < 2LL * c.split * v.kt) continue;    // at least two K slabs per split
+            }
+        } else {
+            if (v.nt > std::max<int64_t>(64, pow2ceil(s.N))) continue;
+            const int rows_per_pass = v.kt;
+            if (g.kchunk < rows_per_pass) continue;  // every split gets at least one pass of rows
+            int smax = 1;
+            for (int sp : gemv_splits())
+                if (ceil_div(std::max<int64_t>(s.K, 1), sp) >= rows_per_pass) smax = sp;
+            if (c.split > 1 && g.wgs > 4 * slots) continue;                  // over-split
+            if (g.wgs < d.num_cus / 2 && c.split != smax) continue;          // under-filled
+            // Little's law: bytes in flight per CU must cover HBM latency
+            const int64_t wg_here = std::min<int64_t>(r.wg_per_cu, ceil_div(g.wgs, d.num_cus));
+            if (wg_here * v.threads * (int64_t)v.unroll * 16 < 8192 && c.split != smax) continue;
+        }
+        Cand cd;
+        cd.id = c.id;
+        cd.r = r;
+        const int64_t waves = ceil_div(std::max<int64_t>(g.wgs, 1), slots);
+        cd.eff = (double)g.wgs / (double)(waves * slots);
+        cd.area = (int64_t)v.mt * v.nt * (gemv ? v.kt : 1);
+        cd.split = c.split;
+        cands.push_back(cd);
+    }
+
+    // heuristic 7: keep register-bound candidates (Block_core == RegLimit),
+    // relaxed when too few survive
+    std::vector<Cand> kept;
+    for (const Cand &c : cands)
+        if (c.r.wg_per_cu == c.r.reg_limit) kept.push_back(c);
+    if ((int)kept.size() < kMinSurvivors) kept = cands;
+
+    // evaluation order: most workgroups per CU first, then fuller last wave,
+    // larger tile, smaller split, lower id
+    std::stable_sort(kept.begin(), kept.end(), [](const Cand &a, const Cand &b) {
+        if (a.r.wg_per_cu != b.r.wg_per_cu) return a.r.wg_per_cu > b.r.wg_per_cu;
+        if (std::fabs(a.eff - b.eff) > 1e-9) return a.eff > b.eff;
+        if (a.area != b.area) return a.area > b.area;
+        if (a.split != b.split) return a.split < b.split;
+        return a.id < b.id;
+    });
+    for (const Cand &c : kept) out.ids.push_back(c.id);
+    return out;
+}
+
+}  // namespace nnjit

@@ -1,0 +1,78 @@
+// Configurations, the Table 1 resource model and the lite-space builder.
+// Host-only code: nothing here calls the HIP runtime.
+#pragma once
+
+#include <cstdint>
+#include <vector>
+
+#include "internal.h"
+#include "../../include/nnjit.h"
+
+namespace nnjit {
+
+// A configuration = a compiled variant + a split-K factor.  Its id is its
+// index in configs().
+struct Config {
+    int id;
+    const Variant *v;
+    int split;
+};
+
+const std::vector<Config> &configs();
+
+// Split-K factors considered per kind (powers of two, heuristic 2).
+const std::vector<int> &gemm_splits();
+const std::vector<int> &gemv_splits();
+
+int family_dtype(int family);       // NNJIT_F32 / NNJIT_F16
+bool family_is_gemv(int family);
+int family_of(int kind, int dtype);  // family whose kernels run this kind/dtype
+const char *family_name(int family);
+
+// Elements of 16 bytes for a dtype (the vector width of heuristic 1).
+inline int vec_elems(int dtype) { return dtype == NNJIT_F16 ? 8 : 4; }
+
+// MI355X defaults for host-only use.
+nnjit_device_limits mi355x_limits();
+
+// Table 1 of the paper on one CDNA4 compute unit.  measured_regs < 0 means
+// "not measured": the estimate is used, inflated by the relaxation ratio.
+nnjit_resources resources_of(const Variant &v, const nnjit_device_limits &d, int measured_regs);
+
+constexpr double kRelaxation = 0.9;  // share of the register file the estimate may claim
+constexpr int kMaxTimed = 64;        // candidates timed per shape at most
+constexpr int kMinSurvivors = 8;     // heuristic 7 is relaxed below this many
+
+struct Shape {
+    int kind;
+    int dtype;
+    int64_t batch, M, N, K;
+};
+
+struct LiteResult {
+    std::vector<int> ids;       // survivors in evaluation order
+    int n_enumerated = 0;       // compiled configurations of the family
+    int64_t n_naive = 0;        // unpruned size of the parameter axes
+};
+
+// measured_regs: per-variant register counts of the compiled kernels for the
+// family's variant table (empty = estimate); spills: per-variant flag.
+LiteResult lite_space(const Shape &s, const nnjit_device_limits &d, const std::vector<int> *measured_regs,
+                      const std::vector<int> *spills);
+
+// Launch geometry of a configuration for a shape.
+struct Geometry {
+    int tiles_m = 0, tiles_n = 0;  // GEMM tiles per batch slice (GEMV: segs in tiles_n)
+    int split = 1;
+    int kchunk = 0;
+    int64_t wgs = 0;               // workgroups over the whole launch
+    int64_t ws_floats = 0;         // split-K partial storage
+    int64_t counters = 0;          // split-K arrival counters
+};
+Geometry geometry_of(const Config &c, int64_t batch, int64_t M, int64_t N, int64_t K);
+
+// Index of a variant inside its family table (used to look up measured data).
+int variant_index(const Variant *v);
+int total_variants();
+
+}  // namespace nnjit

@@ -1,0 +1,164 @@
+"""Host-side tests of the C-ABI library (no GPU): it loads, exports every
+entry point include/nnjit.h declares, validates arguments before touching
+HIP, and its lite-space builder follows the Table 1 resource model and
+heuristics of the paper (Sec. 5.2)."""
+import json
+import os
+import re
+
+import pytest
+
+import paper_2309_08978_amd as nj
+import workloads
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "nnjit.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return nj.load(build_if_missing=True)
+
+
+def _declared():
+    src = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:int|const char \*)\s*(nnjit_\w+)\s*\(", src, re.M)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _declared()
+    assert len(names) >= 15
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(nj.EXPORTED)
+
+
+def test_validation_without_gpu(lib):
+    # bad arguments are reported before any HIP call
+    assert nj.nnjit_matmul(4, 4, 4, 1, 4, 2, 4, 3, 4, 9, None) == nj.NNJIT_EDTYPE
+    assert nj.nnjit_matmul(-1, 4, 4, 1, 4, 2, 4, 3, 4, 0, None) == nj.NNJIT_EINVAL
+    assert nj.nnjit_matmul(4, 4, 4, 1, 3, 2, 4, 3, 4, 0, None) == nj.NNJIT_EINVAL  # lda < K
+    assert nj.nnjit_matmul(4, 4, 4, 1, 4, 2, 3, 3, 4, 0, None) == nj.NNJIT_EINVAL  # ldb < N
+    assert nj.nnjit_matmul(4, 4, 4, 1, 4, 2, 4, 3, 3, 0, None) == nj.NNJIT_EINVAL  # ldc < N
+    assert nj.nnjit_matmul(4, 4, 4, None, 4, 2, 4, 3, 4, 0, None) == nj.NNJIT_EINVAL
+    assert "A is NULL" in nj.nnjit_last_error()
+    assert nj.nnjit_batched_matmul(2, 4, 4, 4, 1, 4, -1, 2, 4, 16, 3, 4, 16, 0, None) == nj.NNJIT_EINVAL
+    assert nj.nnjit_matmul(1 << 31, 4, 4, 1, 4, 2, 4, 3, 4, 0, None) == nj.NNJIT_EINVAL
+    # empty products are no-ops that never touch the GPU
+    assert nj.nnjit_matmul(0, 4, 4, None, 4, 2, 4, None, 4, 0, None) == nj.NNJIT_OK
+    assert nj.nnjit_batched_matmul(0, 4, 4, 4, None, 4, 16, None, 4, 16, None, 4, 16, 0, None) == nj.NNJIT_OK
+    assert nj.nnjit_matmul_config(nj.nnjit_num_configs(), 1, 4, 4, 4, 1, 4, 0, 2, 4, 0, 3, 4, 0, 0, None) == nj.NNJIT_EINVAL
+    assert nj.nnjit_tune(64, 64, 64, 5) == nj.NNJIT_EDTYPE
+    assert nj.nnjit_tune(0, 64, 64, 0) == nj.NNJIT_EINVAL
+
+
+def test_no_gpu_is_ehip_not_abort(lib):
+    try:
+        import torch
+        if torch.cuda.is_available():
+            pytest.skip("a GPU is present")
+    except ImportError:
+        pass
+    assert nj.nnjit_matmul(4, 4, 4, 1, 4, 2, 4, 3, 4, 0, None) == nj.NNJIT_EHIP
+    assert nj.nnjit_tune(64, 768, 768, 0) == nj.NNJIT_EHIP
+    assert nj.nnjit_last_error()
+
+
+def test_config_table(lib):
+    cfgs = nj.configs()
+    assert len(cfgs) == nj.nnjit_num_configs() > 100
+    assert [c["id"] for c in cfgs] == list(range(len(cfgs)))
+    fams = {c["family"] for c in cfgs}
+    assert fams == {"gemm_f32", "gemm_f16", "gemv_f32", "gemv_f16"}
+    p2 = lambda x: x > 0 and (x & (x - 1)) == 0
+    for c in cfgs:
+        assert c["vec"] <= 16                     # heuristic 1: at most 128-bit accesses
+        assert p2(c["split"])
+        if c["family"].startswith("gemm"):
+            for k in ("Mt", "Nt", "Kt"):
+                assert p2(c[k]), (c, k)           # heuristic 2: power-of-two tiles
+            wm, wn = map(int, c["waves"].split("x"))
+            assert c["Mt"] % wm == 0 and c["Nt"] % wn == 0
+            assert c["threads"] == 64 * wm * wn
+        else:
+            assert p2(c["cols"]) and p2(c["lanes_per_seg"]) and p2(c["threads"])
+
+
+def test_table1_resources_golden(lib):
+    g = json.load(open(os.path.join(ROOT, "tests", "golden", "table1_resources.json")))
+    cfg = next(c for c in nj.configs() if c["name"] == g["config_name"] and c["split"] == 1)
+    r = nj.nnjit_config_resources(cfg["id"], nj.mi355x_limits())
+    assert r == g["expected"]
+
+
+def test_resource_limits_follow_the_formula(lib):
+    d = nj.mi355x_limits()
+    for c in nj.configs():
+        r = nj.nnjit_config_resources(c["id"], d)
+        regs = -(-r["regs_per_lane"] // 8) * 8
+        wps = min(8, 512 // regs)
+        assert r["waves_per_wg"] == -(-c["threads"] // 64)
+        assert r["reg_limit"] == 4 * wps // r["waves_per_wg"]
+        assert r["lds_limit"] == min(163840 // max(r["lds_per_wg"], 1), 1 << 20)
+        assert r["wave_limit"] == 32 // r["waves_per_wg"]
+        assert r["wg_per_cu"] == min(r["reg_limit"], r["lds_limit"], r["wave_limit"])
+
+
+def _kind(op):
+    return {"gemm": nj.NNJIT_KIND_GEMM, "batched": nj.NNJIT_KIND_BATCHED, "gemv": nj.NNJIT_KIND_GEMV}[op.kind]
+
+
+ALL_OPS = [(n, i) for n in workloads.WORKLOADS for i in range(len(workloads.workload(n)))]
+
+
+@pytest.mark.parametrize("name,index", ALL_OPS)
+def test_lite_space_is_dozens_and_ordered(lib, name, index):
+    op = workloads.workload(name)[index]
+    d = nj.mi355x_limits()
+    dt = nj.NNJIT_F16 if op.dtype == "f16" else nj.NNJIT_F32
+    ids, n, n_enum, n_naive = nj.nnjit_lite_space(_kind(op), dt, op.batch, op.M, op.N, op.K, d)
+    assert 8 <= n <= 100, n            # "dozens", never empty
+    assert n_naive > (10 * n if op.kind != "gemv" else 2 * n)
+    cfgs = nj.configs()
+    fam = ("gemv_" if op.kind == "gemv" else "gemm_") + op.dtype
+    prev = None
+    for i in ids:
+        c = cfgs[i]
+        assert c["family"] == fam
+        r = nj.nnjit_config_resources(i, d)
+        assert c["threads"] <= 512                       # heuristic 5
+        assert r["lds_per_wg"] <= d.lds_per_wg           # heuristic 6
+        if prev is not None:
+            assert r["wg_per_cu"] <= prev                # evaluated from max to min Block_core
+        prev = r["wg_per_cu"]
+        if op.kind != "gemv":
+            assert c["Mt"] <= max(16, 1 << (op.M - 1).bit_length())
+    # deterministic
+    assert nj.nnjit_lite_space(_kind(op), dt, op.batch, op.M, op.N, op.K, d)[0] == ids
+
+
+def test_heuristic7_prefers_register_bound(lib):
+    d = nj.mi355x_limits()
+    ids, n, _, _ = nj.nnjit_lite_space(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, 1024, 1024, 1024, d)
+    rs = [nj.nnjit_config_resources(i, d) for i in ids]
+    bound = [r["wg_per_cu"] == r["reg_limit"] for r in rs]
+    assert all(bound) or n >= 8
+
+
+def test_more_lds_never_shrinks_limits(lib):
+    d = nj.mi355x_limits()
+    d2 = nj.mi355x_limits()
+    d2.lds_per_cu = 2 * d.lds_per_cu
+    for c in nj.configs()[::7]:
+        a = nj.nnjit_config_resources(c["id"], d)
+        b = nj.nnjit_config_resources(c["id"], d2)
+        assert b["lds_limit"] >= a["lds_limit"] and b["wg_per_cu"] >= a["wg_per_cu"]
+
+
+def test_misaligned_shapes_get_element_load_configs(lib):
+    d = nj.mi355x_limits()
+    ids, n, _, _ = nj.nnjit_lite_space(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, 100, 101, 99, d)
+    cfgs = nj.configs()
+    assert n >= 1 and all(cfgs[i]["vec"] == 4 for i in ids)
+    ids, n, _, _ = nj.nnjit_lite_space(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, 100, 104, 96, d)
+    assert all(cfgs[i]["vec"] == 16 for i in ids)

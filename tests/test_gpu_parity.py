@@ -1,0 +1,259 @@
+"""GPU parity of the HIP path against the CPU oracle, through the C-ABI.
+
+* every configuration id, forced, on small-integer operands at ragged shapes
+  spanning several tiles: bit-exact (all partial sums are exact in fp32, so
+  any summation order gives the oracle's value), and run twice: identical;
+* every workload shape, tuned, on the workload's own value distributions:
+  fp32 within rel-Frobenius 1e-5 and |err| <= 2e-6 K max|A| max|B| per
+  element; fp16 inputs within rel-Frobenius 2e-3 -- on all elements where the
+  oracle finishes in seconds, else on sampled elements;
+* edge cases: K = 0, empty operands, padded leading dimensions, batch strides
+  with gaps, misaligned operands (element-load fallback), M = 1 batches;
+* metamorphic relations: power-of-two scaling and batch slices are
+  bit-exact, (B^T A^T)^T matches within tolerance.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from oracle import accept
+import paper_2309_08978_amd as nj
+import workloads
+from tests.gpu_util import dev, host, gpu_matmul, kind_of, dtype_code
+
+pytestmark = pytest.mark.gpu
+
+FAMILY_DTYPE = {"gemm_f32": "f32", "gemm_f16": "f16", "gemv_f32": "f32", "gemv_f16": "f16"}
+
+
+def _family_shapes(family: str, vec: bool):
+    """(batch, M, N, K) used to pin every configuration of a family.  Vector
+    (16-byte) configurations need N and K multiples of 8 elements; the
+    element-load ones get fully ragged shapes."""
+    gemv = family.startswith("gemv")
+    if gemv:
+        return (1, 1, 1032, 997) if vec else (1, 1, 1027, 997)
+    return (2, 291, 264, 200) if vec else (2, 291, 259, 197)
+
+
+@pytest.fixture(scope="module")
+def all_configs():
+    nj.load()
+    return nj.configs()
+
+
+def _int_case(family, vec, seed):
+    batch, M, N, K = _family_shapes(family, vec)
+    dt = FAMILY_DTYPE[family]
+    A, B = workloads.small_int_operands(seed, batch, M, K, N, dt)
+    R = oracle.matmul(A, B)
+    return A, B, R
+
+
+@pytest.mark.parametrize("family", ["gemm_f32", "gemm_f16", "gemv_f32", "gemv_f16"])
+def test_every_config_bit_exact_small_integers(all_configs, family):
+    import torch
+    cases = {}
+    n = 0
+    for c in all_configs:
+        if c["family"] != family:
+            continue
+        vec = c["vec"] == 16
+        if vec not in cases:
+            cases[vec] = _int_case(family, vec, 1000 + int(vec))
+        A, B, R = cases[vec]
+        dA, dB = dev(A), dev(B)
+        shape = R.shape
+        outs = []
+        for rep in range(2):
+            C = torch.full(shape, float("nan"), dtype=torch.float32, device="cuda:0")
+            if A.ndim == 2:
+                nj.matmul(dA, dB, C, cfg=c["id"])
+            else:
+                nj.batched_matmul(dA, dB, C, cfg=c["id"])
+            outs.append(host(C))
+        assert np.array_equal(outs[0], R), f"config {c['id']} {c['name']} split={c['split']} differs from the oracle"
+        assert np.array_equal(outs[0], outs[1]), f"config {c['id']} not deterministic"
+        n += 1
+    assert n > 0
+    print(f"{family}: {n} configurations bit-exact", flush=True)
+
+
+def _sample_idx(rng, shape, n=1500):
+    """Random output positions plus the corners and the ragged edges."""
+    if len(shape) == 2:
+        shape = (1,) + tuple(shape)
+    b, M, N = shape
+    idx = {(int(rng.integers(b)), int(rng.integers(M)), int(rng.integers(N))) for _ in range(n)}
+    for bb in {0, b - 1}:
+        for i in {0, M - 1}:
+            for j in {0, N - 1}:
+                idx.add((bb, i, j))
+        for j in range(max(0, N - 9), N):
+            idx.add((bb, M - 1, j))
+        for i in range(max(0, M - 9), M):
+            idx.add((bb, i, N - 1))
+    return sorted(idx)
+
+
+FULL_ORACLE_FLOPS = 1.5e9
+
+WL_OPS = [(name, i) for name in workloads.WORKLOADS for i in range(len(workloads.workload(name)))]
+
+
+@pytest.mark.parametrize("name,index", WL_OPS, ids=[f"{n}-{workloads.workload(n)[i].name}" for n, i in WL_OPS])
+def test_workload_shape_parity(name, index):
+    import torch
+    op = workloads.workload(name)[index]
+    A, B = workloads.op_inputs(name, index)
+    dt = dtype_code(op.dtype)
+    if op.batch == 1:
+        cfg = nj.check(nj.nnjit_tune(op.M, op.N, op.K, dt))
+    else:
+        cfg = nj.check(nj.nnjit_tune_batched(op.batch, op.M, op.N, op.K, dt))
+    st = nj.nnjit_last_tune_stats()
+    print(f"{name}/{op.name}: tuned -> {nj.nnjit_config_info(cfg)} | {st['best_us']:.2f} us, "
+          f"lite {st['n_lite']}, timed {st['n_timed']}, tune {st['wall_ms']:.0f} ms", flush=True)
+    lite, _, _, _ = nj.nnjit_lite_space(kind_of(op.batch, op.M), dt, op.batch, op.M, op.N, op.K)
+    assert cfg in lite
+    C = gpu_matmul(A, B)  # dispatch through the tuned cache
+    assert nj.nnjit_cached_config(kind_of(op.batch, op.M), dt, op.batch, op.M, op.N, op.K) == cfg
+    if op.flops <= FULL_ORACLE_FLOPS:
+        R = oracle.matmul(A, B)
+        res = accept.check(C, R, A, B, op.dtype)
+    else:
+        rng = np.random.default_rng(index)
+        idx = _sample_idx(rng, C.shape)
+        Rs = oracle.elements(A, B, idx)
+        C3 = C if C.ndim == 3 else C[None]
+        Cs = np.array([C3[t] for t in idx])
+        res = accept.check(Cs, Rs, A, B, op.dtype, K=op.K)
+    print(f"   rel_fro={res['rel_fro']:.3e} max_err={res['max_err']:.3e} bound={res['elt_bound']:.3e}", flush=True)
+    assert res["ok"], res
+    if op.dtype == "f16":
+        # informational: fp16 x fp16 products are exact in fp32, so the fp32 bar usually holds too
+        print(f"   (fp32 bar on fp16 inputs: {accept.check(C if op.flops <= FULL_ORACLE_FLOPS else Cs, R if op.flops <= FULL_ORACLE_FLOPS else Rs, A, B, 'f32', K=op.K)['ok']})")
+    del C
+    torch.cuda.empty_cache()
+
+
+# ------------------------------------------------------------------ edge cases
+
+@pytest.mark.parametrize("dt", ["f32", "f16"])
+def test_k_zero_writes_zeros(dt):
+    import torch
+    tdt = torch.float16 if dt == "f16" else torch.float32
+    for (b, M, N) in [(1, 37, 45), (1, 1, 64), (3, 17, 9)]:
+        A = torch.empty((b, M, 0), dtype=tdt, device="cuda:0")
+        B = torch.empty((b, 0, N), dtype=tdt, device="cuda:0")
+        C = torch.full((b, M, N), float("nan"), device="cuda:0")
+        if b == 1:
+            nj.matmul(A[0], B[0], C[0])
+        else:
+            nj.batched_matmul(A, B, C)
+        assert np.array_equal(host(C), np.zeros((b, M, N)))
+
+
+def test_empty_shapes_are_noops():
+    import torch
+    C = torch.full((4, 5), 7.0, device="cuda:0")
+    A = torch.ones((4, 3), device="cuda:0")
+    B = torch.ones((3, 5), device="cuda:0")
+    assert nj.nnjit_matmul(0, 5, 3, A, 3, B, 5, C, 5, 0, None) == 0
+    assert nj.nnjit_matmul(4, 0, 3, A, 3, B, 5, C, 5, 0, None) == 0
+    assert nj.nnjit_batched_matmul(0, 4, 5, 3, A, 3, 12, B, 5, 15, C, 5, 20, 0, None) == 0
+    assert np.all(host(C) == 7.0)
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16"])
+def test_padded_leading_dims_and_batch_gaps(dt):
+    import torch
+    b, M, N, K = 3, 70, 136, 96
+    A, B = workloads.small_int_operands(77, b, M, K, N, dt)
+    R = oracle.matmul(A, B)
+    tdt = torch.float16 if dt == "f16" else torch.float32
+    lda, ldb, ldc = K + 8, N + 16, N + 5
+    sA, sB, sC = M * lda + 64, K * ldb + 40, M * ldc + 11
+    bufA = torch.zeros(b * sA, dtype=tdt, device="cuda:0")
+    bufB = torch.zeros(b * sB, dtype=tdt, device="cuda:0")
+    bufC = torch.full((b * sC,), -3.0, device="cuda:0")
+    for i in range(b):
+        bufA[i * sA:i * sA + M * lda].view(M, lda)[:, :K] = dev(A[i])
+        bufB[i * sB:i * sB + K * ldb].view(K, ldb)[:, :N] = dev(B[i])
+    rc = nj.nnjit_batched_matmul(b, M, N, K, bufA, lda, sA, bufB, ldb, sB, bufC, ldc, sC, dtype_code(dt), None)
+    assert rc == 0, nj.nnjit_last_error()
+    hc = host(bufC)
+    for i in range(b):
+        Ci = hc[i * sC:i * sC + M * ldc].reshape(M, ldc)
+        assert np.array_equal(Ci[:, :N], R[i])
+        assert np.all(Ci[:, N:] == -3.0)  # padding untouched
+        if i + 1 < b:
+            assert np.all(hc[i * sC + M * ldc:(i + 1) * sC] == -3.0)
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16"])
+@pytest.mark.parametrize("M", [1, 45])
+def test_misaligned_operands_use_fallback(dt, M):
+    import torch
+    N, K = 200, 96
+    A, B = workloads.small_int_operands(78, 1, M, K, N, dt)
+    R = oracle.matmul(A, B)
+    tdt = torch.float16 if dt == "f16" else torch.float32
+    bA = torch.zeros(M * K + 1, dtype=tdt, device="cuda:0")
+    bB = torch.zeros(K * N + 1, dtype=tdt, device="cuda:0")
+    bA[1:] = dev(A).reshape(-1)
+    bB[1:] = dev(B).reshape(-1)
+    C = torch.full((M, N), float("nan"), device="cuda:0")
+    rc = nj.nnjit_matmul(M, N, K, bA.data_ptr() + bA.element_size(), K, bB.data_ptr() + bB.element_size(), N,
+                         C, N, dtype_code(dt), None)
+    assert rc == 0, nj.nnjit_last_error()
+    assert np.array_equal(host(C), R)
+
+
+def test_batch_of_row_vectors():
+    A, B = workloads.small_int_operands(79, 5, 1, 300, 260, "f32")
+    assert np.array_equal(gpu_matmul(A, B), oracle.matmul(A, B))
+
+
+def test_forced_config_mismatch_is_einval(all_configs):
+    import torch
+    A = torch.ones((4, 8), device="cuda:0")
+    B = torch.ones((8, 8), device="cuda:0")
+    C = torch.empty((4, 8), device="cuda:0")
+    gemv = next(c["id"] for c in all_configs if c["family"] == "gemv_f32")
+    f16 = next(c["id"] for c in all_configs if c["family"] == "gemm_f16")
+    assert nj.nnjit_matmul_config(gemv, 1, 4, 8, 8, A, 8, 0, B, 8, 0, C, 8, 0, 0, None) == nj.NNJIT_EINVAL
+    assert nj.nnjit_matmul_config(f16, 1, 4, 8, 8, A, 8, 0, B, 8, 0, C, 8, 0, 0, None) == nj.NNJIT_EINVAL
+    vec = next(c["id"] for c in all_configs if c["family"] == "gemm_f32" and c["vec"] == 16)
+    rc = nj.nnjit_matmul_config(vec, 1, 4, 8, 8, A.data_ptr() + 4, 8, 0, B, 8, 0, C, 8, 0, 0, None)
+    assert rc == nj.NNJIT_EINVAL
+
+
+# --------------------------------------------------------------- metamorphic
+
+def test_power_of_two_scaling_bit_exact():
+    op = workloads.workload("bart_base_layer_seq128_f32")[2]
+    A, B = workloads.op_inputs("bart_base_layer_seq128_f32", 2)
+    C1 = gpu_matmul(A, B)
+    C2 = gpu_matmul((A * np.float32(8)).astype(np.float32), B)
+    assert np.array_equal(C2, 8 * C1), op.name
+
+
+def test_batch_slices_match_single_products(all_configs):
+    A, B = workloads.random_operands(80, 4, 96, 136, 72, "f32")
+    for c in all_configs:
+        if c["family"] != "gemm_f32" or c["vec"] != 16 or c["split"] not in (1, 4):
+            continue
+        Cb = gpu_matmul(A, B, cfg=c["id"])
+        for i in range(4):
+            assert np.array_equal(Cb[i], gpu_matmul(A[i], B[i], cfg=c["id"])), c["name"]
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16"])
+def test_transpose_identity(dt):
+    A, B = workloads.random_operands(81, 1, 160, 256, 200, dt)
+    C = gpu_matmul(A, B)
+    Ct = gpu_matmul(np.ascontiguousarray(B.T), np.ascontiguousarray(A.T)).T
+    R = oracle.matmul(A, B)
+    assert accept.check(C, R, A, B, dt)["ok"]
+    assert accept.check(Ct, R, A, B, dt)["ok"]
