@@ -1,0 +1,285 @@
+"""Benchmark of the lite-space tuned MatMul / BatchMatMul / GEMV path on one
+MI355X.
+
+A step is one pass over every product of a workload (default: the BART-base
+encoder layer at seq 128, fp32: fused QKV, out-proj, FFN-up, FFN-down
+linears and the two 12-head attention BatchMatMuls), each product through
+the C-ABI on its tuned configuration.  Before timing, every shape is tuned
+just in time (``nnjit_tune``), and the tune wall time is reported per shape.
+The timed steps replay a HIP graph captured from the eager ABI calls (the
+product is launch-bound at these sizes); the eager step time is reported
+beside it.  Inputs are resident in HBM when timing starts.
+
+Prints ONE JSON line.  ``--gpus N`` with N > 1 is refused: this build runs
+on one GPU.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import statistics
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import paper_2309_08978_amd as nj  # noqa: E402
+import workloads  # noqa: E402
+
+METRIC = "GFLOP/s (%MFMA peak) per GEMM shape; GB/s (%HBM) for GEMV; tune time"
+PEAK_TFLOPS = {"f32": 157.3, "f16": 2516.6}  # dense MFMA peaks of MI355X
+PEAK_HBM_GBS = 8000.0
+RIDGE = {dt: PEAK_TFLOPS[dt] * 1e12 / (PEAK_HBM_GBS * 1e9) for dt in PEAK_TFLOPS}
+COLD_BYTES = 1 << 30  # rotate >= 1 GiB of weights for bandwidth-bound workloads (MALL is 256 MB)
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def _kind(op):
+    return {"gemm": nj.NNJIT_KIND_GEMM, "batched": nj.NNJIT_KIND_BATCHED, "gemv": nj.NNJIT_KIND_GEMV}[op.kind]
+
+
+def _dt(op):
+    return nj.NNJIT_F16 if op.dtype == "f16" else nj.NNJIT_F32
+
+
+class OpRun:
+    """Device operands of one product and the call that runs it."""
+
+    def __init__(self, name, index, copies):
+        import torch
+        self.op = workloads.workload(name)[index]
+        A, B = workloads.op_inputs(name, index)
+        self.A = torch.from_numpy(A).to("cuda:0")
+        B0 = torch.from_numpy(B).to("cuda:0")
+        # the weight operand is rotated over `copies` replicas (cold HBM protocol)
+        self.Bs = [B0] + [B0.clone() for _ in range(copies - 1)]
+        op = self.op
+        shape = (op.batch, op.M, op.N) if op.batch > 1 else (op.M, op.N)
+        self.C = torch.empty(shape, dtype=torch.float32, device="cuda:0")
+
+    def call(self, copy=0, stream=None):
+        import torch
+        if stream is None:
+            stream = torch.cuda.current_stream()  # the capture stream while a graph is recorded
+        op = self.op
+        B = self.Bs[copy % len(self.Bs)]
+        if op.batch > 1:
+            rc = nj.nnjit_batched_matmul(op.batch, op.M, op.N, op.K, self.A, op.K, op.M * op.K, B, op.N,
+                                         op.K * op.N, self.C, op.N, op.M * op.N, _dt(op), stream)
+        else:
+            rc = nj.nnjit_matmul(op.M, op.N, op.K, self.A, op.K, B, op.N, self.C, op.N, _dt(op), stream)
+        if rc != 0:
+            raise nj.NnjitError(rc, nj.nnjit_last_error())
+
+
+def roofline_of(op, us):
+    dt = op.dtype
+    ai = op.flops / op.bytes
+    if ai >= RIDGE[dt]:
+        achieved = op.flops / (us * 1e-6) / 1e12
+        return {"bound": "mfma", "achieved": achieved, "peak": PEAK_TFLOPS[dt], "unit": "TFLOP/s",
+                "frac": achieved / PEAK_TFLOPS[dt], "traffic": None}
+    achieved = op.bytes / (us * 1e-6) / 1e9
+    return {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": achieved / PEAK_HBM_GBS, "traffic": None}
+
+
+def cpu_baseline(name, budget_s: float):
+    """The oracle (CPU, fp64) on the same workload: whole steps, repeated
+    until about `budget_s` seconds of CPU work have run (at least one step)."""
+    import oracle
+    ops = workloads.workload(name)
+    inputs = []
+    flops = 0
+    for i, op in enumerate(ops):
+        if op.flops > 5e9:
+            continue  # larger products are left out of the CPU sample
+        inputs.append(workloads.op_inputs(name, i))
+        flops += op.flops
+    oracle.default()
+    t0 = time.perf_counter()
+    steps = 0
+    while True:
+        for A, B in inputs:
+            oracle.matmul(A, B)
+        steps += 1
+        if time.perf_counter() - t0 >= budget_s or steps >= 50:
+            break
+    dt = time.perf_counter() - t0
+    n_ops = len(inputs)
+    return {"value": flops * steps / dt / 1e9, "unit": "GFLOP/s", "cores": oracle.max_threads(), "kind": "oracle",
+            "sample": f"{steps} full step(s) of {n_ops}/{len(ops)} products ({flops / 1e9:.3f} GFLOP each step), "
+                      f"fp64 triple loop, {dt:.1f} s"}
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="bart_base_layer_seq128_f32", choices=sorted(workloads.WORKLOADS))
+    ap.add_argument("--kernel-reps", type=int, default=50, help="event-timed launches per product")
+    ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle work for cpu_baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--eager", action="store_true", help="time eager ABI calls instead of the graph replay")
+    args = ap.parse_args(argv)
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}, WORLD_SIZE {world}); "
+              "this build has no multi-GPU path", file=sys.stderr)
+        return 2
+
+    import torch
+    if not torch.cuda.is_available():
+        print("no GPU available", file=sys.stderr)
+        return 3
+    nj.load()
+    torch.cuda.set_device(0)
+    name = args.workload
+    ops = workloads.workload(name)
+    log(f"[bench] workload {name}: {len(ops)} products")
+
+    weight_bytes = sum(op.batch * op.K * op.N * op.elt for op in ops)
+    cold = all(op.kind == "gemv" for op in ops)
+    copies = max(1, math.ceil(COLD_BYTES / weight_bytes)) if cold else 1
+    runs = [OpRun(name, i, copies) for i in range(len(ops))]
+    torch.cuda.synchronize()
+
+    # just-in-time tuning of every shape
+    tunes = []
+    for r in runs:
+        op = r.op
+        t0 = time.perf_counter()
+        if op.batch > 1:
+            cfg = nj.check(nj.nnjit_tune_batched(op.batch, op.M, op.N, op.K, _dt(op)))
+        else:
+            cfg = nj.check(nj.nnjit_tune(op.M, op.N, op.K, _dt(op)))
+        host_ms = (time.perf_counter() - t0) * 1e3
+        st = nj.nnjit_last_tune_stats()
+        info = nj.nnjit_config_info(cfg)
+        tunes.append({"op": op.name, "cfg": cfg, "tune_ms": round(st["wall_ms"], 1), "host_ms": round(host_ms, 1),
+                      "lite": st["n_lite"], "timed": st["n_timed"], "aborted": st["n_aborted"],
+                      "best_us": round(st["best_us"], 3), "default_us": round(st["default_us"], 3),
+                      "config": info.split(" ", 2)[2].split(" threads=")[0]})
+        log(f"[bench] tuned {op.name}: {tunes[-1]}")
+
+    stream = torch.cuda.current_stream()
+
+    def step(k=0):
+        for r in runs:
+            r.call(k)
+
+    # eager warm-up (allocates split-K scratch) and eager timing
+    for k in range(args.warmup):
+        step(k)
+    torch.cuda.synchronize()
+    n_eager = max(1, min(args.steps, 200))
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for k in range(n_eager):
+        step(k)
+    e1.record()
+    torch.cuda.synchronize()
+    eager_ms = e0.elapsed_time(e1) / n_eager
+
+    # graph of `copies` consecutive steps (one replica of the weights each)
+    graph = None
+    if not args.eager:
+        g = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            for k in range(copies):
+                step(k)  # warm-up on the capture stream (its split-K scratch)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=side):
+            for k in range(copies):
+                step(k)
+        graph = g
+        for _ in range(max(1, args.warmup // copies)):
+            graph.replay()
+        torch.cuda.synchronize()
+
+    # timed region
+    replays = max(1, args.steps // copies) if graph is not None else args.steps
+    nsteps = replays * copies if graph is not None else args.steps
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record()
+    if graph is not None:
+        for _ in range(replays):
+            graph.replay()
+    else:
+        for k in range(args.steps):
+            step(k)
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = e0.elapsed_time(e1) / nsteps
+    total_flops = sum(op.flops for op in ops)
+    total_bytes = sum(op.bytes for op in ops)
+
+    # per-product kernel durations: each launch bracketed by HIP events on the
+    # stream it runs on (cold replicas for bandwidth-bound workloads)
+    per_op = []
+    for r in runs:
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.kernel_reps)]
+        for i, (a, b) in enumerate(evs):
+            a.record()
+            r.call(i)
+            b.record()
+        torch.cuda.synchronize()
+        ts = [a.elapsed_time(b) * 1e3 for a, b in evs]
+        us = statistics.mean(ts)
+        op = r.op
+        rl = roofline_of(op, us)
+        per_op.append({"op": op.name, "shape_MKN": [op.M, op.K, op.N], "batch": op.batch, "dtype": op.dtype,
+                       "us_mean": round(us, 3), "us_median": round(statistics.median(ts), 3),
+                       "gflops": round(op.flops / us / 1e3, 1), "pct_mfma_peak": round(100 * op.flops / us / 1e6 / PEAK_TFLOPS[op.dtype], 2),
+                       "gbs": round(op.bytes / us / 1e3, 1), "pct_hbm": round(100 * op.bytes / us / 1e3 / PEAK_HBM_GBS, 2),
+                       "bound": rl["bound"], "pct_roofline": round(100 * rl["frac"], 2)})
+    dom = max(range(len(runs)), key=lambda i: per_op[i]["us_mean"])
+    rl = roofline_of(runs[dom].op, per_op[dom]["us_mean"])
+    rl.update({"kernel_op": per_op[dom]["op"], "kernel_config": tunes[dom]["config"],
+               "per_launch": ("flops" if rl["bound"] == "mfma" else "bytes"),
+               "algorithmic": runs[dom].op.flops if rl["bound"] == "mfma" else runs[dom].op.bytes,
+               "avg_launch_us": per_op[dom]["us_mean"]})
+
+    value = total_flops / (ms_per_step * 1e-3) / 1e9
+    dt = ops[0].dtype
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "GFLOP/s", "n_gpus": 1, "steps": nsteps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": dt, "data": "synthetic",
+        "config": {"workload": name, "products": [[op.name, op.batch, op.M, op.K, op.N] for op in ops],
+                   "timing": "graph replay" if graph is not None else "eager ABI calls",
+                   "weight_replicas": copies},
+        "pct_mfma_peak": round(100 * value / 1e3 / PEAK_TFLOPS[dt], 2),
+        "gbs": round(total_bytes / (ms_per_step * 1e-3) / 1e9, 1),
+        "eager_ms_per_step": round(eager_ms, 5),
+        "wall_s": round(wall, 4),
+        "tune": tunes,
+        "tune_ms_max": max(t["tune_ms"] for t in tunes),
+        "per_op": per_op,
+        "roofline": rl,
+        "device": torch.cuda.get_device_name(0),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(name, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -39,7 +39,7 @@ template <> struct Mfma16<16> {
 __device__ __forceinline__ unsigned pack_lo(unsigned a, unsigned b) { return (a & 0xffffu) | (b << 16); }
 __device__ __forceinline__ unsigned pack_hi(unsigned a, unsigned b) { return (a >> 16) | (b & 0xffff0000u); }
 
-template <int MT, int NT, int WM, int WN, int MF, int ST, bool VEC>
+template <int MT, int NT, int WM, int WN, int MF, int ST, int PF, bool VEC>
 __global__ void __launch_bounds__(WM * WN * 64)
 gemm_f16_kernel(GemmParams p)
 {
@@ -85,32 +85,37 @@ gemm_f16_kernel(GemmParams p)
     const int M = p.M, N = p.N;
     const long long lda = p.lda, ldb = p.ldb;
 
-    u32x4 ra[LA];
-    u32x4 rb[LB][8];
+    // PF slabs in flight in registers (see the fp32 kernel)
+    u32x4 ra[PF][LA];
+    u32x4 rb[PF][LB][8];
 
-    auto ld8 = [&](const unsigned short *src, int nvalid) -> u32x4 {
-        // 8 halves from src; elements at or beyond nvalid read as +0
-        u32x4 v = {0u, 0u, 0u, 0u};
+    // 8 halves row[c .. c+7]; elements at or beyond lim, and whole chunks
+    // with okr false, are read from the zero buffer (address select only,
+    // see the fp32 kernel).
+    const unsigned short *zero = (const unsigned short *)p.zero;
+    auto ld8 = [&](const unsigned short *row, int c, int lim, bool okr) -> u32x4 {
+        u32x4 v;
         if constexpr (VEC) {
-            if (nvalid >= 8) v = *(const u32x4 *)src;
+            v = *(const u32x4 *)((okr && c < lim) ? row + c : zero);
         } else {
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
-                if (e < nvalid) v[e >> 1] |= (unsigned)src[e] << (16 * (e & 1));
+            for (int w = 0; w < 4; ++w) {
+                const unsigned lo = *((okr && c + 2 * w < lim) ? row + c + 2 * w : zero);
+                const unsigned hi = *((okr && c + 2 * w + 1 < lim) ? row + c + 2 * w + 1 : zero);
+                v[w] = lo | (hi << 16);
+            }
         }
         return v;
     };
 
-    auto gload = [&](int k0) {
+    auto gload = [&](int set, int k0) {
 #pragma unroll
         for (int l = 0; l < LA; ++l) {
             const int f = tid + l * NTHR;
             const int row = f >> 3, c = f & 7;
-            const int gm = m0 + row, gk = k0 + 8 * c;
-            u32x4 v = {0u, 0u, 0u, 0u};
-            if ((A8 % NTHR == 0 || f < A8) && gm < M && gk < kend)
-                v = ld8(A + (long long)gm * lda + gk, kend - gk);
-            ra[l] = v;
+            const int gm = m0 + row;
+            const bool okr = (A8 % NTHR == 0 || f < A8) && gm < M;
+            ra[set][l] = ld8(A + (long long)gm * lda, k0 + 8 * c, kend, okr);
         }
 #pragma unroll
         for (int l = 0; l < LB; ++l) {
@@ -120,21 +125,19 @@ gemm_f16_kernel(GemmParams p)
 #pragma unroll
             for (int r = 0; r < 8; ++r) {
                 const int gk = k0 + 8 * kb + r;
-                u32x4 v = {0u, 0u, 0u, 0u};
-                if ((BB % NTHR == 0 || f < BB) && gk < kend && gn < N)
-                    v = ld8(B + (long long)gk * ldb + gn, N - gn);
-                rb[l][r] = v;
+                const bool okr = (BB % NTHR == 0 || f < BB) && gk < kend;
+                rb[set][l][r] = ld8(B + (long long)gk * ldb, gn, N, okr);
             }
         }
     };
 
-    auto sstore = [&](int buf) {
+    auto sstore = [&](int set, int buf) {
 #pragma unroll
         for (int l = 0; l < LA; ++l) {
             const int f = tid + l * NTHR;
             if (A8 % NTHR == 0 || f < A8) {
                 const int row = f >> 3, c = f & 7;
-                As[buf][row * 8 + (c ^ (row & 7))] = ra[l];
+                As[buf][row * 8 + (c ^ (row & 7))] = ra[set][l];
             }
         }
 #pragma unroll
@@ -149,8 +152,8 @@ gemm_f16_kernel(GemmParams p)
                     u32x4 o;
 #pragma unroll
                     for (int w = 0; w < 4; ++w)
-                        o[w] = (c & 1) ? pack_hi(rb[l][2 * w][d], rb[l][2 * w + 1][d])
-                                       : pack_lo(rb[l][2 * w][d], rb[l][2 * w + 1][d]);
+                        o[w] = (c & 1) ? pack_hi(rb[set][l][2 * w][d], rb[set][l][2 * w + 1][d])
+                                       : pack_lo(rb[set][l][2 * w][d], rb[set][l][2 * w + 1][d]);
                     const int n = 8 * nb + c;
                     Bt[buf][n * 8 + (kb ^ c)] = o;  // (n & 7) == c
                 }
@@ -188,27 +191,37 @@ gemm_f16_kernel(GemmParams p)
         }
     };
 
-    if constexpr (ST == 2) {
-        if (nk > 0) {
-            gload(kbeg);
-            sstore(0);
-        }
-        __syncthreads();
-        for (int it = 0; it < nk; ++it) {
-            const int cur = it & 1;
-            if (it + 1 < nk) gload(kbeg + (it + 1) * KT);
-            compute(cur);
-            if (it + 1 < nk) sstore(cur ^ 1);
+    // Software pipeline.  Slab `it` is loaded into staging set it % PF at
+    // iteration it - PF, stored to LDS buffer it & 1 at iteration it - 1 and
+    // multiplied at iteration it.  The loop is unrolled by PF so every set
+    // index is a compile-time constant, and its loads and LDS stores are
+    // unconditional (slabs past the end read the zero buffer) so the
+    // compiler can keep PF slabs in flight; only the matrix-core work is
+    // skipped past the end.
+    if (nk > 0) {
+#pragma unroll
+        for (int u = 0; u < PF; ++u) gload(u, kbeg + u * KT);
+        if constexpr (ST == 2) {
+            sstore(0, 0);
             __syncthreads();
         }
-    } else {
-        if (nk > 0) gload(kbeg);
-        for (int it = 0; it < nk; ++it) {
-            __syncthreads();
-            sstore(0);
-            __syncthreads();
-            if (it + 1 < nk) gload(kbeg + (it + 1) * KT);
-            compute(0);
+        for (int it0 = 0; it0 < nk; it0 += PF) {
+#pragma unroll
+            for (int u = 0; u < PF; ++u) {
+                const int it = it0 + u;
+                if constexpr (ST == 2) {
+                    gload(u, kbeg + (it + PF) * KT);
+                    if (it < nk) compute(it & 1);
+                    sstore((u + 1) % PF, (it + 1) & 1);
+                    __syncthreads();
+                } else {
+                    __syncthreads();
+                    sstore(u, 0);
+                    __syncthreads();
+                    gload(u, kbeg + (it + PF) * KT);
+                    if (it < nk) compute(0);
+                }
+            }
         }
     }
 
@@ -226,39 +239,24 @@ gemm_f16_kernel(GemmParams p)
         return;
     }
 
-    const long long tile_id = (long long)z * tiles + tile;
-    float *part = p.ws + (tile_id * p.S + s) * (long long)(MT * NT);
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-#pragma unroll
-            for (int r = 0; r < I::NR; ++r)
-                part[((i * FN + j) * I::NR + r) * NTHR + tid] = acc[i][j][r];
-    if (!splitk_arrive_last(&p.counters[tile_id], p.S)) return;
-    const float *base = p.ws + tile_id * p.S * (long long)(MT * NT);
+    // split-K: this split's partial tile goes to ws[s][z][row][col]; a
+    // separate kernel sums the S partials in split order
+    float *part = p.ws + ((long long)s * p.batch + z) * (long long)M * N;
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
 #pragma unroll
             for (int r = 0; r < I::NR; ++r) {
-                const int idx = ((i * FN + j) * I::NR + r) * NTHR + tid;
-                float v = 0.f;
-                for (int t = 0; t < p.S; ++t) {
-                    const float x = (t == s) ? acc[i][j][r] : base[(long long)t * (MT * NT) + idx];
-                    v = (t == 0) ? x : v + x;
-                }
                 const int row = rbase + i * MF + I::row_of(r, lg), col = cbase + j * MF;
-                if (row < M && col < N) C[(long long)row * p.ldc + col] = v;
+                if (row < M && col < N) part[(long long)row * N + col] = acc[i][j][r];
             }
-    if (tid == 0) p.counters[tile_id] = 0u;
 }
 
-template <int MT, int NT, int WM, int WN, int MF, int ST, bool VEC>
+template <int MT, int NT, int WM, int WN, int MF, int ST, int PF, bool VEC>
 static hipError_t launch_gemm_f16(const void *params, dim3 grid, hipStream_t stream)
 {
-    hipLaunchKernelGGL((gemm_f16_kernel<MT, NT, WM, WN, MF, ST, VEC>), grid, dim3(WM * WN * 64), 0, stream,
+    hipLaunchKernelGGL((gemm_f16_kernel<MT, NT, WM, WN, MF, ST, PF, VEC>), grid, dim3(WM * WN * 64), 0, stream,
                        *(const GemmParams *)params);
     return hipGetLastError();
 }
@@ -267,48 +265,54 @@ static hipError_t launch_gemm_f16(const void *params, dim3 grid, hipStream_t str
 // one K step of A and B fragments (4 VGPRs per 8 halves), the staging
 // registers of the global->LDS copy (B needs eight 128-bit rows per 8x8
 // block), and a fixed overhead.
-constexpr int est_regs_f16(int mt, int nt, int wm, int wn, int mf) {
+constexpr int est_regs_f16(int mt, int nt, int wm, int wn, int mf, int pf) {
     return (mt / wm) * (nt / wn) / 64 + 4 * ((mt / wm) / mf) + 4 * ((nt / wn) / mf) +
-           4 * ((mt * 8 + wm * wn * 64 - 1) / (wm * wn * 64)) +
-           32 * ((nt + wm * wn * 64 - 1) / (wm * wn * 64)) + 28;
+           pf * (4 * ((mt * 8 + wm * wn * 64 - 1) / (wm * wn * 64)) +
+                 32 * ((nt + wm * wn * 64 - 1) / (wm * wn * 64))) + 28;
 }
 constexpr int lds_f16(int mt, int nt, int st) { return st * (mt + nt) * 128; }
 
-#define NNJIT_F16_VARIANT(MT, NT, WM, WN, MF, ST, VEC)                                                      \
-    {"gemm_f16_" #MT "x" #NT "x64_w" #WM "x" #WN "_m" #MF "_s" #ST "_v" #VEC, FAM_GEMM_F16, MF,                \
-     (MF == 32 ? 16 : 32), MT, NT, 64, WM, WN, ST, (VEC ? 16 : 2), 0, 0, WM * WN * 64, lds_f16(MT, NT, ST),   \
-     est_regs_f16(MT, NT, WM, WN, MF), (const void *)&gemm_f16_kernel<MT, NT, WM, WN, MF, ST, VEC>,         \
-     &launch_gemm_f16<MT, NT, WM, WN, MF, ST, VEC>}
+#define NNJIT_F16_VARIANT(MT, NT, WM, WN, MF, ST, PF, VEC)                                                  \
+    {"gemm_f16_" #MT "x" #NT "x64_w" #WM "x" #WN "_m" #MF "_s" #ST "_p" #PF "_v" #VEC, FAM_GEMM_F16, MF,        \
+     (MF == 32 ? 16 : 32), MT, NT, 64, WM, WN, ST, PF, (VEC ? 16 : 2), 0, 0, WM * WN * 64,                    \
+     lds_f16(MT, NT, ST), est_regs_f16(MT, NT, WM, WN, MF, PF),                                                \
+     (const void *)&gemm_f16_kernel<MT, NT, WM, WN, MF, ST, PF, VEC>, &launch_gemm_f16<MT, NT, WM, WN, MF, ST, PF, VEC>}
 
 // The compiled fp16 configurations (K slab fixed at 64: 128-byte rows).
 #define NNJIT_F16_LIST(X) \
-    X(256, 256, 2, 2, 32, 2, true) \
-    X(256, 128, 2, 2, 32, 2, true) \
-    X(128, 256, 2, 2, 32, 2, true) \
-    X(256, 128, 4, 2, 32, 2, true) \
-    X(128, 256, 2, 4, 32, 2, true) \
-    X(128, 128, 2, 2, 32, 2, true) \
-    X(128, 128, 1, 2, 32, 2, true) \
-    X(128, 128, 2, 1, 32, 2, true) \
-    X(128, 128, 2, 2, 16, 2, true) \
-    X(128, 128, 2, 2, 32, 1, true) \
-    X(128, 64, 2, 1, 32, 2, true) \
-    X(128, 64, 2, 2, 32, 2, true) \
-    X(64, 128, 1, 2, 32, 2, true) \
-    X(64, 128, 2, 2, 32, 2, true) \
-    X(64, 64, 1, 1, 32, 2, true) \
-    X(64, 64, 2, 2, 32, 2, true) \
-    X(64, 64, 2, 2, 16, 2, true) \
-    X(32, 64, 1, 2, 32, 2, true) \
-    X(64, 32, 2, 1, 32, 2, true) \
-    X(32, 32, 1, 1, 32, 2, true) \
-    X(32, 32, 2, 2, 16, 2, true) \
-    X(16, 64, 1, 4, 16, 2, true) \
-    X(64, 64, 2, 2, 32, 2, false) \
-    X(32, 32, 1, 1, 32, 2, false) \
+    X(256, 256, 2, 2, 32, 2, 1, true) \
+    X(256, 128, 2, 2, 32, 2, 1, true) \
+    X(128, 256, 2, 2, 32, 2, 1, true) \
+    X(256, 128, 4, 2, 32, 2, 1, true) \
+    X(256, 128, 4, 2, 32, 2, 2, true) \
+    X(128, 256, 2, 4, 32, 2, 1, true) \
+    X(128, 128, 2, 2, 32, 2, 1, true) \
+    X(128, 128, 2, 2, 32, 2, 2, true) \
+    X(128, 128, 1, 2, 32, 2, 1, true) \
+    X(128, 128, 2, 1, 32, 2, 1, true) \
+    X(128, 128, 2, 2, 16, 2, 1, true) \
+    X(128, 128, 2, 2, 32, 1, 1, true) \
+    X(128, 128, 2, 2, 32, 1, 2, true) \
+    X(128, 64, 2, 1, 32, 2, 1, true) \
+    X(128, 64, 2, 2, 32, 2, 1, true) \
+    X(128, 64, 2, 2, 32, 2, 2, true) \
+    X(64, 128, 1, 2, 32, 2, 1, true) \
+    X(64, 128, 2, 2, 32, 2, 1, true) \
+    X(64, 128, 2, 2, 32, 2, 2, true) \
+    X(64, 64, 1, 1, 32, 2, 1, true) \
+    X(64, 64, 2, 2, 32, 2, 1, true) \
+    X(64, 64, 2, 2, 32, 2, 2, true) \
+    X(64, 64, 2, 2, 16, 2, 2, true) \
+    X(32, 64, 1, 2, 32, 2, 2, true) \
+    X(64, 32, 2, 1, 32, 2, 2, true) \
+    X(32, 32, 1, 1, 32, 2, 2, true) \
+    X(32, 32, 2, 2, 16, 2, 2, true) \
+    X(16, 64, 1, 4, 16, 2, 2, true) \
+    X(64, 64, 2, 2, 32, 2, 1, false) \
+    X(32, 32, 1, 1, 32, 2, 1, false)
 
-#define NNJIT_F16_INST(MT, NT, WM, WN, MF, ST, VEC) \
-    template __global__ void gemm_f16_kernel<MT, NT, WM, WN, MF, ST, VEC>(GemmParams);
+#define NNJIT_F16_INST(MT, NT, WM, WN, MF, ST, PF, VEC) \
+    template __global__ void gemm_f16_kernel<MT, NT, WM, WN, MF, ST, PF, VEC>(GemmParams);
 NNJIT_F16_LIST(NNJIT_F16_INST)
 
 #if !defined(__HIP_DEVICE_COMPILE__)

@@ -39,7 +39,7 @@ template <> struct Mfma32<16> {
     __device__ static __forceinline__ int row_of(int r, int g) { return 4 * g + r; }
 };
 
-template <int MT, int NT, int KT, int WM, int WN, int MF, int ST, bool VEC>
+template <int MT, int NT, int KT, int WM, int WN, int MF, int ST, int PF, bool VEC>
 __global__ void __launch_bounds__(WM * WN * 64)
 gemm_f32_kernel(GemmParams p)
 {
@@ -88,54 +88,58 @@ gemm_f32_kernel(GemmParams p)
     const int M = p.M, N = p.N;
     const long long lda = p.lda, ldb = p.ldb;
 
-    f32x4 ra[LA], rb[LB];
+    // PF slabs are in flight in registers (a ring of PF staging sets), so
+    // the loads of slab it+PF are issued while slab it is computed
+    f32x4 ra[PF][LA], rb[PF][LB];
 
-    auto gload = [&](int k0) {
+    // Loads are branch-free and never followed by value-dependent work:
+    // an out-of-range element is read from a zero-filled buffer instead
+    // (only the address is selected).  A divergent branch around a load, or
+    // a select on its result, would make the compiler wait for every
+    // outstanding load before the next slab's loads are issued.
+    const float *zero = (const float *)p.zero;
+    auto gload = [&](int set, int k0) {
 #pragma unroll
         for (int l = 0; l < LA; ++l) {
             const int f = tid + l * NTHR;
             const int row = f / (KT / 4), c4 = f % (KT / 4);
             const int gm = m0 + row, gk = k0 + c4 * 4;
-            f32x4 v = {0.f, 0.f, 0.f, 0.f};
-            if ((A4 % NTHR == 0 || f < A4) && gm < M) {
-                const float *src = A + (long long)gm * lda + gk;
-                if constexpr (VEC) {
-                    if (gk < kend) v = *(const f32x4 *)src;
-                } else {
+            const bool okr = (A4 % NTHR == 0 || f < A4) && gm < M;
+            const float *src = A + (long long)gm * lda + gk;
+            f32x4 v;
+            if constexpr (VEC) {
+                v = *(const f32x4 *)((okr && gk < kend) ? src : zero);
+            } else {
 #pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        if (gk + e < kend) v[e] = src[e];
-                }
+                for (int e = 0; e < 4; ++e) v[e] = *((okr && gk + e < kend) ? src + e : zero);
             }
-            ra[l] = v;
+            ra[set][l] = v;
         }
 #pragma unroll
         for (int l = 0; l < LB; ++l) {
             const int f = tid + l * NTHR;
             const int row = f / (NT / 4), c4 = f % (NT / 4);
             const int gk = k0 + row, gn = n0 + c4 * 4;
-            f32x4 v = {0.f, 0.f, 0.f, 0.f};
-            if ((B4 % NTHR == 0 || f < B4) && gk < kend) {
-                const float *src = B + (long long)gk * ldb + gn;
-                if constexpr (VEC) {
-                    if (gn < N) v = *(const f32x4 *)src;
-                } else {
+            const bool okr = (B4 % NTHR == 0 || f < B4) && gk < kend;
+            const float *src = B + (long long)gk * ldb + gn;
+            f32x4 v;
+            if constexpr (VEC) {
+                v = *(const f32x4 *)((okr && gn < N) ? src : zero);
+            } else {
 #pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        if (gn + e < N) v[e] = src[e];
-                }
+                for (int e = 0; e < 4; ++e) v[e] = *((okr && gn + e < N) ? src + e : zero);
             }
-            rb[l] = v;
+            rb[set][l] = v;
         }
     };
 
-    auto sstore = [&](int buf) {
+    auto sstore = [&](int set, int buf) {
 #pragma unroll
         for (int l = 0; l < LA; ++l) {
             const int f = tid + l * NTHR;
             if (A4 % NTHR == 0 || f < A4) {
                 const int row = f / (KT / 4), c4 = f % (KT / 4);
-                *(f32x4 *)&As[buf][row * SA + c4 * 4] = ra[l];
+                *(f32x4 *)&As[buf][row * SA + c4 * 4] = ra[set][l];
             }
         }
 #pragma unroll
@@ -143,7 +147,7 @@ gemm_f32_kernel(GemmParams p)
             const int f = tid + l * NTHR;
             if (B4 % NTHR == 0 || f < B4) {
                 const int row = f / (NT / 4), c4 = f % (NT / 4);
-                *(f32x4 *)&Bs[buf][row * SB + c4 * 4] = rb[l];
+                *(f32x4 *)&Bs[buf][row * SB + c4 * 4] = rb[set][l];
             }
         }
     };
@@ -177,27 +181,37 @@ gemm_f32_kernel(GemmParams p)
         }
     };
 
-    if constexpr (ST == 2) {
-        if (nk > 0) {
-            gload(kbeg);
-            sstore(0);
-        }
-        __syncthreads();
-        for (int it = 0; it < nk; ++it) {
-            const int cur = it & 1;
-            if (it + 1 < nk) gload(kbeg + (it + 1) * KT);
-            compute(cur);
-            if (it + 1 < nk) sstore(cur ^ 1);
+    // Software pipeline.  Slab `it` is loaded into staging set it % PF at
+    // iteration it - PF, stored to LDS buffer it & 1 at iteration it - 1 and
+    // multiplied at iteration it.  The loop is unrolled by PF so every set
+    // index is a compile-time constant, and its loads and LDS stores are
+    // unconditional (slabs past the end read the zero buffer) so the
+    // compiler can keep PF slabs in flight; only the matrix-core work is
+    // skipped past the end.
+    if (nk > 0) {
+#pragma unroll
+        for (int u = 0; u < PF; ++u) gload(u, kbeg + u * KT);
+        if constexpr (ST == 2) {
+            sstore(0, 0);
             __syncthreads();
         }
-    } else {
-        if (nk > 0) gload(kbeg);
-        for (int it = 0; it < nk; ++it) {
-            __syncthreads();
-            sstore(0);
-            __syncthreads();
-            if (it + 1 < nk) gload(kbeg + (it + 1) * KT);
-            compute(0);
+        for (int it0 = 0; it0 < nk; it0 += PF) {
+#pragma unroll
+            for (int u = 0; u < PF; ++u) {
+                const int it = it0 + u;
+                if constexpr (ST == 2) {
+                    gload(u, kbeg + (it + PF) * KT);
+                    if (it < nk) compute(it & 1);
+                    sstore((u + 1) % PF, (it + 1) & 1);
+                    __syncthreads();
+                } else {
+                    __syncthreads();
+                    sstore(u, 0);
+                    __syncthreads();
+                    gload(u, kbeg + (it + PF) * KT);
+                    if (it < nk) compute(0);
+                }
+            }
         }
     }
 
@@ -215,41 +229,24 @@ gemm_f32_kernel(GemmParams p)
         return;
     }
 
-    // split-K: store the partial tile (coalesced, one register index per
-    // 64-lane row), the last arriving split sums all partials in split order.
-    const long long tile_id = (long long)z * tiles + tile;
-    float *part = p.ws + (tile_id * p.S + s) * (long long)(MT * NT);
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-#pragma unroll
-            for (int r = 0; r < I::NR; ++r)
-                part[((i * FN + j) * I::NR + r) * NTHR + tid] = acc[i][j][r];
-    if (!splitk_arrive_last(&p.counters[tile_id], p.S)) return;
-    const float *base = p.ws + tile_id * p.S * (long long)(MT * NT);
+    // split-K: this split's partial tile goes to ws[s][z][row][col]; a
+    // separate kernel sums the S partials in split order
+    float *part = p.ws + ((long long)s * p.batch + z) * (long long)M * N;
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
 #pragma unroll
             for (int r = 0; r < I::NR; ++r) {
-                const int idx = ((i * FN + j) * I::NR + r) * NTHR + tid;
-                float v = 0.f;
-                for (int t = 0; t < p.S; ++t) {
-                    const float x = (t == s) ? acc[i][j][r] : base[(long long)t * (MT * NT) + idx];
-                    v = (t == 0) ? x : v + x;
-                }
                 const int row = rbase + i * MF + I::row_of(r, lg), col = cbase + j * MF;
-                if (row < M && col < N) C[(long long)row * p.ldc + col] = v;
+                if (row < M && col < N) part[(long long)row * N + col] = acc[i][j][r];
             }
-    if (tid == 0) p.counters[tile_id] = 0u;
 }
 
-template <int MT, int NT, int KT, int WM, int WN, int MF, int ST, bool VEC>
+template <int MT, int NT, int KT, int WM, int WN, int MF, int ST, int PF, bool VEC>
 static hipError_t launch_gemm_f32(const void *params, dim3 grid, hipStream_t stream)
 {
-    hipLaunchKernelGGL((gemm_f32_kernel<MT, NT, KT, WM, WN, MF, ST, VEC>), grid, dim3(WM * WN * 64), 0,
+    hipLaunchKernelGGL((gemm_f32_kernel<MT, NT, KT, WM, WN, MF, ST, PF, VEC>), grid, dim3(WM * WN * 64), 0,
                        stream, *(const GemmParams *)params);
     return hipGetLastError();
 }
@@ -258,60 +255,79 @@ static hipError_t launch_gemm_f32(const void *params, dim3 grid, hipStream_t str
 // for one lane: the accumulator tile (x0*y0 over 64 lanes), the A and B
 // fragments of one K step (r0*y0, r0*x0), the global->LDS staging registers,
 // and a fixed overhead for addresses and indices.
-constexpr int est_regs_f32(int mt, int nt, int kt, int wm, int wn, int mf) {
+constexpr int est_regs_f32(int mt, int nt, int kt, int wm, int wn, int mf, int pf) {
     return (mt / wm) * (nt / wn) / 64 + 4 * ((mt / wm) / mf) + ((nt / wn) / mf) +
-           (mt * kt + kt * nt) / (wm * wn * 64) + 28;
+           pf * ((mt * kt + kt * nt) / (wm * wn * 64)) + 28;
 }
 constexpr int lds_f32(int mt, int nt, int kt, int st) { return st * (mt * (kt + 4) + kt * (nt + 4)) * 4; }
 
-#define NNJIT_F32_VARIANT(MT, NT, KT, WM, WN, MF, ST, VEC)                                              \
-    {"gemm_f32_" #MT "x" #NT "x" #KT "_w" #WM "x" #WN "_m" #MF "_s" #ST "_v" #VEC, FAM_GEMM_F32, MF,         \
-     (MF == 32 ? 2 : 4), MT, NT, KT, WM, WN, ST, (VEC ? 16 : 4), 0, 0, WM * WN * 64, lds_f32(MT, NT, KT, ST), \
-     est_regs_f32(MT, NT, KT, WM, WN, MF),                                                              \
-     (const void *)&gemm_f32_kernel<MT, NT, KT, WM, WN, MF, ST, VEC>,                                   \
-     &launch_gemm_f32<MT, NT, KT, WM, WN, MF, ST, VEC>}
+#define NNJIT_F32_VARIANT(MT, NT, KT, WM, WN, MF, ST, PF, VEC)                                          \
+    {"gemm_f32_" #MT "x" #NT "x" #KT "_w" #WM "x" #WN "_m" #MF "_s" #ST "_p" #PF "_v" #VEC, FAM_GEMM_F32, MF, \
+     (MF == 32 ? 2 : 4), MT, NT, KT, WM, WN, ST, PF, (VEC ? 16 : 4), 0, 0, WM * WN * 64,                   \
+     lds_f32(MT, NT, KT, ST), est_regs_f32(MT, NT, KT, WM, WN, MF, PF),                                     \
+     (const void *)&gemm_f32_kernel<MT, NT, KT, WM, WN, MF, ST, PF, VEC>,                                   \
+     &launch_gemm_f32<MT, NT, KT, WM, WN, MF, ST, PF, VEC>}
 
 // The compiled fp32 configurations (the family's full set; the lite space of
 // a shape is a pruned, ordered subset).  Tile edges are powers of two
 // (heuristic 2).  The last entries load element by element, for operands
 // that are not 16-byte aligned.
 #define NNJIT_F32_LIST(X) \
-    X(256, 128, 16, 2, 2, 32, 2, true) \
-    X(128, 256, 16, 2, 2, 32, 2, true) \
-    X(256, 256, 16, 2, 2, 32, 2, true) \
-    X(256, 128, 16, 4, 2, 32, 2, true) \
-    X(128, 128, 16, 2, 2, 32, 2, true) \
-    X(128, 128, 32, 2, 2, 32, 2, true) \
-    X(128, 128, 16, 2, 2, 32, 1, true) \
-    X(128, 128, 16, 1, 2, 32, 2, true) \
-    X(128, 64, 16, 2, 1, 32, 2, true) \
-    X(128, 64, 16, 2, 2, 32, 2, true) \
-    X(128, 64, 32, 2, 2, 32, 2, true) \
-    X(64, 128, 16, 1, 2, 32, 2, true) \
-    X(64, 128, 16, 2, 2, 32, 2, true) \
-    X(64, 128, 32, 2, 2, 32, 2, true) \
-    X(64, 64, 16, 1, 1, 32, 2, true) \
-    X(64, 64, 16, 2, 2, 32, 2, true) \
-    X(64, 64, 32, 2, 2, 32, 2, true) \
-    X(64, 64, 16, 2, 2, 16, 2, true) \
-    X(64, 64, 32, 2, 2, 16, 2, true) \
-    X(64, 64, 16, 2, 2, 32, 1, true) \
-    X(32, 64, 16, 1, 2, 32, 2, true) \
-    X(32, 64, 32, 1, 2, 32, 2, true) \
-    X(64, 32, 16, 2, 1, 32, 2, true) \
-    X(64, 32, 32, 2, 1, 32, 2, true) \
-    X(32, 32, 16, 1, 1, 32, 2, true) \
-    X(32, 32, 32, 1, 1, 32, 2, true) \
-    X(32, 32, 16, 2, 2, 16, 2, true) \
-    X(32, 64, 16, 2, 2, 16, 2, true) \
-    X(64, 32, 16, 2, 2, 16, 2, true) \
-    X(16, 64, 16, 1, 2, 16, 2, true) \
-    X(16, 64, 32, 1, 4, 16, 2, true) \
-    X(64, 64, 16, 2, 2, 32, 2, false) \
-    X(32, 32, 16, 1, 1, 32, 2, false) \
+    X(256, 128, 16, 2, 2, 32, 2, 1, true) \
+    X(128, 256, 16, 2, 2, 32, 2, 1, true) \
+    X(256, 256, 16, 2, 2, 32, 2, 1, true) \
+    X(256, 128, 16, 4, 2, 32, 2, 1, true) \
+    X(256, 128, 16, 4, 2, 32, 2, 2, true) \
+    X(128, 128, 16, 2, 2, 32, 2, 1, true) \
+    X(128, 128, 16, 2, 2, 32, 2, 2, true) \
+    X(128, 128, 32, 2, 2, 32, 2, 1, true) \
+    X(128, 128, 16, 2, 2, 32, 1, 1, true) \
+    X(128, 128, 16, 1, 2, 32, 2, 1, true) \
+    X(128, 64, 16, 2, 2, 32, 2, 1, true) \
+    X(128, 64, 16, 2, 2, 32, 2, 2, true) \
+    X(128, 64, 32, 2, 2, 32, 2, 2, true) \
+    X(64, 128, 16, 2, 2, 32, 2, 1, true) \
+    X(64, 128, 16, 2, 2, 32, 2, 2, true) \
+    X(64, 128, 32, 2, 2, 32, 2, 2, true) \
+    X(64, 64, 16, 2, 2, 32, 2, 1, true) \
+    X(64, 64, 16, 2, 2, 32, 2, 2, true) \
+    X(64, 64, 16, 2, 2, 32, 2, 4, true) \
+    X(64, 64, 32, 2, 2, 32, 2, 2, true) \
+    X(64, 64, 64, 2, 2, 32, 2, 1, true) \
+    X(64, 64, 64, 2, 2, 32, 2, 2, true) \
+    X(64, 64, 64, 2, 2, 16, 2, 2, true) \
+    X(128, 64, 64, 2, 2, 32, 2, 2, true) \
+    X(64, 128, 64, 2, 2, 32, 2, 2, true) \
+    X(32, 64, 64, 1, 2, 32, 2, 2, true) \
+    X(64, 32, 64, 2, 1, 32, 2, 2, true) \
+    X(32, 64, 64, 2, 2, 16, 2, 2, true) \
+    X(64, 32, 64, 2, 2, 16, 2, 2, true) \
+    X(32, 32, 64, 2, 2, 16, 2, 2, true) \
+    X(32, 32, 64, 1, 1, 32, 2, 2, true) \
+    X(64, 64, 16, 2, 2, 16, 2, 2, true) \
+    X(64, 64, 16, 2, 2, 32, 1, 1, true) \
+    X(64, 64, 16, 2, 2, 32, 1, 2, true) \
+    X(64, 64, 16, 1, 1, 32, 2, 2, true) \
+    X(32, 64, 16, 1, 2, 32, 2, 2, true) \
+    X(32, 64, 32, 1, 2, 32, 2, 2, true) \
+    X(64, 32, 16, 2, 1, 32, 2, 2, true) \
+    X(64, 32, 32, 2, 1, 32, 2, 2, true) \
+    X(32, 32, 16, 1, 1, 32, 2, 2, true) \
+    X(32, 32, 32, 1, 1, 32, 2, 2, true) \
+    X(32, 32, 16, 2, 2, 16, 2, 1, true) \
+    X(32, 32, 16, 2, 2, 16, 2, 2, true) \
+    X(32, 32, 16, 2, 2, 16, 2, 4, true) \
+    X(32, 64, 16, 2, 2, 16, 2, 2, true) \
+    X(32, 64, 16, 2, 2, 16, 2, 4, true) \
+    X(64, 32, 16, 2, 2, 16, 2, 2, true) \
+    X(64, 32, 16, 2, 2, 16, 2, 4, true) \
+    X(16, 64, 16, 1, 2, 16, 2, 2, true) \
+    X(16, 64, 32, 1, 4, 16, 2, 2, true) \
+    X(64, 64, 16, 2, 2, 32, 2, 1, false) \
+    X(32, 32, 16, 1, 1, 32, 2, 1, false)
 
-#define NNJIT_F32_INST(MT, NT, KT, WM, WN, MF, ST, VEC) \
-    template __global__ void gemm_f32_kernel<MT, NT, KT, WM, WN, MF, ST, VEC>(GemmParams);
+#define NNJIT_F32_INST(MT, NT, KT, WM, WN, MF, ST, PF, VEC) \
+    template __global__ void gemm_f32_kernel<MT, NT, KT, WM, WN, MF, ST, PF, VEC>(GemmParams);
 NNJIT_F32_LIST(NNJIT_F32_INST)
 
 #if !defined(__HIP_DEVICE_COMPILE__)

@@ -11,8 +11,8 @@
 // Reduction over k, in a fixed order (deterministic):
 //   1. across the row slots of a wave: butterfly over lane xor L, 2L, ...
 //   2. across the waves of the workgroup: through LDS, wave 0 sums in order;
-//   3. across the S workgroups of a segment: partials in device memory, the
-//      last workgroup to arrive sums them in split order.
+//   3. across the S workgroups of a segment: partials in device memory,
+//      summed in split order by a second, elementwise kernel.
 #include "kcommon.h"
 
 namespace nnjit {
@@ -138,26 +138,12 @@ gemv_kernel(GemvParams p)
         return;
     }
 
-    // 3. split-K partials, summed in split order by the last arrival
+    // 3. split-K: this split's partial row, summed in split order by the
+    //    reduction kernel
     if (tid < L)
 #pragma unroll
         for (int e = 0; e < V; ++e)
             if (n + e < N) p.ws[(long long)s * N + n + e] = acc[e];
-    if (!splitk_arrive_last(&p.counters[seg], p.S)) return;
-    if (tid < L) {
-#pragma unroll
-        for (int e = 0; e < V; ++e) {
-            if (n + e < N) {
-                float v = 0.f;
-                for (int t = 0; t < p.S; ++t) {
-                    const float x = (t == s) ? acc[e] : p.ws[(long long)t * N + n + e];
-                    v = (t == 0) ? x : v + x;
-                }
-                p.y[n + e] = v;
-            }
-        }
-    }
-    if (tid == 0) p.counters[seg] = 0u;
 }
 
 template <typename T, int L, int NTHR, int U, bool VEC>
@@ -174,7 +160,7 @@ constexpr int est_regs_gemv(int v, int u) { return v + 5 * u + 24; }
 constexpr int lds_gemv(int nthr, int l, int v) { return nthr > 64 ? (nthr / 64) * l * v * 4 + 4 : 4; }
 
 #define NNJIT_GEMV_VARIANT(T, FAMV, V, L, NTHR, U, VEC)                                                 \
-    {"gemv_" #T "_L" #L "_t" #NTHR "_u" #U "_v" #VEC, FAMV, 0, 0, 1, L * V, NTHR / L, NTHR / 64, 1, 0,   \
+    {"gemv_" #T "_L" #L "_t" #NTHR "_u" #U "_v" #VEC, FAMV, 0, 0, 1, L * V, NTHR / L, NTHR / 64, 1, 0, 0, \
      (VEC ? 16 : (int)sizeof(T)), L, U, NTHR, lds_gemv(NTHR, L, V), est_regs_gemv(V, U),                \
      (const void *)&gemv_kernel<T, L, NTHR, U, VEC>, &launch_gemv<T, L, NTHR, U, VEC>}
 
@@ -221,6 +207,67 @@ NNJIT_GEMV_LIST(NNJIT_GEMV_INST)
 const Variant kGemvVariants[] = {NNJIT_GEMV_LIST(NNJIT_GEMV_ENTRY)};
 const int kNumGemvVariants = sizeof(kGemvVariants) / sizeof(kGemvVariants[0]);
 #endif
+
+// ------------------------------------------------------------------------
+// Split-K reduction: one thread per 4 consecutive columns of one output row,
+// partials summed in split order 0, 1, ..., S-1 (deterministic).  Partials
+// are loaded 8 at a time (indices clamped to S-1, so the loads are
+// unconditional and all in flight together) and added in order.
+__global__ void __launch_bounds__(256)
+splitk_reduce_kernel(const float *__restrict__ ws, int S, long long slice, int rows, int M, int N, float *C,
+                     long long ldc, long long sC)
+{
+    const int nq = (N + 3) >> 2;
+    const long long total = (long long)rows * nq;
+    const long long stride = (long long)gridDim.x * blockDim.x;
+    for (long long t = (long long)blockIdx.x * blockDim.x + threadIdx.x; t < total; t += stride) {
+        const int r = (int)(t / nq), j = (int)(t - (long long)r * nq) * 4;
+        const int z = r / M, i = r - z * M;
+        const float *src = ws + (long long)r * N + j;
+        float *dst = C + z * sC + (long long)i * ldc + j;
+        if ((N & 3) == 0) {
+            f32x4 v = *(const f32x4 *)src;
+            for (int s0 = 1; s0 < S; s0 += 8) {
+                f32x4 w[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) w[u] = *(const f32x4 *)(src + min(s0 + u, S - 1) * slice);
+#pragma unroll
+                for (int u = 0; u < 8; ++u)
+                    if (s0 + u < S)
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) v[e] += w[u][e];
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) dst[e] = v[e];
+        } else {
+            for (int e = 0; e < 4 && j + e < N; ++e) {
+                float v = src[e];
+                for (int s0 = 1; s0 < S; s0 += 8) {
+                    float w[8];
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) w[u] = src[min(s0 + u, S - 1) * slice + e];
+#pragma unroll
+                    for (int u = 0; u < 8; ++u)
+                        if (s0 + u < S) v += w[u];
+                }
+                dst[e] = v;
+            }
+        }
+    }
+}
+
+hipError_t launch_splitk_reduce(const float *ws, int S, int batch, int M, int N, float *C, long long ldc,
+                                long long sC, hipStream_t stream)
+{
+    const int rows = batch * M;
+    const long long total = (long long)rows * ((N + 3) / 4);
+    if (total <= 0) return hipSuccess;
+    long long blocks = (total + 255) / 256;
+    if (blocks > 8192) blocks = 8192;
+    hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, ws, S,
+                       (long long)rows * N, rows, M, N, C, ldc, sC);
+    return hipGetLastError();
+}
 
 // ------------------------------------------------------------------------
 // Scratch fill for the tuner: a counter-based hash of (seed, index) mapped

@@ -19,11 +19,12 @@ struct GemmParams {
     long long lda, ldb, ldc;
     long long sA, sB, sC;  // batch strides, elements
     int M, N, K;
+    int batch;             // batch slices in this launch (grid.z)
     int S;                 // split-K factor
     int kchunk;            // K range of one split, a multiple of the K-slab
     int tiles_m, tiles_n;
-    float *ws;             // S > 1: partial tiles, [batch][tile][S][Mt*Nt]
-    unsigned *counters;    // S > 1: arrivals per (batch, tile); zero between launches
+    float *ws;             // S > 1: partial products, row-major [S][batch][M][N]
+    const void *zero;      // >= 64 bytes of zeros: the load address of out-of-range elements
 };
 
 // Arguments of the M == 1 kernels: y[N] = x[K] . W[K][N].
@@ -37,7 +38,6 @@ struct GemvParams {
     int kchunk;       // rows of W per split
     int segs;         // column segments
     float *ws;        // S > 1: partial rows, [S][N]
-    unsigned *counters;  // S > 1: arrivals per segment; zero between launches
 };
 
 typedef hipError_t (*LaunchFn)(const void *params, dim3 grid, hipStream_t stream);
@@ -51,6 +51,7 @@ struct Variant {
     int mt, nt, kt;       // macro tile (GEMV: mt = 1, nt = columns per WG, kt = rows per pass)
     int wm, wn;           // wave grid of the workgroup (GEMV: wm = waves, wn = 1)
     int stages;           // LDS buffers for the K loop (1 or 2; GEMV 0)
+    int prefetch;         // K slabs in flight in registers (GEMM; GEMV 0)
     int vec_bytes;        // bytes per global load of one lane (16, or the element size)
     int lanes_seg;        // GEMV: lanes across one row segment
     int unroll;           // GEMV: row loads in flight per lane
@@ -69,7 +70,12 @@ extern const int kNumGemmF16Variants;
 extern const Variant kGemvVariants[];
 extern const int kNumGemvVariants;
 
-// Device helper kernels (scratch fill for the tuner).
+// Device helper kernels: the fixed-order split-K reduction
+//   C[z][i][j] = ws[0][z][i][j] + ws[1][z][i][j] + ... + ws[S-1][z][i][j]
+// (ws row-major [S][batch][M][N], C with leading dim ldc and batch stride sC),
+// and the scratch fill of the tuner.
+hipError_t launch_splitk_reduce(const float *ws, int S, int batch, int M, int N, float *C, long long ldc,
+                                long long sC, hipStream_t stream);
 hipError_t launch_fill_uniform(void *dst, long long n, int dtype, unsigned seed, hipStream_t stream);
 
 }  // namespace nnjit

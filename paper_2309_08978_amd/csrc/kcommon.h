@@ -23,22 +23,4 @@ __device__ __forceinline__ int xcd_remap(int flat, int G) {
     return (xcd < r) ? xcd * (q + 1) + local : r * (q + 1) + (xcd - r) * q + local;
 }
 
-// Split-K arrival: every workgroup of a tile has stored its partial; the
-// last one to arrive (and only it) gets true and must reduce.  All threads of
-// the workgroup call this.  The counter is reset by the reducer.  Nothing
-// waits on another workgroup, so the grid always drains.
-__device__ __forceinline__ bool splitk_arrive_last(unsigned *counter, int S) {
-    __shared__ int s_last;
-    __threadfence();   // release this thread's partial stores (device scope)
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        const unsigned prev = atomicAdd(counter, 1u);
-        s_last = (prev == (unsigned)(S - 1)) ? 1 : 0;
-    }
-    __syncthreads();
-    const bool last = s_last != 0;
-    if (last) __threadfence();  // acquire: see the other workgroups' partials
-    return last;
-}
-
 }  // namespace nnjit

@@ -124,15 +124,13 @@ Geometry geometry_of(const Config &c, int64_t batch, int64_t M, int64_t N, int64
         g.kchunk = (int)(ceil_div(per, v.kt) * v.kt);
         const int64_t tiles = batch * g.tiles_m * (int64_t)g.tiles_n;
         g.wgs = tiles * c.split;
-        g.ws_floats = c.split > 1 ? tiles * c.split * (int64_t)v.mt * v.nt : 0;
-        g.counters = c.split > 1 ? tiles : 0;
+        g.ws_floats = c.split > 1 ? (int64_t)c.split * batch * std::max<int64_t>(M, 1) * std::max<int64_t>(N, 1) : 0;
     } else {
         g.tiles_m = 1;
         g.tiles_n = (int)ceil_div(std::max<int64_t>(N, 1), v.nt);
         g.kchunk = (int)std::max<int64_t>(1, ceil_div(std::max<int64_t>(K, 1), c.split));
         g.wgs = (int64_t)g.tiles_n * c.split;
-        g.ws_floats = c.split > 1 ? (int64_t)c.split * N : 0;
-        g.counters = c.split > 1 ? g.tiles_n : 0;
+        g.ws_floats = c.split > 1 ? (int64_t)c.split * std::max<int64_t>(N, 1) : 0;
     }
     return g;
 }
@@ -164,7 +162,7 @@ LiteResult lite_space(const Shape &s, const nnjit_device_limits &d, const std::v
         out.n_naive = 3 /*L*/ * 5 /*threads*/ * 4 /*U*/ * (int64_t)gemv_splits().size();
     }
 
-    std::vector<Cand> cands;
+    std::vector<Cand> cands, unfit;  // unfit: pass the resource heuristics, fail the shape fit (split 1 only)
     for (const Config &c : configs()) {
         const Variant &v = *c.v;
         if (v.family != fam) continue;
@@ -180,28 +178,6 @@ LiteResult lite_space(const Shape &s, const nnjit_device_limits &d, const std::v
 
         const Geometry g = geometry_of(c, s.batch, s.M, s.N, s.K);
         const int64_t slots = (int64_t)d.num_cus * r.wg_per_cu;
-        if (!gemv) {
-            // shape fit: no macro tile wider than the (power-of-two rounded) matrix
-            if (v.mt > std::max<int64_t>(16, pow2ceil(s.M)) || v.nt > std::max<int64_t>(16, pow2ceil(s.N))) continue;
-            const int64_t tiles = s.batch * g.tiles_m * (int64_t)g.tiles_n;
-            if (c.split > 1) {
-                if (tiles >= slots) continue;               // already fills the chip
-                if (tiles * c.split > 2 * slots) continue;  // over-split
-                if (s.K < 2LL * c.split * v.kt) continue;    // at least two K slabs per split
-            }
-        } else {
-            if (v.nt > std::max<int64_t>(64, pow2ceil(s.N))) continue;
-            const int rows_per_pass = v.kt;
-            if (g.kchunk < rows_per_pass) continue;  // every split gets at least one pass of rows
-            int smax = 1;
-            for (int sp : gemv_splits())
-                if (ceil_div(std::max<int64_t>(s.K, 1), sp) >= rows_per_pass) smax = sp;
-            if (c.split > 1 && g.wgs > 4 * slots) continue;                  // over-split
-            if (g.wgs < d.num_cus / 2 && c.split != smax) continue;          // under-filled
-            // Little's law: bytes in flight per CU must cover HBM latency
-            const int64_t wg_here = std::min<int64_t>(r.wg_per_cu, ceil_div(g.wgs, d.num_cus));
-            if (wg_here * v.threads * (int64_t)v.unroll * 16 < 8192 && c.split != smax) continue;
-        }
         Cand cd;
         cd.id = c.id;
         cd.r = r;
@@ -209,8 +185,42 @@ LiteResult lite_space(const Shape &s, const nnjit_device_limits &d, const std::v
         cd.eff = (double)g.wgs / (double)(waves * slots);
         cd.area = (int64_t)v.mt * v.nt * (gemv ? v.kt : 1);
         cd.split = c.split;
-        cands.push_back(cd);
+        bool fit = true;
+        if (!gemv) {
+            // shape fit: no macro tile wider than the (power-of-two rounded) matrix
+            if (v.mt > std::max<int64_t>(16, pow2ceil(s.M)) || v.nt > std::max<int64_t>(16, pow2ceil(s.N))) fit = false;
+            const int64_t tiles = s.batch * g.tiles_m * (int64_t)g.tiles_n;
+            if (c.split > 1) {
+                // split K only to fill the CUs: keep the smallest power of two
+                // that gives every CU a workgroup, and its two neighbours
+                if (tiles >= d.num_cus) continue;
+                int64_t sfill = 1;
+                while (tiles * sfill < d.num_cus) sfill <<= 1;
+                if (c.split < sfill / 2 || c.split > 2 * sfill) continue;
+                if (tiles * c.split > 2 * slots) continue;  // over-split
+                if (s.K < 2LL * c.split * v.kt) continue;    // at least two K slabs per split
+            }
+        } else {
+            if (v.nt > std::max<int64_t>(64, pow2ceil(s.N))) fit = false;
+            const int rows_per_pass = v.kt;
+            if (c.split > 1) {
+                if (g.kchunk < rows_per_pass) continue;  // every split gets at least one pass of rows
+                int smax = 1;
+                for (int sp : gemv_splits())
+                    if (ceil_div(std::max<int64_t>(s.K, 1), sp) >= rows_per_pass) smax = sp;
+                if (g.wgs > 4 * slots) continue;                                  // over-split
+                if (g.wgs < d.num_cus / 2 && c.split != smax) continue;           // under-filled
+                // Little's law: bytes in flight per CU must cover HBM latency
+                const int64_t wg_here = std::min<int64_t>(r.wg_per_cu, ceil_div(g.wgs, d.num_cus));
+                if (wg_here * v.threads * (int64_t)v.unroll * 16 < 8192 && c.split != smax) continue;
+            }
+        }
+        if (fit) cands.push_back(cd);
+        else if (c.split == 1) unfit.push_back(cd);
     }
+    // the shape fit never empties the space: tiny shapes fall back to the
+    // unsplit configurations that passed the resource heuristics
+    if (cands.empty()) cands = unfit;
 
     // heuristic 7: keep register-bound candidates (Block_core == RegLimit),
     // relaxed when too few survive

@@ -40,7 +40,7 @@ nnjit_device_limits mi355x_limits();
 nnjit_resources resources_of(const Variant &v, const nnjit_device_limits &d, int measured_regs);
 
 constexpr double kRelaxation = 0.9;  // share of the register file the estimate may claim
-constexpr int kMaxTimed = 64;        // candidates timed per shape at most
+constexpr int kMaxTimed = 96;        // candidates timed per shape at most
 constexpr int kMinSurvivors = 8;     // heuristic 7 is relaxed below this many
 
 struct Shape {
@@ -66,8 +66,7 @@ struct Geometry {
     int split = 1;
     int kchunk = 0;
     int64_t wgs = 0;               // workgroups over the whole launch
-    int64_t ws_floats = 0;         // split-K partial storage
-    int64_t counters = 0;          // split-K arrival counters
+    int64_t ws_floats = 0;         // split-K partial storage (S x batch x M x N floats)
 };
 Geometry geometry_of(const Config &c, int64_t batch, int64_t M, int64_t N, int64_t K);
 

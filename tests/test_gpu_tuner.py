@@ -1,0 +1,121 @@
+"""The just-in-time tuner on the GPU (Sec. 3 JIT phase; Sec. 5.2 lite space):
+it returns a configuration of the shape's lite space, measured on the
+device, within the one-second budget; a second call is a cache hit; a
+candidate that fails to launch is skipped; the dispatch then uses the tuned
+configuration; and tuned calls replay correctly from a captured HIP graph."""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import accept
+import paper_2309_08978_amd as nj
+import workloads
+from tests.gpu_util import dev, host, kind_of, dtype_code
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = [("matmul_64x768x768_f32", 0)] + [("bart_base_layer_seq128_f32", i) for i in range(6)] + \
+         [("llama2_7b_decode_f16", i) for i in (0, 5)] + [("llama2_7b_decode_f32", 4)]
+
+
+def _tune(op):
+    dt = dtype_code(op.dtype)
+    if op.batch == 1:
+        return nj.nnjit_tune(op.M, op.N, op.K, dt)
+    return nj.nnjit_tune_batched(op.batch, op.M, op.N, op.K, dt)
+
+
+@pytest.mark.parametrize("name,index", SHAPES)
+def test_tune_returns_measured_lite_config_within_budget(name, index):
+    op = workloads.workload(name)[index]
+    dt = dtype_code(op.dtype)
+    nj.nnjit_cache_clear()
+    cfg = nj.check(_tune(op))
+    st = nj.nnjit_last_tune_stats()
+    lite, n, n_enum, _ = nj.nnjit_lite_space(kind_of(op.batch, op.M), dt, op.batch, op.M, op.N, op.K)
+    print(f"{op.name}: cfg {cfg} {nj.nnjit_config_info(cfg).split()[2]} best {st['best_us']:.2f} us "
+          f"(default {st['default_us']:.2f}), lite {st['n_lite']}/{n_enum}, timed {st['n_timed']}, "
+          f"aborted {st['n_aborted']}, {st['wall_ms']:.1f} ms", flush=True)
+    assert cfg in lite and st["chosen"] == cfg and st["n_lite"] == n
+    assert 1 <= st["n_timed"] and st["n_timed"] + st["n_aborted"] + st["n_failed"] <= n
+    assert 0 < st["best_us"] <= st["default_us"] * 1.0001 + 1e-9 or st["best_us"] <= st["default_us"] * 1.03
+    assert st["wall_ms"] <= 1000.0, st
+    # cache hit
+    assert _tune(op) == cfg
+    st2 = nj.nnjit_last_tune_stats()
+    assert st2["cache_hit"] == 1 and st2["wall_ms"] < 5.0
+    assert nj.nnjit_cached_config(kind_of(op.batch, op.M), dt, op.batch, op.M, op.N, op.K) == cfg
+
+
+def test_measured_resources_are_used():
+    for c in nj.configs()[::11]:
+        r = nj.nnjit_config_resources(c["id"])
+        assert r["regs_measured"] == 1 and 0 < r["regs_per_lane"] <= 512
+        assert r["wg_per_cu"] >= 1 or c["threads"] > 512
+
+
+def test_failing_candidate_is_skipped(monkeypatch):
+    op = workloads.workload("bart_base_layer_seq128_f32")[1]
+    lite, _, _, _ = nj.nnjit_lite_space(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, op.M, op.N, op.K)
+    nj.nnjit_cache_clear()
+    monkeypatch.setenv("NNJIT_FAULT_CONFIG", str(lite[0]))
+    cfg = nj.check(nj.nnjit_tune(op.M, op.N, op.K, nj.NNJIT_F32))
+    st = nj.nnjit_last_tune_stats()
+    assert cfg != lite[0] and cfg in lite and st["n_failed"] >= 1
+    monkeypatch.delenv("NNJIT_FAULT_CONFIG")
+    nj.nnjit_cache_clear()
+
+
+def test_dispatch_uses_tuned_config_and_matches_oracle():
+    name, i = "bart_base_layer_seq128_f32", 3
+    op = workloads.workload(name)[i]
+    A, B = workloads.op_inputs(name, i)
+    nj.nnjit_cache_clear()
+    cfg = nj.check(nj.nnjit_tune(op.M, op.N, op.K, nj.NNJIT_F32))
+    dA, dB = dev(A), dev(B)
+    C_tuned = host(nj.matmul(dA, dB))
+    C_forced = host(nj.matmul(dA, dB, cfg=cfg))
+    assert np.array_equal(C_tuned, C_forced)
+    assert accept.check(C_tuned, oracle.matmul(A, B), A, B, "f32")["ok"]
+
+
+def test_graph_replay_matches_eager():
+    """Tuned calls (split-K included) captured in a graph: every replay,
+    with eager work between replays, equals the eager result."""
+    import torch
+    name = "bart_base_layer_seq128_f32"
+    ops = workloads.workload(name)
+    ins = [workloads.op_inputs(name, i) for i in range(len(ops))]
+    dins = [(dev(A), dev(B)) for A, B in ins]
+    for op in ops:
+        nj.check(_tune(op))
+
+    def run(stream=None):
+        return [nj.matmul(a, b, stream=stream) if a.dim() == 2 else nj.batched_matmul(a, b, stream=stream)
+                for a, b in dins]
+
+    eager = [host(c) for c in run()]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        outs = [torch.empty(c.shape, dtype=torch.float32, device="cuda:0") for c in eager]
+
+        def step():
+            for (a, b), c in zip(dins, outs):
+                (nj.matmul if a.dim() == 2 else nj.batched_matmul)(a, b, c, stream=side)
+        step()  # warm-up on the capture stream (allocates its scratch)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        step()
+    for rep in range(4):
+        for c in outs:
+            c.fill_(float("nan"))
+        run()  # eager work between replays
+        g.replay()
+        torch.cuda.synchronize()
+        for c, e in zip(outs, eager):
+            assert np.array_equal(host(c), e), f"replay {rep}"
