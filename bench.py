@@ -130,6 +130,10 @@ def main(argv=None):
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager", action="store_true", help="time eager ABI calls instead of the graph replay")
+    ap.add_argument("--tuned-cache", default=None,
+                    help="kernel database file: loaded before tuning if it exists, written after")
+    ap.add_argument("--copy-ref-mb", type=int, default=0,
+                    help="first run a plain device copy of this many MiB (reference for HBM counter scaling)")
     args = ap.parse_args(argv)
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -154,6 +158,10 @@ def main(argv=None):
     runs = [OpRun(name, i, copies) for i in range(len(ops))]
     torch.cuda.synchronize()
 
+    if args.tuned_cache and os.path.exists(args.tuned_cache):
+        loaded = nj.check(nj.nnjit_cache_load(args.tuned_cache))
+        log(f"[bench] loaded {loaded} tuned shapes from {args.tuned_cache}")
+
     # just-in-time tuning of every shape
     tunes = []
     for r in runs:
@@ -171,8 +179,16 @@ def main(argv=None):
                       "best_us": round(st["best_us"], 3), "default_us": round(st["default_us"], 3),
                       "config": info.split(" ", 2)[2].split(" threads=")[0]})
         log(f"[bench] tuned {op.name}: {tunes[-1]}")
+    if args.tuned_cache:
+        nj.check(nj.nnjit_cache_save(args.tuned_cache))
 
-    stream = torch.cuda.current_stream()
+    if args.copy_ref_mb > 0:
+        src = torch.ones(args.copy_ref_mb << 18, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     def step(k=0):
         for r in runs:
@@ -251,7 +267,14 @@ def main(argv=None):
                        "bound": rl["bound"], "pct_roofline": round(100 * rl["frac"], 2)})
     dom = max(range(len(runs)), key=lambda i: per_op[i]["us_mean"])
     rl = roofline_of(runs[dom].op, per_op[dom]["us_mean"])
+    cfg_fields = dict(kv.split("=", 1) for kv in nj.nnjit_config_info(tunes[dom]["cfg"]).split() if "=" in kv)
+    dop = runs[dom].op
+    if cfg_fields["family"].startswith("gemm"):
+        wgs = -(-dop.M // int(cfg_fields["Mt"])) * -(-dop.N // int(cfg_fields["Nt"])) * int(cfg_fields["split"])
+    else:
+        wgs = -(-dop.N // int(cfg_fields["cols"])) * int(cfg_fields["split"])
     rl.update({"kernel_op": per_op[dom]["op"], "kernel_config": tunes[dom]["config"],
+               "kernel_grid_wgs": wgs, "kernel_grid_z": dop.batch,
                "per_launch": ("flops" if rl["bound"] == "mfma" else "bytes"),
                "algorithmic": runs[dom].op.flops if rl["bound"] == "mfma" else runs[dom].op.bytes,
                "avg_launch_us": per_op[dom]["us_mean"]})

@@ -91,9 +91,10 @@ int nnjit_batched_matmul(int64_t batch, int64_t M, int64_t N, int64_t K,
  * builds the shape's lite space (enumerate the compiled configurations of
  * the kind and dtype, compute each one's Table 1 resource use on this
  * device, prune by the heuristics, order by workgroups per CU, most first),
- * times every survivor on device scratch of this exact shape (1 warm-up + 3
- * timed launches, median; a candidate whose warm-up is more than 1.5x the
- * best so far is dropped), keeps the fastest in the per-shape cache and
+ * times every survivor on device scratch of this exact shape (1 untimed
+ * warm-up + 3 timed launches, median; a candidate whose first timed launch
+ * is more than 1.5x the best so far is dropped; at most 96 candidates and
+ * about 900 ms of evaluation), keeps the fastest in the per-shape cache and
  * returns its configuration id (>= 0).  Synchronous; uses its own stream and
  * a library-owned scratch buffer.  Re-tuning a cached shape replaces the
  * incumbent only if the new winner is at least 3% faster.  Wall time and
@@ -120,8 +121,8 @@ int nnjit_num_configs(void);
 
 /* Writes a one-line description of configuration `cfg` into buf (at most
  * len bytes including the terminating NUL), e.g.
- * "id=12 family=gemm_f32 mfma=32x32x2 Mt=128 Nt=64 Kt=16 waves=2x2 stages=2
- *  vec=16 split=4 threads=256 lds=...".  Returns the full length of the
+ * "id=12 family=gemm_f32 name=... mfma=32x32x2 Mt=128 Nt=64 Kt=16 waves=2x2
+ *  stages=2 prefetch=2 vec=16 split=4 threads=256 lds=...".  Returns the full length of the
  * description, or NNJIT_EINVAL. */
 int nnjit_config_info(int cfg, char *buf, int64_t len);
 
@@ -197,6 +198,22 @@ int nnjit_cached_config(int kind, int dtype, int64_t batch, int64_t M, int64_t N
 
 /* Forget every tuned shape and release the tuner's scratch.  Returns NNJIT_OK. */
 int nnjit_cache_clear(void);
+
+/* Persistent kernel database (the paper's kernel database keyed by kernel
+ * type, shape and device, Sec. 5.3): write every tuned shape of every
+ * initialised device to a text file at `path` (one line per shape: device
+ * signature = architecture name and CU count, kind, dtype, batch, M, N, K,
+ * configuration name, split, measured time).  Configurations are stored by
+ * name, not id, so a file stays valid across builds that reorder the table.
+ * Returns the number of entries written, or NNJIT_EINVAL / NNJIT_EHIP. */
+int nnjit_cache_save(const char *path);
+
+/* Read such a file into the per-shape cache of the current device: entries
+ * for another device signature, unknown configuration names, configurations
+ * that do not fit the entry's kind and dtype, and malformed lines are skipped.
+ * Loaded entries replace tuned ones.  Returns the number of entries loaded
+ * (>= 0), or NNJIT_EINVAL (unreadable file) / NNJIT_EHIP. */
+int nnjit_cache_load(const char *path);
 
 /* Message for the last error on this thread ("" if none).  The pointer stays
  * valid until the next nnjit_* call on the same thread. */

@@ -29,7 +29,7 @@ ERROR_NAMES = {-1: "NNJIT_EINVAL", -2: "NNJIT_EDTYPE", -3: "NNJIT_ENOCFG", -4: "
 EXPORTED = ["nnjit_matmul", "nnjit_batched_matmul", "nnjit_tune", "nnjit_tune_batched", "nnjit_matmul_config",
             "nnjit_num_configs", "nnjit_config_info", "nnjit_config_resources", "nnjit_lite_space",
             "nnjit_last_tune_stats", "nnjit_last_tune_trace", "nnjit_cached_config", "nnjit_cache_clear",
-            "nnjit_last_error", "nnjit_version"]
+            "nnjit_cache_save", "nnjit_cache_load", "nnjit_last_error", "nnjit_version"]
 
 
 class NnjitError(RuntimeError):
@@ -95,6 +95,8 @@ def load(build_if_missing: bool = False) -> ctypes.CDLL:
                                       ctypes.POINTER(ctypes.c_double), ci],
             "nnjit_cached_config": [ci, ci, i64, i64, i64, i64],
             "nnjit_cache_clear": [],
+            "nnjit_cache_save": [ctypes.c_char_p],
+            "nnjit_cache_load": [ctypes.c_char_p],
             "nnjit_last_error": [],
             "nnjit_version": [],
         }
@@ -200,6 +202,14 @@ def nnjit_cached_config(kind, dtype, batch, M, N, K) -> int:
 
 def nnjit_cache_clear() -> int:
     return load().nnjit_cache_clear()
+
+
+def nnjit_cache_save(path) -> int:
+    return load().nnjit_cache_save(os.fsencode(path))
+
+
+def nnjit_cache_load(path) -> int:
+    return load().nnjit_cache_load(os.fsencode(path))
 
 
 def nnjit_last_error() -> str:

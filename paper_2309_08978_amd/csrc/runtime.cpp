@@ -665,6 +665,68 @@ int nnjit_cache_clear(void) {
     return NNJIT_OK;
 }
 
+int nnjit_cache_save(const char *path) {
+    t_err.clear();
+    if (!path) return fail(NNJIT_EINVAL, "NULL path");
+    std::lock_guard<std::mutex> lk(g_mu);
+    FILE *f = fopen(path, "w");
+    if (!f) return fail(NNJIT_EINVAL, "cannot write %s", path);
+    fprintf(f, "# nnjit kernel database v1: signature kind dtype batch M N K config split us\n");
+    int n = 0;
+    for (const auto &kv : g_tuned) {
+        const int dev = std::get<0>(kv.first);
+        auto di = g_devices.find(dev);
+        if (di == g_devices.end() || !di->second.ready) continue;
+        const Config &c = configs()[kv.second.cfg];
+        fprintf(f, "%s:%d %d %d %lld %lld %lld %lld %s %d %.4f\n", di->second.arch.c_str(), di->second.limits.num_cus,
+                std::get<1>(kv.first), std::get<2>(kv.first), (long long)std::get<3>(kv.first),
+                (long long)std::get<4>(kv.first), (long long)std::get<5>(kv.first), (long long)std::get<6>(kv.first),
+                c.v->name, c.split, kv.second.us);
+        ++n;
+    }
+    fclose(f);
+    return n;
+}
+
+int nnjit_cache_load(const char *path) {
+    t_err.clear();
+    if (!path) return fail(NNJIT_EINVAL, "NULL path");
+    std::lock_guard<std::mutex> lk(g_mu);
+    Device *d = nullptr;
+    int rc = device_ready(&d);
+    if (rc != NNJIT_OK) return rc;
+    FILE *f = fopen(path, "r");
+    if (!f) return fail(NNJIT_EINVAL, "cannot read %s", path);
+    char sig_want[160];
+    snprintf(sig_want, sizeof sig_want, "%s:%d", d->arch.c_str(), d->limits.num_cus);
+    char line[512];
+    int n = 0;
+    while (fgets(line, sizeof line, f)) {
+        if (line[0] == '#') continue;
+        char sig[160], name[160];
+        int kind, dtype, split;
+        long long batch, M, N, K;
+        double us;
+        if (sscanf(line, "%159s %d %d %lld %lld %lld %lld %159s %d %lf", sig, &kind, &dtype, &batch, &M, &N, &K, name,
+                   &split, &us) != 10)
+            continue;
+        if (strcmp(sig, sig_want) != 0) continue;
+        if (kind < NNJIT_KIND_GEMM || kind > NNJIT_KIND_GEMV || (dtype != NNJIT_F32 && dtype != NNJIT_F16)) continue;
+        if (batch < 1 || M < 1 || N < 1 || K < 0) continue;
+        int id = -1;
+        for (const Config &c : configs())
+            if (c.split == split && strcmp(c.v->name, name) == 0) {
+                id = c.id;
+                break;
+            }
+        if (id < 0 || configs()[id].v->family != family_of(kind, dtype)) continue;
+        g_tuned[ShapeKey(d->ordinal, kind, dtype, batch, M, N, K)] = Tuned{id, us};
+        ++n;
+    }
+    fclose(f);
+    return n;
+}
+
 const char *nnjit_last_error(void) { return t_err.c_str(); }
 
 int nnjit_version(void) { return (0 << 16) | 1; }

@@ -119,3 +119,27 @@ def test_graph_replay_matches_eager():
         torch.cuda.synchronize()
         for c, e in zip(outs, eager):
             assert np.array_equal(host(c), e), f"replay {rep}"
+
+
+def test_kernel_database_roundtrip(tmp_path):
+    """Tuned shapes survive a save / clear / load cycle; foreign-device,
+    unknown-configuration and malformed lines are skipped."""
+    op = workloads.workload("bart_base_layer_seq128_f32")[0]
+    nj.nnjit_cache_clear()
+    cfg = nj.check(nj.nnjit_tune(op.M, op.N, op.K, nj.NNJIT_F32))
+    path = tmp_path / "db.txt"
+    assert nj.check(nj.nnjit_cache_save(str(path))) >= 1
+    lines = path.read_text().splitlines()
+    entry = next(l for l in lines if not l.startswith("#"))
+    sig = entry.split()[0]
+    with open(path, "a") as f:
+        f.write("gfx000:1 " + " ".join(entry.split()[1:]) + "\n")          # another device
+        f.write(" ".join([sig] + entry.split()[1:7] + ["no_such_config", "1", "1.0"]) + "\n")
+        f.write("garbage line\n")
+    nj.nnjit_cache_clear()
+    assert nj.nnjit_cached_config(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, op.M, op.N, op.K) == nj.NNJIT_ENOCFG
+    assert nj.check(nj.nnjit_cache_load(str(path))) == len([l for l in lines if not l.startswith("#")])
+    assert nj.nnjit_cached_config(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, op.M, op.N, op.K) == cfg
+    assert nj.check(nj.nnjit_tune(op.M, op.N, op.K, nj.NNJIT_F32)) == cfg
+    assert nj.nnjit_last_tune_stats()["cache_hit"] == 1
+    assert nj.nnjit_cache_load(str(tmp_path / "missing.txt")) == nj.NNJIT_EINVAL
