@@ -10,9 +10,11 @@
 // K x N) is transposed on its way into LDS: each thread loads an 8 x 8 block
 // of B (eight 128-bit rows), transposes it in registers and stores eight
 // 128-bit columns.  Both LDS slabs are [row][8 chunks of 16 bytes] with the
-// chunk index XOR-swizzled by (row & 7), which keeps the 128-bit LDS reads
-// of the fragments and the 128-bit stores of the loaders free of bank
-// conflicts without padding.
+// chunk index XOR-swizzled by (row >> 1) & 7.  Measured on gfx950: a 128-bit
+// LDS read is served 16 lanes (256 bytes) at a time, a 128-bit write 8 lanes
+// (128 bytes) at a time.  16 consecutive rows read at one logical chunk then
+// hit 16 distinct 16-byte bank groups, and the loaders' stores (8 lanes fill
+// the 8 chunks of one row) are conflict-free too, without padding.
 #include "kcommon.h"
 
 namespace nnjit {
@@ -137,7 +139,7 @@ gemm_f16_kernel(GemmParams p)
             const int f = tid + l * NTHR;
             if (A8 % NTHR == 0 || f < A8) {
                 const int row = f >> 3, c = f & 7;
-                As[buf][row * 8 + (c ^ (row & 7))] = ra[set][l];
+                As[buf][row * 8 + (c ^ ((row >> 1) & 7))] = ra[set][l];
             }
         }
 #pragma unroll
@@ -145,7 +147,8 @@ gemm_f16_kernel(GemmParams p)
             const int f = tid + l * NTHR;
             if (BB % NTHR == 0 || f < BB) {
                 const int kb = f & 7, nb = f >> 3;
-                // column c of the 8x8 block: halves k = 0..7 of column n = 8*nb + c
+                // column c of the 8x8 block: halves k = 0..7 of column n = 8*nb + c;
+                // the 8 lanes of one LDS write phase fill the 8 chunks of one row
 #pragma unroll
                 for (int c = 0; c < 8; ++c) {
                     const int d = c >> 1;
@@ -155,7 +158,7 @@ gemm_f16_kernel(GemmParams p)
                         o[w] = (c & 1) ? pack_hi(rb[set][l][2 * w][d], rb[set][l][2 * w + 1][d])
                                        : pack_lo(rb[set][l][2 * w][d], rb[set][l][2 * w + 1][d]);
                     const int n = 8 * nb + c;
-                    Bt[buf][n * 8 + (kb ^ c)] = o;  // (n & 7) == c
+                    Bt[buf][n * 8 + (kb ^ ((n >> 1) & 7))] = o;
                 }
             }
         }
@@ -177,12 +180,12 @@ gemm_f16_kernel(GemmParams p)
 #pragma unroll
             for (int i = 0; i < FM; ++i) {
                 const int row = wm * WTM + i * MF + li;
-                a[i] = __builtin_bit_cast(f16x8, As[buf][row * 8 + (chunk ^ (row & 7))]);
+                a[i] = __builtin_bit_cast(f16x8, As[buf][row * 8 + (chunk ^ ((row >> 1) & 7))]);
             }
 #pragma unroll
             for (int j = 0; j < FN; ++j) {
                 const int col = wn * WTN + j * MF + li;
-                b[j] = __builtin_bit_cast(f16x8, Bt[buf][col * 8 + (chunk ^ (col & 7))]);
+                b[j] = __builtin_bit_cast(f16x8, Bt[buf][col * 8 + (chunk ^ ((col >> 1) & 7))]);
             }
 #pragma unroll
             for (int i = 0; i < FM; ++i)
@@ -274,7 +277,7 @@ constexpr int lds_f16(int mt, int nt, int st) { return st * (mt + nt) * 128; }
 
 #define NNJIT_F16_VARIANT(MT, NT, WM, WN, MF, ST, PF, VEC)                                                  \
     {"gemm_f16_" #MT "x" #NT "x64_w" #WM "x" #WN "_m" #MF "_s" #ST "_p" #PF "_v" #VEC, FAM_GEMM_F16, MF,        \
-     (MF == 32 ? 16 : 32), MT, NT, 64, WM, WN, ST, PF, (VEC ? 16 : 2), 0, 0, WM * WN * 64,                    \
+     (MF == 32 ? 16 : 32), MT, NT, 64, WM, WN, ST, PF, 1, (VEC ? 16 : 2), 0, 0, WM * WN * 64,                 \
      lds_f16(MT, NT, ST), est_regs_f16(MT, NT, WM, WN, MF, PF),                                                \
      (const void *)&gemm_f16_kernel<MT, NT, WM, WN, MF, ST, PF, VEC>, &launch_gemm_f16<MT, NT, WM, WN, MF, ST, PF, VEC>}
 

@@ -39,34 +39,58 @@ template <> struct Mfma32<16> {
     __device__ static __forceinline__ int row_of(int r, int g) { return 4 * g + r; }
 };
 
-template <int MT, int NT, int KT, int WM, int WN, int MF, int ST, int PF, bool VEC>
-__global__ void __launch_bounds__(WM * WN * 64)
+// Sliced K: a workgroup holds KS groups of WM x WN waves.  Group g takes the
+// K slabs g, g + KS, g + 2 KS, ... of the workgroup's K range through its own
+// LDS buffers; at the end the groups' accumulators are added in group order
+// through LDS (deterministic).  KS multiplies the waves and the loads in
+// flight per CU without a second kernel, which is what small-M products
+// (few tiles, long K) need.
+template <int MT, int NT, int KT, int WM, int WN, int MF, int ST, int PF, int KS, bool VEC>
+__global__ void __launch_bounds__(KS * WM * WN * 64)
 gemm_f32_kernel(GemmParams p)
 {
     typedef Mfma32<MF> I;
     typedef typename I::acc_t acc_t;
-    constexpr int NTHR = WM * WN * 64;
+    constexpr int NTG = WM * WN * 64;    // threads of one K group
     constexpr int WTM = MT / WM, WTN = NT / WN;
     constexpr int FM = WTM / MF, FN = WTN / MF;
-    constexpr int SA = KT + 4;           // LDS row stride of the A slab (floats)
-    constexpr int SB = NT + 4;           // LDS row stride of the B slab (floats)
+    // A slab: [Mt][Kt] floats.  Measured on gfx950: a 128-bit LDS read is
+    // served 16 lanes (256 bytes) at a time, a 128-bit write 8 lanes (128
+    // bytes).  Kt = 16 rows (64 bytes) are unpadded with the 16-byte chunk
+    // index XOR-swizzled by (row >> 2) & 3, deeper slabs are padded by 4
+    // floats; both keep the 128-bit stores (8 lanes = 128 contiguous bytes)
+    // and the fragment reads (16 consecutive rows) free of bank conflicts.
+    constexpr bool SWZ = (KT == 16);
+    constexpr int SA = SWZ ? KT : KT + 4;
+    constexpr int SB = NT + 4;           // B slab: [Kt][Nt + 4] floats
     constexpr int A4 = MT * KT / 4;      // 16-byte chunks of one A slab
     constexpr int B4 = KT * NT / 4;
-    constexpr int LA = (A4 + NTHR - 1) / NTHR;
-    constexpr int LB = (B4 + NTHR - 1) / NTHR;
+    constexpr int LA = (A4 + NTG - 1) / NTG;
+    constexpr int LB = (B4 + NTG - 1) / NTG;
     constexpr int KG = 64 / MF;          // lane groups along k
     constexpr int KL = KT / KG;          // k values of one lane group per slab
+    constexpr int SLAB = MT * SA + KT * SB;                       // floats per buffer
+    constexpr int NREG = FM * FN * I::NR;                         // accumulators per lane
+    constexpr int LDS_MAIN = KS * ST * SLAB;
+    constexpr int LDS_RED = (KS - 1) * NREG * NTG;
+    constexpr int LDSF = LDS_MAIN > LDS_RED ? LDS_MAIN : LDS_RED;
     static_assert(FM >= 1 && FN >= 1 && WTM % MF == 0 && WTN % MF == 0, "wave tile");
     static_assert(KL % 4 == 0, "K-slab too small for 128-bit LDS reads");
-    static_assert(MT * NT == NTHR * FM * FN * I::NR, "tile / accumulator count");
+    static_assert(MT * NT == NTG * NREG, "tile / accumulator count");
 
-    __shared__ __attribute__((aligned(16))) float As[ST][MT * SA];
-    __shared__ __attribute__((aligned(16))) float Bs[ST][KT * SB];
+    __shared__ __attribute__((aligned(16))) float lds[LDSF];
 
     const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
+    const int kgp = tid / NTG, tg = tid % NTG;   // K group, thread within the group
+    const int lane = tg & 63, wave = tg >> 6;
     const int wm = wave / WN, wn = wave % WN;
     const int li = lane % MF, lg = lane / MF;
+    float *gl = lds + kgp * ST * SLAB;            // this group's buffers
+    auto As = [&](int buf) { return gl + buf * SLAB; };
+    auto Bs = [&](int buf) { return gl + buf * SLAB + MT * SA; };
+    auto a_off = [](int row, int chunk) {
+        return row * SA + 4 * (SWZ ? (chunk ^ ((row >> 2) & 3)) : chunk);
+    };
 
     // workgroup -> (batch z, split s, tile)
     const int tiles = p.tiles_m * p.tiles_n;
@@ -80,7 +104,8 @@ gemm_f32_kernel(GemmParams p)
     const int m0 = tm * MT, n0 = tn * NT;
     const int kbeg = s * p.kchunk;
     const int kend = min(p.K, kbeg + p.kchunk);
-    const int nk = kend > kbeg ? (kend - kbeg + KT - 1) / KT : 0;
+    const int nk = kend > kbeg ? (kend - kbeg + KT - 1) / KT : 0;   // slabs of the workgroup
+    const int nkg = (nk + KS - 1) / KS;                              // iterations of every group
 
     const float *A = (const float *)p.A + (long long)z * p.sA;
     const float *B = (const float *)p.B + (long long)z * p.sB;
@@ -92,19 +117,20 @@ gemm_f32_kernel(GemmParams p)
     // the loads of slab it+PF are issued while slab it is computed
     f32x4 ra[PF][LA], rb[PF][LB];
 
-    // Loads are branch-free and never followed by value-dependent work:
-    // an out-of-range element is read from a zero-filled buffer instead
-    // (only the address is selected).  A divergent branch around a load, or
-    // a select on its result, would make the compiler wait for every
+    // Loads are branch-free and never followed by value-dependent work: an
+    // out-of-range element is read from a zero-filled buffer instead (only
+    // the address is selected).  A divergent branch around a load, or a
+    // select on its result, would make the compiler wait for every
     // outstanding load before the next slab's loads are issued.
     const float *zero = (const float *)p.zero;
-    auto gload = [&](int set, int k0) {
+    auto gload = [&](int set, int it) {
+        const int k0 = kbeg + (it * KS + kgp) * KT;   // this group's slab of iteration it
 #pragma unroll
         for (int l = 0; l < LA; ++l) {
-            const int f = tid + l * NTHR;
+            const int f = tg + l * NTG;
             const int row = f / (KT / 4), c4 = f % (KT / 4);
             const int gm = m0 + row, gk = k0 + c4 * 4;
-            const bool okr = (A4 % NTHR == 0 || f < A4) && gm < M;
+            const bool okr = (A4 % NTG == 0 || f < A4) && gm < M;
             const float *src = A + (long long)gm * lda + gk;
             f32x4 v;
             if constexpr (VEC) {
@@ -117,10 +143,10 @@ gemm_f32_kernel(GemmParams p)
         }
 #pragma unroll
         for (int l = 0; l < LB; ++l) {
-            const int f = tid + l * NTHR;
+            const int f = tg + l * NTG;
             const int row = f / (NT / 4), c4 = f % (NT / 4);
             const int gk = k0 + row, gn = n0 + c4 * 4;
-            const bool okr = (B4 % NTHR == 0 || f < B4) && gk < kend;
+            const bool okr = (B4 % NTG == 0 || f < B4) && gk < kend;
             const float *src = B + (long long)gk * ldb + gn;
             f32x4 v;
             if constexpr (VEC) {
@@ -134,20 +160,21 @@ gemm_f32_kernel(GemmParams p)
     };
 
     auto sstore = [&](int set, int buf) {
+        float *as = As(buf), *bs = Bs(buf);
 #pragma unroll
         for (int l = 0; l < LA; ++l) {
-            const int f = tid + l * NTHR;
-            if (A4 % NTHR == 0 || f < A4) {
+            const int f = tg + l * NTG;
+            if (A4 % NTG == 0 || f < A4) {
                 const int row = f / (KT / 4), c4 = f % (KT / 4);
-                *(f32x4 *)&As[buf][row * SA + c4 * 4] = ra[set][l];
+                *(f32x4 *)&as[a_off(row, c4)] = ra[set][l];
             }
         }
 #pragma unroll
         for (int l = 0; l < LB; ++l) {
-            const int f = tid + l * NTHR;
-            if (B4 % NTHR == 0 || f < B4) {
+            const int f = tg + l * NTG;
+            if (B4 % NTG == 0 || f < B4) {
                 const int row = f / (NT / 4), c4 = f % (NT / 4);
-                *(f32x4 *)&Bs[buf][row * SB + c4 * 4] = rb[set][l];
+                *(f32x4 *)&bs[row * SB + c4 * 4] = rb[set][l];
             }
         }
     };
@@ -161,13 +188,14 @@ gemm_f32_kernel(GemmParams p)
             for (int r = 0; r < I::NR; ++r) acc[i][j][r] = 0.f;
 
     auto compute = [&](int buf) {
-        const float *as = &As[buf][(wm * WTM + li) * SA + lg * KL];
-        const float *bs = &Bs[buf][(lg * KL) * SB + wn * WTN + li];
+        const float *as = As(buf);
+        const float *bs = Bs(buf) + (lg * KL) * SB + wn * WTN + li;
 #pragma unroll
         for (int q = 0; q < KL / 4; ++q) {
             f32x4 a[FM];
 #pragma unroll
-            for (int i = 0; i < FM; ++i) a[i] = *(const f32x4 *)&as[i * MF * SA + 4 * q];
+            for (int i = 0; i < FM; ++i)
+                a[i] = *(const f32x4 *)&as[a_off(wm * WTM + i * MF + li, lg * (KL / 4) + q)];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 float b[FN];
@@ -181,57 +209,77 @@ gemm_f32_kernel(GemmParams p)
         }
     };
 
-    // Software pipeline.  Slab `it` is loaded into staging set it % PF at
-    // iteration it - PF, stored to LDS buffer it & 1 at iteration it - 1 and
-    // multiplied at iteration it.  The loop is unrolled by PF so every set
-    // index is a compile-time constant, and its loads and LDS stores are
-    // unconditional (slabs past the end read the zero buffer) so the
-    // compiler can keep PF slabs in flight; only the matrix-core work is
-    // skipped past the end.
+    // Software pipeline (per K group).  Iteration it's slab is loaded into
+    // staging set it % PF at iteration it - PF, stored to LDS buffer it & 1 at
+    // iteration it - 1 and multiplied at iteration it.  The loop is unrolled
+    // by PF so every set index is a compile-time constant, and its loads and
+    // LDS stores are unconditional (slabs past the end read the zero buffer)
+    // so the compiler keeps PF slabs in flight; only the matrix-core work is
+    // skipped past the end.  Every group runs the same iterations, so the
+    // workgroup barriers match.
     if (nk > 0) {
 #pragma unroll
-        for (int u = 0; u < PF; ++u) gload(u, kbeg + u * KT);
+        for (int u = 0; u < PF; ++u) gload(u, u);
         if constexpr (ST == 2) {
             sstore(0, 0);
             __syncthreads();
         }
-        for (int it0 = 0; it0 < nk; it0 += PF) {
+        for (int it0 = 0; it0 < nkg; it0 += PF) {
 #pragma unroll
             for (int u = 0; u < PF; ++u) {
                 const int it = it0 + u;
+                const bool live = it * KS + kgp < nk;
                 if constexpr (ST == 2) {
-                    gload(u, kbeg + (it + PF) * KT);
-                    if (it < nk) compute(it & 1);
+                    gload(u, it + PF);
+                    if (live) compute(it & 1);
                     sstore((u + 1) % PF, (it + 1) & 1);
                     __syncthreads();
                 } else {
                     __syncthreads();
                     sstore(u, 0);
                     __syncthreads();
-                    gload(u, kbeg + (it + PF) * KT);
-                    if (it < nk) compute(0);
+                    gload(u, it + PF);
+                    if (live) compute(0);
                 }
             }
         }
     }
 
-    const int rbase = m0 + wm * WTM, cbase = n0 + wn * WTN + li;
-    if (p.S == 1) {
+    if constexpr (KS > 1) {
+        // groups 1 .. KS-1 hand their accumulators to group 0 through LDS
+        __syncthreads();
+        if (kgp > 0) {
+            float *red = lds + (long long)(kgp - 1) * NREG * NTG;
 #pragma unroll
-        for (int i = 0; i < FM; ++i)
+            for (int i = 0; i < FM; ++i)
 #pragma unroll
-            for (int j = 0; j < FN; ++j)
+                for (int j = 0; j < FN; ++j)
 #pragma unroll
-                for (int r = 0; r < I::NR; ++r) {
-                    const int row = rbase + i * MF + I::row_of(r, lg), col = cbase + j * MF;
-                    if (row < M && col < N) C[(long long)row * p.ldc + col] = acc[i][j][r];
-                }
-        return;
+                    for (int r = 0; r < I::NR; ++r) red[((i * FN + j) * I::NR + r) * NTG + tg] = acc[i][j][r];
+        }
+        __syncthreads();
+        if (kgp > 0) return;
+#pragma unroll
+        for (int g = 1; g < KS; ++g) {
+            const float *red = lds + (long long)(g - 1) * NREG * NTG;
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+#pragma unroll
+                    for (int r = 0; r < I::NR; ++r) acc[i][j][r] += red[((i * FN + j) * I::NR + r) * NTG + tg];
+        }
     }
 
-    // split-K: this split's partial tile goes to ws[s][z][row][col]; a
-    // separate kernel sums the S partials in split order
-    float *part = p.ws + ((long long)s * p.batch + z) * (long long)M * N;
+    const int rbase = m0 + wm * WTM, cbase = n0 + wn * WTN + li;
+    // S == 1: C directly; S > 1: this split's partial tile goes to
+    // ws[s][z][row][col] and a separate kernel sums the S partials in order
+    float *out = C;
+    long long ldo = p.ldc;
+    if (p.S > 1) {
+        out = p.ws + ((long long)s * p.batch + z) * (long long)M * N;
+        ldo = N;
+    }
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -239,14 +287,14 @@ gemm_f32_kernel(GemmParams p)
 #pragma unroll
             for (int r = 0; r < I::NR; ++r) {
                 const int row = rbase + i * MF + I::row_of(r, lg), col = cbase + j * MF;
-                if (row < M && col < N) part[(long long)row * N + col] = acc[i][j][r];
+                if (row < M && col < N) out[(long long)row * ldo + col] = acc[i][j][r];
             }
 }
 
-template <int MT, int NT, int KT, int WM, int WN, int MF, int ST, int PF, bool VEC>
+template <int MT, int NT, int KT, int WM, int WN, int MF, int ST, int PF, int KS, bool VEC>
 static hipError_t launch_gemm_f32(const void *params, dim3 grid, hipStream_t stream)
 {
-    hipLaunchKernelGGL((gemm_f32_kernel<MT, NT, KT, WM, WN, MF, ST, PF, VEC>), grid, dim3(WM * WN * 64), 0,
+    hipLaunchKernelGGL((gemm_f32_kernel<MT, NT, KT, WM, WN, MF, ST, PF, KS, VEC>), grid, dim3(KS * WM * WN * 64), 0,
                        stream, *(const GemmParams *)params);
     return hipGetLastError();
 }
@@ -259,75 +307,94 @@ constexpr int est_regs_f32(int mt, int nt, int kt, int wm, int wn, int mf, int p
     return (mt / wm) * (nt / wn) / 64 + 4 * ((mt / wm) / mf) + ((nt / wn) / mf) +
            pf * ((mt * kt + kt * nt) / (wm * wn * 64)) + 28;
 }
-constexpr int lds_f32(int mt, int nt, int kt, int st) { return st * (mt * (kt + 4) + kt * (nt + 4)) * 4; }
+constexpr int lds_f32(int mt, int nt, int kt, int st, int ks) {
+    return (ks * st * (mt * (kt == 16 ? kt : kt + 4) + kt * (nt + 4)) > (ks - 1) * mt * nt
+                ? ks * st * (mt * (kt == 16 ? kt : kt + 4) + kt * (nt + 4))
+                : (ks - 1) * mt * nt) * 4;
+}
 
-#define NNJIT_F32_VARIANT(MT, NT, KT, WM, WN, MF, ST, PF, VEC)                                          \
-    {"gemm_f32_" #MT "x" #NT "x" #KT "_w" #WM "x" #WN "_m" #MF "_s" #ST "_p" #PF "_v" #VEC, FAM_GEMM_F32, MF, \
-     (MF == 32 ? 2 : 4), MT, NT, KT, WM, WN, ST, PF, (VEC ? 16 : 4), 0, 0, WM * WN * 64,                   \
-     lds_f32(MT, NT, KT, ST), est_regs_f32(MT, NT, KT, WM, WN, MF, PF),                                     \
-     (const void *)&gemm_f32_kernel<MT, NT, KT, WM, WN, MF, ST, PF, VEC>,                                   \
-     &launch_gemm_f32<MT, NT, KT, WM, WN, MF, ST, PF, VEC>}
+#define NNJIT_F32_VARIANT(MT, NT, KT, WM, WN, MF, ST, PF, KS, VEC)                                        \
+    {"gemm_f32_" #MT "x" #NT "x" #KT "_w" #WM "x" #WN "_m" #MF "_s" #ST "_p" #PF "_k" #KS "_v" #VEC,             \
+     FAM_GEMM_F32, MF, (MF == 32 ? 2 : 4), MT, NT, KT, WM, WN, ST, PF, KS, (VEC ? 16 : 4), 0, 0,               \
+     KS * WM * WN * 64, lds_f32(MT, NT, KT, ST, KS), est_regs_f32(MT, NT, KT, WM, WN, MF, PF),                 \
+     (const void *)&gemm_f32_kernel<MT, NT, KT, WM, WN, MF, ST, PF, KS, VEC>,                                 \
+     &launch_gemm_f32<MT, NT, KT, WM, WN, MF, ST, PF, KS, VEC>}
 
 // The compiled fp32 configurations (the family's full set; the lite space of
 // a shape is a pruned, ordered subset).  Tile edges are powers of two
 // (heuristic 2).  The last entries load element by element, for operands
 // that are not 16-byte aligned.
 #define NNJIT_F32_LIST(X) \
-    X(256, 128, 16, 2, 2, 32, 2, 1, true) \
-    X(128, 256, 16, 2, 2, 32, 2, 1, true) \
-    X(256, 256, 16, 2, 2, 32, 2, 1, true) \
-    X(256, 128, 16, 4, 2, 32, 2, 1, true) \
-    X(256, 128, 16, 4, 2, 32, 2, 2, true) \
-    X(128, 128, 16, 2, 2, 32, 2, 1, true) \
-    X(128, 128, 16, 2, 2, 32, 2, 2, true) \
-    X(128, 128, 32, 2, 2, 32, 2, 1, true) \
-    X(128, 128, 16, 2, 2, 32, 1, 1, true) \
-    X(128, 128, 16, 1, 2, 32, 2, 1, true) \
-    X(128, 64, 16, 2, 2, 32, 2, 1, true) \
-    X(128, 64, 16, 2, 2, 32, 2, 2, true) \
-    X(128, 64, 32, 2, 2, 32, 2, 2, true) \
-    X(64, 128, 16, 2, 2, 32, 2, 1, true) \
-    X(64, 128, 16, 2, 2, 32, 2, 2, true) \
-    X(64, 128, 32, 2, 2, 32, 2, 2, true) \
-    X(64, 64, 16, 2, 2, 32, 2, 1, true) \
-    X(64, 64, 16, 2, 2, 32, 2, 2, true) \
-    X(64, 64, 16, 2, 2, 32, 2, 4, true) \
-    X(64, 64, 32, 2, 2, 32, 2, 2, true) \
-    X(64, 64, 64, 2, 2, 32, 2, 1, true) \
-    X(64, 64, 64, 2, 2, 32, 2, 2, true) \
-    X(64, 64, 64, 2, 2, 16, 2, 2, true) \
-    X(128, 64, 64, 2, 2, 32, 2, 2, true) \
-    X(64, 128, 64, 2, 2, 32, 2, 2, true) \
-    X(32, 64, 64, 1, 2, 32, 2, 2, true) \
-    X(64, 32, 64, 2, 1, 32, 2, 2, true) \
-    X(32, 64, 64, 2, 2, 16, 2, 2, true) \
-    X(64, 32, 64, 2, 2, 16, 2, 2, true) \
-    X(32, 32, 64, 2, 2, 16, 2, 2, true) \
-    X(32, 32, 64, 1, 1, 32, 2, 2, true) \
-    X(64, 64, 16, 2, 2, 16, 2, 2, true) \
-    X(64, 64, 16, 2, 2, 32, 1, 1, true) \
-    X(64, 64, 16, 2, 2, 32, 1, 2, true) \
-    X(64, 64, 16, 1, 1, 32, 2, 2, true) \
-    X(32, 64, 16, 1, 2, 32, 2, 2, true) \
-    X(32, 64, 32, 1, 2, 32, 2, 2, true) \
-    X(64, 32, 16, 2, 1, 32, 2, 2, true) \
-    X(64, 32, 32, 2, 1, 32, 2, 2, true) \
-    X(32, 32, 16, 1, 1, 32, 2, 2, true) \
-    X(32, 32, 32, 1, 1, 32, 2, 2, true) \
-    X(32, 32, 16, 2, 2, 16, 2, 1, true) \
-    X(32, 32, 16, 2, 2, 16, 2, 2, true) \
-    X(32, 32, 16, 2, 2, 16, 2, 4, true) \
-    X(32, 64, 16, 2, 2, 16, 2, 2, true) \
-    X(32, 64, 16, 2, 2, 16, 2, 4, true) \
-    X(64, 32, 16, 2, 2, 16, 2, 2, true) \
-    X(64, 32, 16, 2, 2, 16, 2, 4, true) \
-    X(16, 64, 16, 1, 2, 16, 2, 2, true) \
-    X(16, 64, 32, 1, 4, 16, 2, 2, true) \
-    X(64, 64, 16, 2, 2, 32, 2, 1, false) \
-    X(32, 32, 16, 1, 1, 32, 2, 1, false)
+    X(64, 64, 16, 2, 2, 32, 2, 2, 2, true) \
+    X(64, 64, 16, 2, 2, 32, 2, 2, 4, true) \
+    X(64, 64, 32, 2, 2, 32, 2, 2, 2, true) \
+    X(64, 64, 16, 2, 2, 16, 2, 2, 2, true) \
+    X(64, 64, 16, 2, 2, 16, 2, 2, 4, true) \
+    X(64, 32, 16, 2, 2, 16, 2, 2, 2, true) \
+    X(64, 32, 16, 2, 2, 16, 2, 2, 4, true) \
+    X(32, 64, 16, 2, 2, 16, 2, 2, 2, true) \
+    X(32, 64, 16, 2, 2, 16, 2, 2, 4, true) \
+    X(32, 32, 16, 2, 2, 16, 2, 2, 4, true) \
+    X(64, 32, 32, 2, 1, 32, 2, 2, 4, true) \
+    X(32, 64, 32, 1, 2, 32, 2, 2, 4, true) \
+    X(128, 64, 16, 2, 2, 32, 2, 2, 2, true) \
+    X(64, 128, 16, 2, 2, 32, 2, 2, 2, true) \
+    X(128, 128, 16, 2, 2, 32, 2, 1, 2, true) \
+    X(256, 128, 16, 2, 2, 32, 2, 1, 1, true) \
+    X(128, 256, 16, 2, 2, 32, 2, 1, 1, true) \
+    X(256, 256, 16, 2, 2, 32, 2, 1, 1, true) \
+    X(256, 128, 16, 4, 2, 32, 2, 1, 1, true) \
+    X(256, 128, 16, 4, 2, 32, 2, 2, 1, true) \
+    X(128, 128, 16, 2, 2, 32, 2, 1, 1, true) \
+    X(128, 128, 16, 2, 2, 32, 2, 2, 1, true) \
+    X(128, 128, 32, 2, 2, 32, 2, 1, 1, true) \
+    X(128, 128, 16, 2, 2, 32, 1, 1, 1, true) \
+    X(128, 128, 16, 1, 2, 32, 2, 1, 1, true) \
+    X(128, 64, 16, 2, 2, 32, 2, 1, 1, true) \
+    X(128, 64, 16, 2, 2, 32, 2, 2, 1, true) \
+    X(128, 64, 32, 2, 2, 32, 2, 2, 1, true) \
+    X(64, 128, 16, 2, 2, 32, 2, 1, 1, true) \
+    X(64, 128, 16, 2, 2, 32, 2, 2, 1, true) \
+    X(64, 128, 32, 2, 2, 32, 2, 2, 1, true) \
+    X(64, 64, 16, 2, 2, 32, 2, 1, 1, true) \
+    X(64, 64, 16, 2, 2, 32, 2, 2, 1, true) \
+    X(64, 64, 16, 2, 2, 32, 2, 4, 1, true) \
+    X(64, 64, 32, 2, 2, 32, 2, 2, 1, true) \
+    X(64, 64, 64, 2, 2, 32, 2, 1, 1, true) \
+    X(64, 64, 64, 2, 2, 32, 2, 2, 1, true) \
+    X(64, 64, 64, 2, 2, 16, 2, 2, 1, true) \
+    X(128, 64, 64, 2, 2, 32, 2, 2, 1, true) \
+    X(64, 128, 64, 2, 2, 32, 2, 2, 1, true) \
+    X(32, 64, 64, 1, 2, 32, 2, 2, 1, true) \
+    X(64, 32, 64, 2, 1, 32, 2, 2, 1, true) \
+    X(32, 64, 64, 2, 2, 16, 2, 2, 1, true) \
+    X(64, 32, 64, 2, 2, 16, 2, 2, 1, true) \
+    X(32, 32, 64, 2, 2, 16, 2, 2, 1, true) \
+    X(32, 32, 64, 1, 1, 32, 2, 2, 1, true) \
+    X(64, 64, 16, 2, 2, 16, 2, 2, 1, true) \
+    X(64, 64, 16, 2, 2, 32, 1, 1, 1, true) \
+    X(64, 64, 16, 2, 2, 32, 1, 2, 1, true) \
+    X(64, 64, 16, 1, 1, 32, 2, 2, 1, true) \
+    X(32, 64, 16, 1, 2, 32, 2, 2, 1, true) \
+    X(32, 64, 32, 1, 2, 32, 2, 2, 1, true) \
+    X(64, 32, 16, 2, 1, 32, 2, 2, 1, true) \
+    X(64, 32, 32, 2, 1, 32, 2, 2, 1, true) \
+    X(32, 32, 16, 1, 1, 32, 2, 2, 1, true) \
+    X(32, 32, 32, 1, 1, 32, 2, 2, 1, true) \
+    X(32, 32, 16, 2, 2, 16, 2, 1, 1, true) \
+    X(32, 32, 16, 2, 2, 16, 2, 2, 1, true) \
+    X(32, 32, 16, 2, 2, 16, 2, 4, 1, true) \
+    X(32, 64, 16, 2, 2, 16, 2, 2, 1, true) \
+    X(32, 64, 16, 2, 2, 16, 2, 4, 1, true) \
+    X(64, 32, 16, 2, 2, 16, 2, 2, 1, true) \
+    X(64, 32, 16, 2, 2, 16, 2, 4, 1, true) \
+    X(16, 64, 16, 1, 2, 16, 2, 2, 1, true) \
+    X(16, 64, 32, 1, 4, 16, 2, 2, 1, true) \
+    X(64, 64, 16, 2, 2, 32, 2, 1, 1, false) \
+    X(32, 32, 16, 1, 1, 32, 2, 1, 1, false)
 
-#define NNJIT_F32_INST(MT, NT, KT, WM, WN, MF, ST, PF, VEC) \
-    template __global__ void gemm_f32_kernel<MT, NT, KT, WM, WN, MF, ST, PF, VEC>(GemmParams);
+#define NNJIT_F32_INST(MT, NT, KT, WM, WN, MF, ST, PF, KS, VEC) \
+    template __global__ void gemm_f32_kernel<MT, NT, KT, WM, WN, MF, ST, PF, KS, VEC>(GemmParams);
 NNJIT_F32_LIST(NNJIT_F32_INST)
 
 #if !defined(__HIP_DEVICE_COMPILE__)

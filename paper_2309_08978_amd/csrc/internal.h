@@ -52,6 +52,7 @@ struct Variant {
     int wm, wn;           // wave grid of the workgroup (GEMV: wm = waves, wn = 1)
     int stages;           // LDS buffers for the K loop (1 or 2; GEMV 0)
     int prefetch;         // K slabs in flight in registers (GEMM; GEMV 0)
+    int kslices;          // K groups of waves inside a workgroup (GEMM; GEMV 1)
     int vec_bytes;        // bytes per global load of one lane (16, or the element size)
     int lanes_seg;        // GEMV: lanes across one row segment
     int unroll;           // GEMV: row loads in flight per lane

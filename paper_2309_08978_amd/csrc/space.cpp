@@ -172,7 +172,7 @@ LiteResult lite_space(const Shape &s, const nnjit_device_limits &d, const std::v
         if (spills && gi < (int)spills->size() && (*spills)[gi]) continue;
         const int mregs = (measured_regs && gi < (int)measured_regs->size()) ? (*measured_regs)[gi] : -1;
         const nnjit_resources r = resources_of(v, d, mregs);
-        if (r.threads_per_wg > std::min(512, d.max_threads_per_wg)) continue;  // heuristic 5
+        if (r.threads_per_wg > d.max_threads_per_wg) continue;                // heuristic 5
         if (r.lds_per_wg > d.lds_per_wg) continue;                            // heuristic 6
         if (r.wg_per_cu < 1) continue;
 
@@ -190,13 +190,16 @@ LiteResult lite_space(const Shape &s, const nnjit_device_limits &d, const std::v
             // shape fit: no macro tile wider than the (power-of-two rounded) matrix
             if (v.mt > std::max<int64_t>(16, pow2ceil(s.M)) || v.nt > std::max<int64_t>(16, pow2ceil(s.N))) fit = false;
             const int64_t tiles = s.batch * g.tiles_m * (int64_t)g.tiles_n;
+            // K groups inside a workgroup pay off only while the chip has
+            // fewer workgroups than CUs
+            if (v.kslices > 1 && tiles * c.split >= d.num_cus) continue;
             if (c.split > 1) {
                 // split K only to fill the CUs: keep the smallest power of two
-                // that gives every CU a workgroup, and its two neighbours
+                // that gives every CU a workgroup, and twice that
                 if (tiles >= d.num_cus) continue;
                 int64_t sfill = 1;
                 while (tiles * sfill < d.num_cus) sfill <<= 1;
-                if (c.split < sfill / 2 || c.split > 2 * sfill) continue;
+                if (c.split < sfill || c.split > 2 * sfill) continue;
                 if (tiles * c.split > 2 * slots) continue;  // over-split
                 if (s.K < 2LL * c.split * v.kt) continue;    // at least two K slabs per split
             }

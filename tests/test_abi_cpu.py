@@ -79,7 +79,7 @@ def test_config_table(lib):
                 assert p2(c[k]), (c, k)           # heuristic 2: power-of-two tiles
             wm, wn = map(int, c["waves"].split("x"))
             assert c["Mt"] % wm == 0 and c["Nt"] % wn == 0
-            assert c["threads"] == 64 * wm * wn
+            assert c["threads"] == 64 * wm * wn * c["kslices"]
         else:
             assert p2(c["cols"]) and p2(c["lanes_per_seg"]) and p2(c["threads"])
 
@@ -126,7 +126,7 @@ def test_lite_space_is_dozens_and_ordered(lib, name, index):
         c = cfgs[i]
         assert c["family"] == fam
         r = nj.nnjit_config_resources(i, d)
-        assert c["threads"] <= 512                       # heuristic 5
+        assert c["threads"] <= d.max_threads_per_wg       # heuristic 5
         assert r["lds_per_wg"] <= d.lds_per_wg           # heuristic 6
         if prev is not None:
             assert r["wg_per_cu"] <= prev                # evaluated from max to min Block_core
