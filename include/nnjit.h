@@ -159,8 +159,9 @@ typedef struct nnjit_resources {
 int nnjit_config_resources(int cfg, const nnjit_device_limits *dev, nnjit_resources *out);
 
 /* The lite space of a shape: writes up to `cap` configuration ids, in
- * evaluation order, into `ids` and returns how many survive pruning (which
- * may exceed cap).  *n_enumerated (if not NULL) receives the number of
+ * evaluation order, into `ids` and returns the size of the lite space (the
+ * survivors of pruning, at most the first 96 in evaluation order; may exceed
+ * cap).  *n_enumerated (if not NULL) receives the number of
  * compiled configurations of the kind and dtype that were considered, and
  * *n_naive the size of the unpruned space over the same parameter axes.
  * With dev != NULL this is pure host code (no GPU needed) and uses estimated

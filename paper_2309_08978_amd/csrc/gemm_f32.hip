@@ -299,6 +299,168 @@ static hipError_t launch_gemm_f32(const void *params, dim3 grid, hipStream_t str
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// LDS-free ("direct") variant for small M.  Every wave owns a WTM x WTN block
+// of C and one K slice; it loads its matrix-core fragments straight from
+// global memory (L2-resident operands at these sizes) into a ring of PF
+// register sets and never waits at a barrier inside the K loop.  A
+// workgroup holds CB column blocks x KS K slices of waves: the CB waves of a
+// slice share A rows in L1, and at the end the KS slices of a block are
+// added through LDS in slice order (deterministic).  Fragment lane layout as
+// above: lane group g takes k in [g*KL, (g+1)*KL) of each K slab, so its A
+// values are 16-byte contiguous and its B values are one 4-byte word per k
+// (consecutive lanes read consecutive columns, coalesced).
+template <int WTM, int WTN, int KT, int CB, int MF, int PF, int KS, bool VEC>
+__global__ void __launch_bounds__(CB * KS * 64)
+gemm_f32_direct_kernel(GemmParams p)
+{
+    typedef Mfma32<MF> I;
+    typedef typename I::acc_t acc_t;
+    constexpr int FM = WTM / MF, FN = WTN / MF;
+    constexpr int KG = 64 / MF;          // lane groups along k
+    constexpr int KL = KT / KG;          // k values of one lane group per slab
+    constexpr int NREG = FM * FN * I::NR;
+    static_assert(FM >= 1 && FN >= 1 && KL % 4 == 0, "direct tile");
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int cb = wave % CB, ks = wave / CB;       // column block, K slice
+    const int li = lane % MF, lg = lane / MF;
+
+    const int tiles = p.tiles_m * p.tiles_n;
+    const int gx = gridDim.x;
+    const int logical = xcd_remap(blockIdx.x + gx * blockIdx.z, gx * gridDim.z);
+    const int z = logical / gx;
+    const int rest = logical - z * gx;
+    const int s = rest / tiles;
+    const int tile = rest - s * tiles;
+    const int tm = tile % p.tiles_m, tn = tile / p.tiles_m;
+    const int m0 = tm * WTM, n0 = tn * (CB * WTN) + cb * WTN;
+    const int kbeg = s * p.kchunk;
+    const int kend = min(p.K, kbeg + p.kchunk);
+    const int nk = kend > kbeg ? (kend - kbeg + KT - 1) / KT : 0;
+    const int nps = (nk + KS - 1) / KS;              // slabs of one K slice
+    const int sl0 = ks * nps;                        // this slice's first slab
+    const int nmine = max(0, min(nk - sl0, nps));
+
+    const float *A = (const float *)p.A + (long long)z * p.sA;
+    const float *B = (const float *)p.B + (long long)z * p.sB;
+    float *C = p.C + (long long)z * p.sC;
+    const int M = p.M, N = p.N;
+    const long long lda = p.lda, ldb = p.ldb;
+    const float *zero = (const float *)p.zero;
+
+    f32x4 ra[PF][FM][KL / 4];
+    float rb[PF][FN][KL];
+    auto gload = [&](int set, int it) {
+        const int k0 = kbeg + (sl0 + it) * KT + lg * KL;
+        const bool okk = it < nmine;
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+            const int gm = m0 + i * MF + li;
+            const float *src = A + (long long)gm * lda + k0;
+#pragma unroll
+            for (int q = 0; q < KL / 4; ++q) {
+                if constexpr (VEC) {
+                    ra[set][i][q] = *(const f32x4 *)((okk && gm < M && k0 + 4 * q < kend) ? src + 4 * q : zero);
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        ra[set][i][q][e] = *((okk && gm < M && k0 + 4 * q + e < kend) ? src + 4 * q + e : zero);
+                }
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+            const int gn = n0 + j * MF + li;
+            const float *src = B + (long long)k0 * ldb + gn;
+#pragma unroll
+            for (int e = 0; e < KL; ++e)
+                rb[set][j][e] = *((okk && gn < N && k0 + e < kend) ? src + (long long)e * ldb : zero);
+        }
+    };
+
+    acc_t acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int r = 0; r < I::NR; ++r) acc[i][j][r] = 0.f;
+
+    auto compute = [&](int set) {
+#pragma unroll
+        for (int e = 0; e < KL; ++e)
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j) acc[i][j] = I::mma(ra[set][i][e >> 2][e & 3], rb[set][j][e], acc[i][j]);
+    };
+
+    // register ring: slab it is loaded PF iterations ahead; loads are
+    // unconditional (past the end they read the zero buffer)
+#pragma unroll
+    for (int u = 0; u < PF; ++u) gload(u, u);
+    for (int it0 = 0; it0 < nmine; it0 += PF) {
+#pragma unroll
+        for (int u = 0; u < PF; ++u) {
+            const int it = it0 + u;
+            if (it < nmine) compute(u);
+            gload(u, it + PF);
+        }
+    }
+
+    if constexpr (KS > 1) {
+        // slices 1 .. KS-1 hand their accumulators to slice 0 through LDS
+        __shared__ float red[(KS > 1 ? KS - 1 : 1) * CB * NREG * 64];
+        if (ks > 0) {
+            float *r = red + ((ks - 1) * CB + cb) * NREG * 64;
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+#pragma unroll
+                    for (int q = 0; q < I::NR; ++q) r[((i * FN + j) * I::NR + q) * 64 + lane] = acc[i][j][q];
+        }
+        __syncthreads();
+        if (ks > 0) return;
+#pragma unroll
+        for (int g = 1; g < KS; ++g) {
+            const float *r = red + ((g - 1) * CB + cb) * NREG * 64;
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+#pragma unroll
+                    for (int q = 0; q < I::NR; ++q) acc[i][j][q] += r[((i * FN + j) * I::NR + q) * 64 + lane];
+        }
+    }
+
+    float *out = C;
+    long long ldo = p.ldc;
+    if (p.S > 1) {
+        out = p.ws + ((long long)s * p.batch + z) * (long long)M * N;
+        ldo = N;
+    }
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int r = 0; r < I::NR; ++r) {
+                const int row = m0 + i * MF + I::row_of(r, lg), col = n0 + j * MF + li;
+                if (row < M && col < N) out[(long long)row * ldo + col] = acc[i][j][r];
+            }
+}
+
+template <int WTM, int WTN, int KT, int CB, int MF, int PF, int KS, bool VEC>
+static hipError_t launch_gemm_f32_direct(const void *params, dim3 grid, hipStream_t stream)
+{
+    hipLaunchKernelGGL((gemm_f32_direct_kernel<WTM, WTN, KT, CB, MF, PF, KS, VEC>), grid, dim3(CB * KS * 64), 0, stream,
+                       *(const GemmParams *)params);
+    return hipGetLastError();
+}
+
 // Register estimate of the Table 1 formula Reg_thread = x0*r0 + r0*y0 + x0*y0
 // for one lane: the accumulator tile (x0*y0 over 64 lanes), the A and B
 // fragments of one K step (r0*y0, r0*x0), the global->LDS staging registers,
@@ -320,6 +482,38 @@ constexpr int lds_f32(int mt, int nt, int kt, int st, int ks) {
      (const void *)&gemm_f32_kernel<MT, NT, KT, WM, WN, MF, ST, PF, KS, VEC>,                                 \
      &launch_gemm_f32<MT, NT, KT, WM, WN, MF, ST, PF, KS, VEC>}
 
+// Direct variants: macro tile = WTM x (CB * WTN); waves = CB x KS; no LDS
+// staging (only the final K-slice reduction); registers = accumulators +
+// PF x (A + B fragments of one slab) + overhead.
+constexpr int est_regs_f32d(int wtm, int wtn, int kt, int mf, int pf) {
+    return wtm * wtn / 64 + pf * ((wtm / mf) * (kt / (64 / mf)) + (wtn / mf) * (kt / (64 / mf))) + 24;
+}
+#define NNJIT_F32D_VARIANT(WTM, WTN, KT, CB, MF, PF, KS, VEC)                                                  \
+    {"gemm_f32d_" #WTM "x" #WTN "x" #KT "_c" #CB "_m" #MF "_p" #PF "_k" #KS "_v" #VEC, FAM_GEMM_F32, MF,          \
+     (MF == 32 ? 2 : 4), WTM, CB * WTN, KT, 1, CB, 0, PF, KS, (VEC ? 16 : 4), 0, 0, CB * KS * 64,                \
+     (KS > 1 ? (KS - 1) * CB * WTM * WTN * 4 : 4), est_regs_f32d(WTM, WTN, KT, MF, PF),                         \
+     (const void *)&gemm_f32_direct_kernel<WTM, WTN, KT, CB, MF, PF, KS, VEC>,                                   \
+     &launch_gemm_f32_direct<WTM, WTN, KT, CB, MF, PF, KS, VEC>}
+
+#define NNJIT_F32D_LIST(X) \
+    X(32, 32, 16, 4, 16, 4, 4, true) \
+    X(32, 32, 16, 4, 16, 2, 4, true) \
+    X(32, 32, 16, 2, 16, 4, 4, true) \
+    X(32, 32, 16, 2, 32, 4, 4, true) \
+    X(32, 32, 16, 4, 32, 4, 4, true) \
+    X(16, 16, 16, 4, 16, 4, 4, true) \
+    X(16, 16, 16, 4, 16, 8, 4, true) \
+    X(32, 16, 16, 4, 16, 4, 4, true) \
+    X(16, 32, 16, 4, 16, 4, 4, true) \
+    X(32, 64, 16, 2, 32, 4, 4, true) \
+    X(64, 32, 16, 2, 32, 4, 4, true) \
+    X(32, 32, 32, 4, 16, 2, 4, true) \
+    X(32, 32, 32, 2, 32, 2, 4, true)
+
+#define NNJIT_F32D_INST(WTM, WTN, KT, CB, MF, PF, KS, VEC) \
+    template __global__ void gemm_f32_direct_kernel<WTM, WTN, KT, CB, MF, PF, KS, VEC>(GemmParams);
+NNJIT_F32D_LIST(NNJIT_F32D_INST)
+
 // The compiled fp32 configurations (the family's full set; the lite space of
 // a shape is a pruned, ordered subset).  Tile edges are powers of two
 // (heuristic 2).  The last entries load element by element, for operands
@@ -327,6 +521,15 @@ constexpr int lds_f32(int mt, int nt, int kt, int st, int ks) {
 #define NNJIT_F32_LIST(X) \
     X(64, 64, 16, 2, 2, 32, 2, 2, 2, true) \
     X(64, 64, 16, 2, 2, 32, 2, 2, 4, true) \
+    X(64, 32, 16, 2, 2, 16, 2, 4, 4, true) \
+    X(32, 64, 16, 2, 2, 16, 2, 4, 4, true) \
+    X(64, 64, 16, 2, 2, 16, 2, 4, 4, true) \
+    X(32, 32, 16, 2, 2, 16, 2, 4, 4, true) \
+    X(64, 32, 32, 2, 2, 16, 2, 2, 4, true) \
+    X(32, 64, 32, 2, 2, 16, 2, 2, 4, true) \
+    X(64, 64, 32, 2, 2, 16, 2, 2, 4, true) \
+    X(64, 32, 16, 2, 1, 32, 2, 4, 4, true) \
+    X(32, 64, 16, 1, 2, 32, 2, 4, 4, true) \
     X(64, 64, 32, 2, 2, 32, 2, 2, 2, true) \
     X(64, 64, 16, 2, 2, 16, 2, 2, 2, true) \
     X(64, 64, 16, 2, 2, 16, 2, 2, 4, true) \
@@ -399,7 +602,8 @@ NNJIT_F32_LIST(NNJIT_F32_INST)
 
 #if !defined(__HIP_DEVICE_COMPILE__)
 #define NNJIT_F32_ENTRY(...) NNJIT_F32_VARIANT(__VA_ARGS__),
-const Variant kGemmF32Variants[] = {NNJIT_F32_LIST(NNJIT_F32_ENTRY)};
+#define NNJIT_F32D_ENTRY(...) NNJIT_F32D_VARIANT(__VA_ARGS__),
+const Variant kGemmF32Variants[] = {NNJIT_F32_LIST(NNJIT_F32_ENTRY) NNJIT_F32D_LIST(NNJIT_F32D_ENTRY)};
 const int kNumGemmF32Variants = sizeof(kGemmF32Variants) / sizeof(kGemmF32Variants[0]);
 #endif
 

@@ -167,6 +167,14 @@ constexpr int lds_gemv(int nthr, int l, int v) { return nthr > 64 ? (nthr / 64) 
 
 // The compiled GEMV configurations of both dtypes.
 #define NNJIT_GEMV_LIST(X) \
+    X(float, 16, 256, 16, true) \
+    X(float, 64, 256, 16, true) \
+    X(float, 16, 512, 8, true) \
+    X(_Float16, 16, 256, 16, true) \
+    X(_Float16, 32, 256, 16, true) \
+    X(_Float16, 64, 256, 16, true) \
+    X(_Float16, 16, 512, 8, true) \
+    X(_Float16, 32, 512, 8, true) \
     X(float, 64, 256, 4, true) \
     X(float, 64, 256, 8, true) \
     X(float, 64, 512, 4, true) \

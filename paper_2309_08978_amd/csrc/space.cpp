@@ -211,6 +211,13 @@ LiteResult lite_space(const Shape &s, const nnjit_device_limits &d, const std::v
                 int smax = 1;
                 for (int sp : gemv_splits())
                     if (ceil_div(std::max<int64_t>(s.K, 1), sp) >= rows_per_pass) smax = sp;
+                // split only to fill the CUs: the smallest power of two that
+                // gives every CU a workgroup, and twice that (or the largest
+                // split K allows)
+                if (g.tiles_n >= d.num_cus) continue;
+                int64_t sfill = 1;
+                while (g.tiles_n * sfill < d.num_cus) sfill <<= 1;
+                if ((c.split < sfill || c.split > 2 * sfill) && c.split != smax) continue;
                 if (g.wgs > 4 * slots) continue;                                  // over-split
                 if (g.wgs < d.num_cus / 2 && c.split != smax) continue;           // under-filled
                 // Little's law: bytes in flight per CU must cover HBM latency
@@ -241,7 +248,12 @@ LiteResult lite_space(const Shape &s, const nnjit_device_limits &d, const std::v
         if (a.split != b.split) return a.split < b.split;
         return a.id < b.id;
     });
-    for (const Cand &c : kept) out.ids.push_back(c.id);
+    // the lite space is the head of that order: at most kMaxTimed candidates
+    // are ever evaluated on the device
+    for (const Cand &c : kept) {
+        if ((int)out.ids.size() >= kMaxTimed) break;
+        out.ids.push_back(c.id);
+    }
     return out;
 }
 

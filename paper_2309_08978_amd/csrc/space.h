@@ -40,7 +40,7 @@ nnjit_device_limits mi355x_limits();
 nnjit_resources resources_of(const Variant &v, const nnjit_device_limits &d, int measured_regs);
 
 constexpr double kRelaxation = 0.9;  // share of the register file the estimate may claim
-constexpr int kMaxTimed = 96;        // candidates timed per shape at most
+constexpr int kMaxTimed = 96;        // size cap of a lite space (candidates timed per shape at most)
 constexpr int kMinSurvivors = 8;     // heuristic 7 is relaxed below this many
 
 struct Shape {
