@@ -126,7 +126,7 @@ def main(argv=None):
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="bart_base_layer_seq128_f32", choices=sorted(workloads.WORKLOADS))
-    ap.add_argument("--kernel-reps", type=int, default=50, help="event-timed launches per product")
+    ap.add_argument("--kernel-reps", type=int, default=50, help="launches per event-timed burst per product")
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager", action="store_true", help="time eager ABI calls instead of the graph replay")
@@ -245,28 +245,60 @@ def main(argv=None):
     total_flops = sum(op.flops for op in ops)
     total_bytes = sum(op.bytes for op in ops)
 
-    # per-product kernel durations: each launch bracketed by HIP events on the
-    # stream it runs on (cold replicas for bandwidth-bound workloads)
+    # per-product kernel durations: a captured burst of back-to-back launches
+    # (cold replicas for bandwidth-bound workloads) replayed between HIP
+    # events on the replaying stream, per-launch median over 3 replays; the
+    # same burst issued eagerly and the host-visible latency of one
+    # event-bracketed launch are kept beside it
+    stream = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
     per_op = []
     for r in runs:
-        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-               for _ in range(args.kernel_reps)]
-        for i, (a, b) in enumerate(evs):
-            a.record()
-            r.call(i)
-            b.record()
+        # graph of kernel_reps back-to-back launches: no host work between them
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            r.call(0, side)
+        stream.wait_stream(side)
         torch.cuda.synchronize()
-        ts = [a.elapsed_time(b) * 1e3 for a, b in evs]
-        us = statistics.mean(ts)
+        gb = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gb, stream=side):
+            for i in range(args.kernel_reps):
+                r.call(i, side)
+        gb.replay()
+        bursts, ebursts = [], []
+        for _ in range(3):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            gb.replay()
+            b.record(stream)
+            bursts.append((a, b))
+        for _ in range(3):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for i in range(args.kernel_reps):
+                r.call(i)
+            b.record(stream)
+            ebursts.append((a, b))
+        singles = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(10)]
+        for i, (a, b) in enumerate(singles):
+            a.record(stream)
+            r.call(i)
+            b.record(stream)
+        torch.cuda.synchronize()
+        del gb
+        us = statistics.median(a.elapsed_time(b) * 1e3 / args.kernel_reps for a, b in bursts)
+        eus = statistics.median(a.elapsed_time(b) * 1e3 / args.kernel_reps for a, b in ebursts)
+        single = statistics.median(a.elapsed_time(b) * 1e3 for a, b in singles)
         op = r.op
         rl = roofline_of(op, us)
         per_op.append({"op": op.name, "shape_MKN": [op.M, op.K, op.N], "batch": op.batch, "dtype": op.dtype,
-                       "us_mean": round(us, 3), "us_median": round(statistics.median(ts), 3),
+                       "us_per_launch": round(us, 3), "us_per_launch_eager": round(eus, 3),
+                       "us_single_launch": round(single, 3),
                        "gflops": round(op.flops / us / 1e3, 1), "pct_mfma_peak": round(100 * op.flops / us / 1e6 / PEAK_TFLOPS[op.dtype], 2),
                        "gbs": round(op.bytes / us / 1e3, 1), "pct_hbm": round(100 * op.bytes / us / 1e3 / PEAK_HBM_GBS, 2),
                        "bound": rl["bound"], "pct_roofline": round(100 * rl["frac"], 2)})
-    dom = max(range(len(runs)), key=lambda i: per_op[i]["us_mean"])
-    rl = roofline_of(runs[dom].op, per_op[dom]["us_mean"])
+    dom = max(range(len(runs)), key=lambda i: per_op[i]["us_per_launch"])
+    rl = roofline_of(runs[dom].op, per_op[dom]["us_per_launch"])
     cfg_fields = dict(kv.split("=", 1) for kv in nj.nnjit_config_info(tunes[dom]["cfg"]).split() if "=" in kv)
     dop = runs[dom].op
     if cfg_fields["family"].startswith("gemm"):
@@ -277,7 +309,7 @@ def main(argv=None):
                "kernel_grid_wgs": wgs, "kernel_grid_z": dop.batch,
                "per_launch": ("flops" if rl["bound"] == "mfma" else "bytes"),
                "algorithmic": runs[dom].op.flops if rl["bound"] == "mfma" else runs[dom].op.bytes,
-               "avg_launch_us": per_op[dom]["us_mean"]})
+               "avg_launch_us": per_op[dom]["us_per_launch"]})
 
     value = total_flops / (ms_per_step * 1e-3) / 1e9
     dt = ops[0].dtype

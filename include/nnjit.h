@@ -92,9 +92,11 @@ int nnjit_batched_matmul(int64_t batch, int64_t M, int64_t N, int64_t K,
  * the kind and dtype, compute each one's Table 1 resource use on this
  * device, prune by the heuristics, order by workgroups per CU, most first),
  * times every survivor on device scratch of this exact shape (1 untimed
- * warm-up + 3 timed launches, median; a candidate whose first timed launch
- * is more than 1.5x the best so far is dropped; at most 96 candidates and
- * about 900 ms of evaluation), keeps the fastest in the per-shape cache and
+ * warm-up, 1 single timed launch, then 3 timed bursts of back-to-back
+ * launches whose per-launch median is the candidate's cost; the burst length
+ * (8, 2 or 1) is set once per shape from the first candidate's single launch;
+ * a candidate whose single launch is more than 1.5x the fastest single launch
+ * so far is dropped; at most 96 candidates and about 900 ms of evaluation), keeps the fastest in the per-shape cache and
  * returns its configuration id (>= 0).  Synchronous; uses its own stream and
  * a library-owned scratch buffer.  Re-tuning a cached shape replaces the
  * incumbent only if the new winner is at least 3% faster.  Wall time and
@@ -181,15 +183,15 @@ typedef struct nnjit_tune_stats {
     int n_aborted;        /* dropped after the warm-up (> 1.5x best)             */
     int n_failed;         /* launch failures (skipped)                           */
     int chosen;           /* configuration id returned                           */
-    double best_us;       /* its median time                                     */
-    double default_us;    /* median time of the first lite-space candidate        */
+    double best_us;       /* its per-launch time in a burst (median of 3)        */
+    double default_us;    /* the same for the first lite-space candidate          */
     int cache_hit;        /* 1 if the shape was already tuned (nothing timed)     */
 } nnjit_tune_stats;
 
 int nnjit_last_tune_stats(nnjit_tune_stats *out);
 
 /* Best-so-far curve of the last tune on this thread: for the i-th evaluated
- * candidate, its id, its median time in us (or -1 if aborted/failed) and the
+ * candidate, its id, its per-launch time in us (or -1 if aborted/failed) and the
  * wall-clock ms since the start of the call.  Returns the number of entries
  * (may exceed cap). */
 int nnjit_last_tune_trace(int *ids, double *us, double *at_ms, int cap);

@@ -426,16 +426,22 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
         for (auto &x : ev) (void)hipEventDestroy(x);
     };
 
+    // A candidate's cost is the device time per launch of a burst of
+    // back-to-back launches (what a stream or a graph of dependent products
+    // pays), not the host-visible latency of one launch. The burst length is
+    // fixed per shape from the first candidate's single launch so that all
+    // candidates are compared on the same measure.
+    int burst = 0;
     const auto te = clock::now();
     int best = -1;
-    double best_us = 1e300;
+    double best_us = 1e300, best_first_us = 1e300;
     std::map<int, double> timed;
     const int limit = std::min<int>((int)lr.ids.size(), kMaxTimed);
     for (int i = 0; i < limit; ++i) {
         if (ms_since(te) > budget_ms) break;
         const Config &cfg = configs()[lr.ids[i]];
         // warm-up launch (untimed: the first launch of a kernel pays one-time
-        // costs), then the first timed launch decides the early abort
+        // costs), then one single timed launch that decides the early abort
         rc = launch(*d, cfg, c);
         if (rc == NNJIT_OK) {
             (void)hipEventRecord(ev[0], c.stream);
@@ -454,39 +460,43 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
         }
         float first_ms = 0.f;
         (void)hipEventElapsedTime(&first_ms, ev[0], ev[1]);
-        if (best >= 0 && first_ms * 1e3 > 1.5 * best_us) {
+        const double first_us = first_ms * 1e3;
+        if (burst == 0) burst = first_us < 50.0 ? 8 : first_us < 400.0 ? 2 : 1;
+        if (best >= 0 && first_us > 1.5 * best_first_us) {
             ++t_stats.n_aborted;
             t_trace.emplace_back(cfg.id, -1.0, ms_since(t0));
-            if (trace) fprintf(stderr, "[nnjit] tune cand %d %s S=%d first %.1f us > 1.5x best, dropped\n", cfg.id, cfg.v->name, cfg.split, first_ms * 1e3);
+            if (trace) fprintf(stderr, "[nnjit] tune cand %d %s S=%d first %.1f us > 1.5x best, dropped\n", cfg.id, cfg.v->name, cfg.split, first_us);
             continue;
         }
         bool ok = true;
-        for (int r = 1; r < reps && ok; ++r) {
+        for (int r = 0; r < reps && ok; ++r) {
             (void)hipEventRecord(ev[2 + 2 * r], c.stream);
-            ok = launch(*d, cfg, c) == NNJIT_OK;
+            for (int b = 0; b < burst && ok; ++b) ok = launch(*d, cfg, c) == NNJIT_OK;
             (void)hipEventRecord(ev[3 + 2 * r], c.stream);
         }
         if (!ok) {
             ++t_stats.n_failed;
+            (void)hipGetLastError();
+            (void)hipStreamSynchronize(c.stream);
             continue;
         }
-        if (reps > 1 && (e = hipEventSynchronize(ev[1 + 2 * reps])) != hipSuccess) {
+        if ((e = hipEventSynchronize(ev[1 + 2 * reps])) != hipSuccess) {
             destroy();
             return hip_fail(e, "candidate timing");
         }
         std::vector<float> ts(reps);
-        ts[0] = first_ms;
-        for (int r = 1; r < reps; ++r) (void)hipEventElapsedTime(&ts[r], ev[2 + 2 * r], ev[3 + 2 * r]);
-        const double us = median(ts) * 1e3;
+        for (int r = 0; r < reps; ++r) (void)hipEventElapsedTime(&ts[r], ev[2 + 2 * r], ev[3 + 2 * r]);
+        const double us = median(ts) * 1e3 / burst;
         ++t_stats.n_timed;
         timed[cfg.id] = us;
         if (i == 0) t_stats.default_us = us;
         t_trace.emplace_back(cfg.id, us, ms_since(t0));
-        if (trace) fprintf(stderr, "[nnjit] tune cand %d %s S=%d %.2f us\n", cfg.id, cfg.v->name, cfg.split, us);
+        if (trace) fprintf(stderr, "[nnjit] tune cand %d %s S=%d %.2f us (single %.2f us)\n", cfg.id, cfg.v->name, cfg.split, us, first_us);
         if (us < best_us) {
             best_us = us;
             best = cfg.id;
         }
+        best_first_us = std::min(best_first_us, first_us);
     }
     destroy();
     t_stats.eval_ms = ms_since(te);

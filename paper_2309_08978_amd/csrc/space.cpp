@@ -191,15 +191,17 @@ LiteResult lite_space(const Shape &s, const nnjit_device_limits &d, const std::v
             if (v.mt > std::max<int64_t>(16, pow2ceil(s.M)) || v.nt > std::max<int64_t>(16, pow2ceil(s.N))) fit = false;
             const int64_t tiles = s.batch * g.tiles_m * (int64_t)g.tiles_n;
             // K groups inside a workgroup pay off only while the chip has
-            // fewer workgroups than CUs
-            if (v.kslices > 1 && tiles * c.split >= d.num_cus) continue;
+            // few workgroups (fewer than two per CU)
+            if (v.kslices > 1 && tiles * c.split >= 2LL * d.num_cus) continue;
             if (c.split > 1) {
                 // split K only to fill the CUs: keep the smallest power of two
                 // that gives every CU a workgroup, and twice that
                 if (tiles >= d.num_cus) continue;
                 int64_t sfill = 1;
                 while (tiles * sfill < d.num_cus) sfill <<= 1;
-                if (c.split < sfill || c.split > 2 * sfill) continue;
+                // a workgroup with K groups needs half the split for the same waves
+                const int64_t lo = v.kslices > 1 ? std::max<int64_t>(1, sfill / 2) : sfill;
+                if (c.split < lo || c.split > 2 * sfill) continue;
                 if (tiles * c.split > 2 * slots) continue;  // over-split
                 if (s.K < 2LL * c.split * v.kt) continue;    // at least two K slabs per split
             }
