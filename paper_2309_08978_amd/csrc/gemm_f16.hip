@@ -264,6 +264,282 @@ static hipError_t launch_gemm_f16(const void *params, dim3 grid, hipStream_t str
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Direct-copy variant ("gemm_f16t").  Both slabs go from global memory to LDS
+// with global_load_lds_dwordx4 (no staging registers, no LDS store
+// instructions): one such instruction moves 64 x 16 bytes and writes them to
+// LDS contiguously at a wave-uniform base, lane l at base + 16 l.  The LDS
+// layouts are therefore chosen by which global 16-byte chunk each lane
+// fetches.
+//
+// A slab: [Mt rows][128 bytes], chunk c of row r stored at slot
+//   c ^ ((r >> 1) & 7) (the conflict-free layout of the kernel above).
+// B slab: row-major [64 k rows][Nt halves], the 32-byte unit u of row k
+//   stored at unit u ^ sB(k), sB(k) = ((k & 3) << 1) | ((k >> 3) & 1).
+//
+// B is read with ds_read_b64_tr_b16.  Measured on gfx950: within each group
+// of 16 lanes, lanes 4r .. 4r+3 each name 8 bytes of a 16-half row r, and
+// lane i of the group receives column i of that 4 x 16 block (4 halves, one
+// per row).  Naming rows k .. k+3 of the slab at columns n .. n+15 gives lane
+// i the halves B[k .. k+3][n + i]: the K-contiguous fragment the matrix core
+// wants, without a transpose anywhere.  Two such reads make the 8 halves of
+// one fragment.  sB keeps the 4 rows of a group, and the two groups of a
+// half-wave (next 16 columns, or next 8 k rows), on distinct banks.
+//
+// Pipeline: ST LDS stages; slab kk is copied into stage kk % ST while slab
+// kk - ST + 1 is multiplied; one barrier per slab.
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt()
+{
+    static_assert(N >= 0 && N <= 63, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// 16 bytes per lane from global memory to LDS: lane l's bytes land at LDS
+// address lds + 16 l (lds must be wave-uniform).  Issued as inline assembly
+// so that the compiler does not treat the copy as an LDS store of unknown
+// target and wait for every copy in flight before each LDS read; the kernel
+// orders the copies against the reads itself (counted vmcnt waits plus a
+// barrier).  Vector memory loads complete in issue order, so the compiler's
+// own vmcnt waits stay correct with these extra loads in the queue.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"   // m0 is written on purpose
+__device__ __forceinline__ void copy16_to_lds(const void *src, unsigned lds)
+{
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// Scheduling pattern for NMMA matrix-core instructions and NRD LDS reads of
+// one K step: MFMA, reads, MFMA, reads, ... with the reads spread evenly.
+template <int Q, int NMMA, int NRD>
+__device__ __forceinline__ void interleave_mfma_ds()
+{
+    if constexpr (Q < NMMA) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+        constexpr int nr = (NRD * (Q + 1)) / NMMA - (NRD * Q) / NMMA;
+        if constexpr (nr > 0) __builtin_amdgcn_sched_group_barrier(0x100, nr, 0);   // LDS reads
+        interleave_mfma_ds<Q + 1, NMMA, NRD>();
+    }
+}
+
+// Workgroup barrier for the copy pipeline: this wave's LDS reads are complete
+// and every wave has arrived.  Global memory ordering is not needed here (the
+// copies are waited for by count), so unlike __syncthreads() it does not
+// wait for all outstanding vector memory operations.
+__device__ __forceinline__ void lds_barrier()
+{
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+template <int MT, int NT, int WM, int WN, int MF, int ST>
+__global__ void __launch_bounds__(WM * WN * 64)
+gemm_f16t_kernel(GemmParams p)
+{
+    typedef Mfma16<MF> I;
+    typedef typename I::acc_t acc_t;
+    constexpr int KT = 64;
+    constexpr int NW = WM * WN;
+    constexpr int WTM = MT / WM, WTN = NT / WN;
+    constexpr int FM = WTM / MF, FN = WTN / MF;
+    constexpr int KG = 64 / MF;                 // lane groups along k
+    constexpr int NSTEP = KT / (8 * KG);        // instructions per slab and fragment pair
+    constexpr int A_BYTES = MT * 128;
+    constexpr int B_ROW = NT * 2;
+    constexpr int B_BYTES = KT * B_ROW;
+    constexpr int STAGE = A_BYTES + B_BYTES;
+    constexpr int LA = A_BYTES / 1024 / NW, LB = B_BYTES / 1024 / NW;   // copies per wave and slab
+    static_assert(LA * NW * 1024 == A_BYTES && LB * NW * 1024 == B_BYTES, "copies must split evenly over waves");
+    static_assert(NT >= 128 && (NT & (NT - 1)) == 0, "B swizzle needs a power-of-two row of >= 8 units");
+    static_assert(FM >= 1 && FN >= 1 && WTM % MF == 0 && WTN % MF == 0, "wave tile");
+    static_assert((ST - 2) * (LA + LB) <= 63, "copies in flight exceed the vmcnt range");
+
+    // one LDS object per stage, so that the compiler can tell which stage a
+    // fragment read depends on
+    __shared__ __attribute__((aligned(1024))) char smem0[STAGE];
+    __shared__ __attribute__((aligned(1024))) char smem1[STAGE];
+    __shared__ __attribute__((aligned(1024))) char smem2[ST > 2 ? STAGE : 1024];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / WN, wn = wave % WN;
+
+    const int tiles = p.tiles_m * p.tiles_n;
+    const int gx = gridDim.x;
+    const int logical = xcd_remap(blockIdx.x + gx * blockIdx.z, gx * gridDim.z);
+    const int z = logical / gx;
+    const int rest = logical - z * gx;
+    const int s = rest / tiles;
+    const int tile = rest - s * tiles;
+    const int tm = tile % p.tiles_m, tn = tile / p.tiles_m;
+    const int m0 = tm * MT, n0 = tn * NT;
+    const int kbeg = s * p.kchunk;
+    const int kend = min(p.K, kbeg + p.kchunk);
+    const int nk = kend > kbeg ? (kend - kbeg + KT - 1) / KT : 0;
+
+    const unsigned short *A = (const unsigned short *)p.A + (long long)z * p.sA;
+    const unsigned short *B = (const unsigned short *)p.B + (long long)z * p.sB;
+    float *C = p.C + (long long)z * p.sC;
+    const int M = p.M, N = p.N;
+    const long long lda = p.lda, ldb = p.ldb;
+    const unsigned short *zero = (const unsigned short *)p.zero;
+    typedef __attribute__((address_space(3))) char lds_char;
+    auto stage_base = [&](int u) -> lds_char * {
+        return (lds_char *)(u == 0 ? smem0 : u == 1 ? smem1 : smem2);
+    };
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+
+    // per-lane sources of this wave's copies for the split's first slab;
+    // slab kk adds a uniform offset (kk * 64 columns of A, kk * 64 rows of B)
+    const unsigned short *a_src[LA];
+    int a_k[LA];
+    bool a_ok[LA];
+#pragma unroll
+    for (int j = 0; j < LA; ++j) {
+        const int row = 8 * (wave + j * NW) + (lane >> 3);
+        const int col = 8 * ((lane & 7) ^ ((row >> 1) & 7));
+        a_ok[j] = m0 + row < M;
+        a_k[j] = kbeg + col;
+        a_src[j] = A + (long long)(a_ok[j] ? m0 + row : 0) * lda + kbeg + col;
+    }
+    const unsigned short *b_src[LB];
+    int b_k[LB];
+    bool b_ok[LB];
+#pragma unroll
+    for (int j = 0; j < LB; ++j) {
+        const int o = 1024 * (wave + j * NW) + 16 * lane;
+        const int k = o / B_ROW, pos = (o % B_ROW) >> 4;
+        const int sb = ((k & 3) << 1) | ((k >> 3) & 1);
+        const int col = 16 * ((pos >> 1) ^ sb) + 8 * (pos & 1);
+        b_ok[j] = n0 + col < N;
+        b_k[j] = kbeg + k;
+        b_src[j] = B + (long long)(kbeg + k) * ldb + (b_ok[j] ? n0 + col : 0);
+    }
+
+    auto copy_slab = [&](int stage, int kk) {
+        const bool live = kk < nk;
+        const int dk = kk * KT;
+        const long long db = (long long)dk * ldb;
+#pragma unroll
+        for (int j = 0; j < LA; ++j) {
+            const bool ok = live && a_ok[j] && a_k[j] + dk < kend;
+            copy16_to_lds(ok ? a_src[j] + dk : zero, (unsigned)(uintptr_t)(stage_base(stage) + 1024 * (wave_u + j * NW)));
+        }
+#pragma unroll
+        for (int j = 0; j < LB; ++j) {
+            const bool ok = live && b_ok[j] && b_k[j] + dk < kend;
+            copy16_to_lds(ok ? b_src[j] + db : zero,
+                          (unsigned)(uintptr_t)(stage_base(stage) + A_BYTES + 1024 * (wave_u + j * NW)));
+        }
+    };
+
+    acc_t acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int r = 0; r < I::NR; ++r) acc[i][j][r] = 0.f;
+
+    // lane constants of the fragment reads
+    const int li = lane % MF, lg = lane / MF;
+    const int grp = lane >> 4, tr_r = (lane >> 2) & 3, tr_q = lane & 3;
+    const int tr_g = MF == 32 ? grp >> 1 : grp;              // k lane group of this 16-lane group
+    const int tr_n = (MF == 32 ? 16 * (grp & 1) : 0) + 4 * tr_q;
+
+    // fragments of one K step (FM A fragments, FN B fragments)
+    auto read_frags = [&](lds_char *sa, int st, f16x8 (&a)[FM], f16x8 (&b)[FN]) {
+        lds_char *sbp = sa + A_BYTES;
+        const int chunk = st * KG + lg;
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+            const int row = wm * WTM + i * MF + li;
+            a[i] = __builtin_bit_cast(f16x8, *(lds_u32x4 *)(sa + row * 128 + 16 * (chunk ^ ((row >> 1) & 7))));
+        }
+        const int kc = st * KG + tr_g;                       // 8-row k chunk of this lane group
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+            const int n = wn * WTN + j * MF + tr_n;
+            s16x4 h[2];
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh) {
+                const int k = 8 * kc + 4 * hh + tr_r;
+                const int unit = (n >> 4) ^ ((tr_r << 1) | (kc & 1));
+                h[hh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(sbp + k * B_ROW + unit * 32 + (n & 15) * 2));
+            }
+            b[j] = __builtin_bit_cast(f16x8, __builtin_shufflevector(h[0], h[1], 0, 1, 2, 3, 4, 5, 6, 7));
+        }
+    };
+
+    // One slab: the fragments of step st + 1 are read while the matrix
+    // cores work on step st, and the scheduler is told to interleave the
+    // two (one MFMA, then a share of the LDS reads), so that a wave's own
+    // MFMAs cover its LDS latency.
+    constexpr int NMMA = FM * FN, NRD = FM + 2 * FN;
+    auto compute = [&](int stage) {
+        lds_char *sa = stage_base(stage);
+        f16x8 a[2][FM], b[2][FN];
+        read_frags(sa, 0, a[0], b[0]);
+#pragma unroll
+        for (int st = 0; st < NSTEP; ++st) {
+            const int cur = st & 1;
+            if (st + 1 < NSTEP) read_frags(sa, st + 1, a[cur ^ 1], b[cur ^ 1]);
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j) acc[i][j] = I::mma(a[cur][i], b[cur][j], acc[i][j]);
+            if (st + 1 < NSTEP) interleave_mfma_ds<0, NMMA, NRD>();
+        }
+    };
+
+#pragma unroll
+    for (int u = 0; u < ST - 1; ++u) copy_slab(u, u);
+    for (int it0 = 0; it0 < nk; it0 += ST) {
+#pragma unroll
+        for (int u = 0; u < ST; ++u) {
+            const int it = it0 + u;
+            // this wave's copies of slab `it` are done once at most the
+            // copies of the ST - 2 later slabs are pending; the barrier
+            // then makes every wave's copies visible and frees the stage
+            // multiplied in the previous iteration
+            wait_vmcnt<(ST - 2) * (LA + LB)>();
+            lds_barrier();
+            copy_slab((u + ST - 1) % ST, it + ST - 1);
+            if (it < nk) compute(u);
+        }
+    }
+    wait_vmcnt<0>();   // no copy may still target LDS when the workgroup ends
+
+    const int rbase = m0 + wm * WTM, cbase = n0 + wn * WTN + li;
+    float *out = C;
+    long long ldo = p.ldc;
+    if (p.S > 1) {
+        out = p.ws + ((long long)s * p.batch + z) * (long long)M * N;
+        ldo = N;
+    }
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int r = 0; r < I::NR; ++r) {
+                const int row = rbase + i * MF + I::row_of(r, lg), col = cbase + j * MF;
+                if (row < M && col < N) out[(long long)row * ldo + col] = acc[i][j][r];
+            }
+}
+
+template <int MT, int NT, int WM, int WN, int MF, int ST>
+static hipError_t launch_gemm_f16t(const void *params, dim3 grid, hipStream_t stream)
+{
+    hipLaunchKernelGGL((gemm_f16t_kernel<MT, NT, WM, WN, MF, ST>), grid, dim3(WM * WN * 64), 0, stream,
+                       *(const GemmParams *)params);
+    return hipGetLastError();
+}
+
 // Table 1 register formula for one lane (see est_regs_f32): accumulators,
 // one K step of A and B fragments (4 VGPRs per 8 halves), the staging
 // registers of the global->LDS copy (B needs eight 128-bit rows per 8x8
@@ -314,13 +590,52 @@ constexpr int lds_f16(int mt, int nt, int st) { return st * (mt + nt) * 128; }
     X(64, 64, 2, 2, 32, 2, 1, false) \
     X(32, 32, 1, 1, 32, 2, 1, false)
 
+// Direct-copy family: accumulators, one K step of fragments, the per-lane
+// copy geometry (2 registers per copy) and a fixed overhead; no staging.
+constexpr int est_regs_f16t(int mt, int nt, int wm, int wn, int mf) {
+    return (mt / wm) * (nt / wn) / 64 + 4 * ((mt / wm) / mf) + 4 * ((nt / wn) / mf) +
+           2 * (mt * 128 / 1024 / (wm * wn) + nt * 128 / 1024 / (wm * wn)) + 32;
+}
+
+#define NNJIT_F16T_VARIANT(MT, NT, WM, WN, MF, ST)                                                          \
+    {"gemm_f16t_" #MT "x" #NT "x64_w" #WM "x" #WN "_m" #MF "_s" #ST, FAM_GEMM_F16, MF, (MF == 32 ? 16 : 32),     \
+     MT, NT, 64, WM, WN, ST, ST - 1, 1, 16, 0, 0, WM * WN * 64, lds_f16(MT, NT, ST),                          \
+     est_regs_f16t(MT, NT, WM, WN, MF), (const void *)&gemm_f16t_kernel<MT, NT, WM, WN, MF, ST>,              \
+     &launch_gemm_f16t<MT, NT, WM, WN, MF, ST>}
+
+// The compiled direct-copy configurations (16-byte aligned operands, Nt >= 128).
+#define NNJIT_F16T_LIST(X) \
+    X(256, 256, 4, 2, 32, 2) \
+    X(256, 256, 2, 4, 32, 2) \
+    X(256, 128, 2, 2, 32, 2) \
+    X(256, 128, 2, 2, 32, 3) \
+    X(256, 128, 4, 2, 32, 2) \
+    X(256, 128, 4, 2, 32, 3) \
+    X(128, 256, 2, 2, 32, 2) \
+    X(128, 256, 2, 2, 32, 3) \
+    X(128, 256, 2, 4, 32, 2) \
+    X(128, 256, 2, 4, 32, 3) \
+    X(128, 128, 2, 2, 32, 2) \
+    X(128, 128, 2, 2, 32, 3) \
+    X(128, 128, 2, 2, 16, 2) \
+    X(128, 128, 2, 2, 16, 3) \
+    X(128, 128, 4, 2, 32, 3) \
+    X(64, 128, 2, 2, 32, 2) \
+    X(64, 128, 2, 2, 32, 3) \
+    X(64, 128, 1, 2, 32, 3)
+
+#define NNJIT_F16T_INST(MT, NT, WM, WN, MF, ST) \
+    template __global__ void gemm_f16t_kernel<MT, NT, WM, WN, MF, ST>(GemmParams);
+NNJIT_F16T_LIST(NNJIT_F16T_INST)
+
 #define NNJIT_F16_INST(MT, NT, WM, WN, MF, ST, PF, VEC) \
     template __global__ void gemm_f16_kernel<MT, NT, WM, WN, MF, ST, PF, VEC>(GemmParams);
 NNJIT_F16_LIST(NNJIT_F16_INST)
 
 #if !defined(__HIP_DEVICE_COMPILE__)
 #define NNJIT_F16_ENTRY(...) NNJIT_F16_VARIANT(__VA_ARGS__),
-const Variant kGemmF16Variants[] = {NNJIT_F16_LIST(NNJIT_F16_ENTRY)};
+#define NNJIT_F16T_ENTRY(...) NNJIT_F16T_VARIANT(__VA_ARGS__),
+const Variant kGemmF16Variants[] = {NNJIT_F16_LIST(NNJIT_F16_ENTRY) NNJIT_F16T_LIST(NNJIT_F16T_ENTRY)};
 const int kNumGemmF16Variants = sizeof(kGemmF16Variants) / sizeof(kGemmF16Variants[0]);
 #endif
 
