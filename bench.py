@@ -92,6 +92,23 @@ def roofline_of(op, us):
             "frac": achieved / PEAK_HBM_GBS, "traffic": None}
 
 
+def measured_traffic(db_path, workload, op, config_info):
+    """HBM bytes per launch of this product from the counter database, or
+    None when it has no entry for the exact configuration or the kernel
+    sources changed since the counters were taken."""
+    try:
+        with open(db_path) as f:
+            db = json.load(f)
+    except (OSError, ValueError):
+        return None
+    cfg = config_info.split()[0].split("=", 1)[1]
+    split = int(config_info.rsplit("split=", 1)[1])
+    e = db.get(f"{workload}|{op}|{cfg}|{split}")
+    if not e or e.get("digest") != nj.kernel_digest():
+        return None
+    return e["hbm_bytes_per_launch"]
+
+
 def cpu_baseline(name, budget_s: float):
     """The oracle (CPU, fp64) on the same workload: whole steps, repeated
     until about `budget_s` seconds of CPU work have run (at least one step)."""
@@ -134,6 +151,11 @@ def main(argv=None):
                     help="kernel database file: loaded before tuning if it exists, written after")
     ap.add_argument("--copy-ref-mb", type=int, default=0,
                     help="first run a plain device copy of this many MiB (reference for HBM counter scaling)")
+    ap.add_argument("--profile-op", default=None,
+                    help="counter-collection mode: tune, run the reference copy, then launch only this product "
+                         "--kernel-reps times and print one metadata line")
+    ap.add_argument("--traffic-db", default=os.path.join(ROOT, "profiles", "traffic.json"),
+                    help="measured HBM traffic per launch (written from rocprofv3 counter runs)")
     args = ap.parse_args(argv)
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -189,6 +211,21 @@ def main(argv=None):
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+
+    if args.profile_op is not None:
+        # counter-collection mode: after the reference copy, only this
+        # product runs (kernel_reps launches, rotating weight replicas)
+        idx = next(i for i, r in enumerate(runs) if r.op.name == args.profile_op)
+        r = runs[idx]
+        for i in range(args.kernel_reps):
+            r.call(i)
+        torch.cuda.synchronize()
+        t = tunes[idx]
+        print(json.dumps({"workload": name, "op": r.op.name, "config": t["config"].split()[0].split("=", 1)[1],
+                          "split": int(t["config"].rsplit("split=", 1)[1]), "reps": args.kernel_reps,
+                          "copy_ref_mb": args.copy_ref_mb, "algorithmic_bytes": r.op.bytes,
+                          "digest": nj.kernel_digest()}), flush=True)
+        return 0
 
     def step(k=0):
         for r in runs:
@@ -305,6 +342,7 @@ def main(argv=None):
         wgs = -(-dop.M // int(cfg_fields["Mt"])) * -(-dop.N // int(cfg_fields["Nt"])) * int(cfg_fields["split"])
     else:
         wgs = -(-dop.N // int(cfg_fields["cols"])) * int(cfg_fields["split"])
+    rl["traffic"] = measured_traffic(args.traffic_db, name, dop.name, tunes[dom]["config"])
     rl.update({"kernel_op": per_op[dom]["op"], "kernel_config": tunes[dom]["config"],
                "kernel_grid_wgs": wgs, "kernel_grid_z": dop.batch,
                "per_launch": ("flops" if rl["bound"] == "mfma" else "bytes"),

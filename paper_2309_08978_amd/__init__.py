@@ -223,6 +223,18 @@ def nnjit_version() -> int:
 
 # ------------------------------------------------------------ conveniences
 
+def kernel_digest() -> str:
+    """Short digest of the kernel and launch sources (csrc/): counter
+    measurements recorded against one digest are stale under another."""
+    import hashlib
+    h = hashlib.sha256()
+    d = os.path.join(HERE, "csrc")
+    for name in sorted(os.listdir(d)):
+        with open(os.path.join(d, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
+
+
 def dtype_code(t) -> int:
     import torch
     if t.dtype == torch.float32:

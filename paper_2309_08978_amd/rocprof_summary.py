@@ -11,6 +11,11 @@ or of a ``--pmc`` run (``*_counter_collection.csv``), and prints:
 * for a counter run, the per-dispatch mean of each counter per (kernel, grid).
 
     python -m paper_2309_08978_amd.rocprof_summary <rocprofv3 output dir> [--last N]
+
+With --traffic FETCH_DIR WRITE_DIR --meta META [--db profiles/traffic.json] it
+turns two counter runs of ``bench.py --profile-op`` (``rocprofv3 --pmc
+FETCH_SIZE`` and ``--pmc WRITE_SIZE``) into HBM bytes per launch of the
+profiled product, scaled by the reference copy in the same run.
 """
 from __future__ import annotations
 
@@ -79,12 +84,74 @@ def summarize(out_dir: str, last: int, top: int = 12) -> str:
     return "\n".join(lines)
 
 
+def _pmc_dispatches(out_dir, counter):
+    """[(kernel name, grid in workgroups, counter value)] in dispatch order."""
+    path = sorted(glob.glob(os.path.join(out_dir, "**", "*counter_collection.csv"), recursive=True))
+    if not path:
+        raise SystemExit(f"no counter_collection.csv under {out_dir}")
+    per = OrderedDict()
+    for r in _rows(path[0]):
+        if r["Counter_Name"] != counter:
+            continue
+        d = int(r["Dispatch_Id"])
+        wg = int(r.get("Workgroup_Size", 1) or 1)
+        if d not in per:
+            per[d] = [r["Kernel_Name"], int(r.get("Grid_Size", 0) or 0) // max(wg, 1), 0.0]
+        per[d][2] += float(r["Counter_Value"])
+    return [tuple(v) for _, v in sorted(per.items())]
+
+
+def traffic(fetch_dir, write_dir, meta):
+    """HBM bytes per launch of the profiled product (bench.py --profile-op):
+    the product's dispatches after the reference copy, FETCH_SIZE and
+    WRITE_SIZE (KiB) each scaled by what the counter reads for the copy."""
+    ref_bytes = meta["copy_ref_mb"] << 20
+    out = {}
+    for key, d, counter in (("fetch", fetch_dir, "FETCH_SIZE"), ("write", write_dir, "WRITE_SIZE")):
+        rows = _pmc_dispatches(d, counter)
+        copies = [i for i, r in enumerate(rows) if "copyBuffer" in r[0] or "copy_kernel" in r[0]]
+        if not copies:
+            raise SystemExit(f"{d}: no reference copy dispatch found")
+        ref = statistics.mean(rows[i][2] for i in copies)
+        factor = ref_bytes / (ref * 1024.0)
+        after = [r for r in rows[copies[-1] + 1:] if "nnjit" in r[0]]
+        kib = sum(r[2] for r in after) / meta["reps"]
+        out[key] = {"kib_per_launch_raw": round(kib, 1), "scale": round(factor, 4),
+                    "bytes_per_launch": round(kib * 1024.0 * factor),
+                    "kernels": sorted({f"{_short(r[0])} x{r[1]}" for r in after})}
+    total = out["fetch"]["bytes_per_launch"] + out["write"]["bytes_per_launch"]
+    return {"digest": meta["digest"], "hbm_bytes_per_launch": total, "algorithmic_bytes": meta["algorithmic_bytes"],
+            "ratio_to_algorithmic": round(total / meta["algorithmic_bytes"], 3), "fetch": out["fetch"],
+            "write": out["write"], "reps": meta["reps"], "copy_ref_mb": meta["copy_ref_mb"]}
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser()
-    ap.add_argument("out_dir")
+    ap.add_argument("out_dir", nargs="?")
     ap.add_argument("--last", type=int, default=0, help="only the last N dispatches in the per-grid table")
     ap.add_argument("--top", type=int, default=12)
+    ap.add_argument("--traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="counter runs of bench.py --profile-op: record HBM bytes per launch")
+    ap.add_argument("--meta", help="file holding the metadata line bench.py --profile-op printed")
+    ap.add_argument("--db", help="traffic database (JSON) to add the entry to")
     a = ap.parse_args(argv)
+    if a.traffic:
+        import json
+        with open(a.meta) as f:
+            meta = next(json.loads(l) for l in f if l.startswith("{"))
+        entry = traffic(a.traffic[0], a.traffic[1], meta)
+        key = f"{meta['workload']}|{meta['op']}|{meta['config']}|{meta['split']}"
+        print(key, json.dumps(entry, indent=1))
+        if a.db:
+            db = {}
+            if os.path.exists(a.db):
+                with open(a.db) as f:
+                    db = json.load(f)
+            db[key] = entry
+            with open(a.db, "w") as f:
+                json.dump(db, f, indent=1, sort_keys=True)
+                f.write("\n")
+        return 0
     print(summarize(a.out_dir, a.last, a.top))
     return 0
 
