@@ -244,34 +244,50 @@ def main(argv=None):
     torch.cuda.synchronize()
     eager_ms = e0.elapsed_time(e1) / n_eager
 
-    # graph of `copies` consecutive steps (one replica of the weights each)
-    graph = None
+    # graph of `per_graph` consecutive steps: at least one per weight replica,
+    # and enough steps (up to ~0.5 ms of work) that the per-replay launch
+    # cost of the graph is amortised
+    per_graph = copies
+    if eager_ms < 0.5:
+        per_graph = max(copies, min(64, math.ceil(0.5 / max(eager_ms, 1e-3))))
+    graph = rest = None
     if not args.eager:
-        g = torch.cuda.CUDAGraph()
         side = torch.cuda.Stream()
-        side.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(side):
-            for k in range(copies):
-                step(k)  # warm-up on the capture stream (its split-K scratch)
-        torch.cuda.current_stream().wait_stream(side)
-        torch.cuda.synchronize()
-        with torch.cuda.graph(g, stream=side):
-            for k in range(copies):
-                step(k)
-        graph = g
-        for _ in range(max(1, args.warmup // copies)):
+
+        def capture(n):
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                for k in range(n):
+                    step(k)  # warm-up on the capture stream (its split-K scratch)
+            torch.cuda.current_stream().wait_stream(side)
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=side):
+                for k in range(n):
+                    step(k)
+            return g
+
+        per_graph = min(per_graph, args.steps)
+        graph = capture(per_graph)
+        if args.steps % per_graph:
+            rest = capture(args.steps % per_graph)   # the timed region runs exactly --steps steps
+        for _ in range(max(1, args.warmup // per_graph)):
             graph.replay()
+        if rest is not None:
+            rest.replay()
         torch.cuda.synchronize()
 
     # timed region
-    replays = max(1, args.steps // copies) if graph is not None else args.steps
-    nsteps = replays * copies if graph is not None else args.steps
+    replays = args.steps // per_graph if graph is not None else args.steps
+    nsteps = args.steps
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     e0.record()
     if graph is not None:
         for _ in range(replays):
             graph.replay()
+        if rest is not None:
+            rest.replay()
     else:
         for k in range(args.steps):
             step(k)
@@ -357,7 +373,7 @@ def main(argv=None):
         "vs_baseline": None, "dtype": dt, "data": "synthetic",
         "config": {"workload": name, "products": [[op.name, op.batch, op.M, op.K, op.N] for op in ops],
                    "timing": "graph replay" if graph is not None else "eager ABI calls",
-                   "weight_replicas": copies},
+                   "weight_replicas": copies, "steps_per_graph": per_graph if graph is not None else None},
         "pct_mfma_peak": round(100 * value / 1e3 / PEAK_TFLOPS[dt], 2),
         "gbs": round(total_bytes / (ms_per_step * 1e-3) / 1e9, 1),
         "eager_ms_per_step": round(eager_ms, 5),
