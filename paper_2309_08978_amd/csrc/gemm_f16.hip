@@ -292,28 +292,6 @@ typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
 
-template <int N>
-__device__ __forceinline__ void wait_vmcnt()
-{
-    static_assert(N >= 0 && N <= 63, "vmcnt range");
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-
-// 16 bytes per lane from global memory to LDS: lane l's bytes land at LDS
-// address lds + 16 l (lds must be wave-uniform).  Issued as inline assembly
-// so that the compiler does not treat the copy as an LDS store of unknown
-// target and wait for every copy in flight before each LDS read; the kernel
-// orders the copies against the reads itself (counted vmcnt waits plus a
-// barrier).  Vector memory loads complete in issue order, so the compiler's
-// own vmcnt waits stay correct with these extra loads in the queue.
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"   // m0 is written on purpose
-__device__ __forceinline__ void copy16_to_lds(const void *src, unsigned lds)
-{
-    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds) : "memory", "m0");
-}
-#pragma clang diagnostic pop
-
 // Scheduling pattern for NMMA matrix-core instructions and NRD LDS reads of
 // one K step: MFMA, reads, MFMA, reads, ... with the reads spread evenly.
 template <int Q, int NMMA, int NRD>
@@ -325,15 +303,6 @@ __device__ __forceinline__ void interleave_mfma_ds()
         if constexpr (nr > 0) __builtin_amdgcn_sched_group_barrier(0x100, nr, 0);   // LDS reads
         interleave_mfma_ds<Q + 1, NMMA, NRD>();
     }
-}
-
-// Workgroup barrier for the copy pipeline: this wave's LDS reads are complete
-// and every wave has arrived.  Global memory ordering is not needed here (the
-// copies are waited for by count), so unlike __syncthreads() it does not
-// wait for all outstanding vector memory operations.
-__device__ __forceinline__ void lds_barrier()
-{
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
 template <int MT, int NT, int WM, int WN, int MF, int ST>
@@ -601,7 +570,7 @@ constexpr int est_regs_f16t(int mt, int nt, int wm, int wn, int mf) {
     {"gemm_f16t_" #MT "x" #NT "x64_w" #WM "x" #WN "_m" #MF "_s" #ST, FAM_GEMM_F16, MF, (MF == 32 ? 16 : 32),     \
      MT, NT, 64, WM, WN, ST, ST - 1, 1, 16, 0, 0, WM * WN * 64, lds_f16(MT, NT, ST),                          \
      est_regs_f16t(MT, NT, WM, WN, MF), (const void *)&gemm_f16t_kernel<MT, NT, WM, WN, MF, ST>,              \
-     &launch_gemm_f16t<MT, NT, WM, WN, MF, ST>}
+     &launch_gemm_f16t<MT, NT, WM, WN, MF, ST>, 1}
 
 // The compiled direct-copy configurations (16-byte aligned operands, Nt >= 128).
 #define NNJIT_F16T_LIST(X) \

@@ -300,32 +300,53 @@ static hipError_t launch_gemm_f32(const void *params, dim3 grid, hipStream_t str
 }
 
 // ---------------------------------------------------------------------------
-// LDS-free ("direct") variant for small M.  Every wave owns a WTM x WTN block
-// of C and one K slice; it loads its matrix-core fragments straight from
-// global memory (L2-resident operands at these sizes) into a ring of PF
-// register sets and never waits at a barrier inside the K loop.  A
-// workgroup holds CB column blocks x KS K slices of waves: the CB waves of a
-// slice share A rows in L1, and at the end the KS slices of a block are
-// added through LDS in slice order (deterministic).  Fragment lane layout as
-// above: lane group g takes k in [g*KL, (g+1)*KL) of each K slab, so its A
-// values are 16-byte contiguous and its B values are one 4-byte word per k
-// (consecutive lanes read consecutive columns, coalesced).
-template <int WTM, int WTN, int KT, int CB, int MF, int PF, int KS, bool VEC>
-__global__ void __launch_bounds__(CB * KS * 64)
-gemm_f32_direct_kernel(GemmParams p)
+// Wave-private K slices ("gemm_f32w") for small-M products.  A workgroup of
+// KS waves computes one Mt x Nt tile; wave w takes the K slabs w, w + KS,
+// w + 2 KS, ... of the workgroup's K range into its own LDS region with
+// global_load_lds_dwordx4 (ST stages) and multiplies them with no barrier in
+// the K loop: it waits only for its own copies, by count.  At the end the KS
+// partial tiles are added through LDS in wave order (deterministic), each
+// wave summing and storing its share of the tile.  Against the shared-slab
+// kernel above this gives up operand sharing between waves for a deeper
+// pipeline (ST - 1 slabs per wave in flight) and no workgroup lock-step.
+//
+// Layouts (Kt = 16): A slab [Mt rows][16 floats], the 16-byte piece p of row
+// r at piece p ^ ((r >> 2) & 3), so 16 consecutive rows read at one piece hit
+// distinct banks; B slab [16 k rows][Nt floats] in 1 KiB copy chunks of R
+// rows, each chunk followed by a 16 R-byte gap, so that rows k and k + 8,
+// which the two half-waves read in the same instruction, sit on opposite
+// halves of the 64 banks.  Lane group g (l / 32) takes k in [8g, 8g + 8) of
+// a slab, as in the kernel above.
+template <int MT, int NT, int KS, int ST>
+__global__ void __launch_bounds__(KS * 64)
+gemm_f32w_kernel(GemmParams p)
 {
-    typedef Mfma32<MF> I;
+    typedef Mfma32<32> I;
     typedef typename I::acc_t acc_t;
-    constexpr int FM = WTM / MF, FN = WTN / MF;
-    constexpr int KG = 64 / MF;          // lane groups along k
-    constexpr int KL = KT / KG;          // k values of one lane group per slab
+    constexpr int KT = 16;
+    constexpr int FM = MT / 32, FN = NT / 32;
+    constexpr int A_BYTES = MT * KT * 4;
+    constexpr int B_ROW = NT * 4;
+    constexpr int RB = 1024 / B_ROW;               // B rows per copy chunk
+    constexpr int B_CHUNK = 1024 + 16 * RB;        // chunk plus its bank-half gap
+    constexpr int NBC = KT / RB;                   // B copies per slab
+    constexpr int NA = A_BYTES / 1024;             // A copies per slab
+    constexpr int NCOPY = NA + NBC;
+    constexpr int STAGE = A_BYTES + NBC * B_CHUNK;
+    constexpr int WAVE_LDS = ST * STAGE;
     constexpr int NREG = FM * FN * I::NR;
-    static_assert(FM >= 1 && FN >= 1 && KL % 4 == 0, "direct tile");
+    constexpr int RED = KS * NREG * 64 * 4;
+    constexpr int LDS_BYTES = KS * WAVE_LDS > RED ? KS * WAVE_LDS : RED;
+    static_assert(MT % 32 == 0 && NT % 32 == 0 && NT <= 256 && A_BYTES % 1024 == 0, "tile");
+    static_assert(NREG % KS == 0, "epilogue share");
+    static_assert((ST - 2) * NCOPY <= 63, "copies in flight exceed the vmcnt range");
 
-    const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
-    const int cb = wave % CB, ks = wave / CB;       // column block, K slice
-    const int li = lane % MF, lg = lane / MF;
+    __shared__ __attribute__((aligned(1024))) char smem[LDS_BYTES];
+    typedef __attribute__((address_space(3))) char lds_char;
+
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+    const int li = lane & 31, lg = lane >> 5;
 
     const int tiles = p.tiles_m * p.tiles_n;
     const int gx = gridDim.x;
@@ -335,13 +356,11 @@ gemm_f32_direct_kernel(GemmParams p)
     const int s = rest / tiles;
     const int tile = rest - s * tiles;
     const int tm = tile % p.tiles_m, tn = tile / p.tiles_m;
-    const int m0 = tm * WTM, n0 = tn * (CB * WTN) + cb * WTN;
+    const int m0 = tm * MT, n0 = tn * NT;
     const int kbeg = s * p.kchunk;
     const int kend = min(p.K, kbeg + p.kchunk);
     const int nk = kend > kbeg ? (kend - kbeg + KT - 1) / KT : 0;
-    const int nps = (nk + KS - 1) / KS;              // slabs of one K slice
-    const int sl0 = ks * nps;                        // this slice's first slab
-    const int nmine = max(0, min(nk - sl0, nps));
+    const int nmine = nk > wave ? (nk - wave + KS - 1) / KS : 0;    // slabs of this wave
 
     const float *A = (const float *)p.A + (long long)z * p.sA;
     const float *B = (const float *)p.B + (long long)z * p.sB;
@@ -349,34 +368,49 @@ gemm_f32_direct_kernel(GemmParams p)
     const int M = p.M, N = p.N;
     const long long lda = p.lda, ldb = p.ldb;
     const float *zero = (const float *)p.zero;
+    lds_char *mine = (lds_char *)smem + wave_u * WAVE_LDS;
 
-    f32x4 ra[PF][FM][KL / 4];
-    float rb[PF][FN][KL];
-    auto gload = [&](int set, int it) {
-        const int k0 = kbeg + (sl0 + it) * KT + lg * KL;
-        const bool okk = it < nmine;
+    // per-lane copy sources for slab 0 of the workgroup's range
+    const float *a_src[NA];
+    int a_k[NA];
+    bool a_ok[NA];
 #pragma unroll
-        for (int i = 0; i < FM; ++i) {
-            const int gm = m0 + i * MF + li;
-            const float *src = A + (long long)gm * lda + k0;
+    for (int c = 0; c < NA; ++c) {
+        const int row = 16 * c + (lane >> 2);
+        const int piece = (lane & 3) ^ ((row >> 2) & 3);
+        a_ok[c] = m0 + row < M;
+        a_k[c] = kbeg + 4 * piece;
+        a_src[c] = A + (long long)(a_ok[c] ? m0 + row : 0) * lda + kbeg + 4 * piece;
+    }
+    const float *b_src[NBC];
+    int b_k[NBC];
+    bool b_ok[NBC];
 #pragma unroll
-            for (int q = 0; q < KL / 4; ++q) {
-                if constexpr (VEC) {
-                    ra[set][i][q] = *(const f32x4 *)((okk && gm < M && k0 + 4 * q < kend) ? src + 4 * q : zero);
-                } else {
+    for (int c = 0; c < NBC; ++c) {
+        const int row = RB * c + lane / (NT / 4);
+        const int col = 4 * (lane % (NT / 4));
+        b_ok[c] = n0 + col < N;
+        b_k[c] = kbeg + row;
+        b_src[c] = B + (long long)(kbeg + row) * ldb + (b_ok[c] ? n0 + col : 0);
+    }
+
+    // copy this wave's kk-th slab into stage st (past the wave's last slab the
+    // sources are the zero buffer, so every wave issues the same copies)
+    auto copy_slab = [&](int st, int kk) {
+        const int sl = wave + kk * KS;
+        const bool live = sl < nk;
+        const int dk = sl * KT;
+        const long long db = (long long)dk * ldb;
+        lds_char *dst = mine + st * STAGE;
 #pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        ra[set][i][q][e] = *((okk && gm < M && k0 + 4 * q + e < kend) ? src + 4 * q + e : zero);
-                }
-            }
+        for (int c = 0; c < NA; ++c) {
+            const bool ok = live && a_ok[c] && a_k[c] + dk < kend;
+            copy16_to_lds(ok ? a_src[c] + dk : zero, (unsigned)(uintptr_t)(dst + 1024 * c));
         }
 #pragma unroll
-        for (int j = 0; j < FN; ++j) {
-            const int gn = n0 + j * MF + li;
-            const float *src = B + (long long)k0 * ldb + gn;
-#pragma unroll
-            for (int e = 0; e < KL; ++e)
-                rb[set][j][e] = *((okk && gn < N && k0 + e < kend) ? src + (long long)e * ldb : zero);
+        for (int c = 0; c < NBC; ++c) {
+            const bool ok = live && b_ok[c] && b_k[c] + dk < kend;
+            copy16_to_lds(ok ? b_src[c] + db : zero, (unsigned)(uintptr_t)(dst + A_BYTES + B_CHUNK * c));
         }
     };
 
@@ -388,53 +422,67 @@ gemm_f32_direct_kernel(GemmParams p)
 #pragma unroll
             for (int r = 0; r < I::NR; ++r) acc[i][j][r] = 0.f;
 
-    auto compute = [&](int set) {
+    // one slab: every fragment read is issued before the first MFMA (the
+    // reads return in order, so MFMA t waits only for the reads it uses and
+    // the LDS latency is paid once per slab rather than once per step)
+    auto compute = [&](int st) {
+        lds_char *sa = mine + st * STAGE;
+        lds_char *sb = sa + A_BYTES;
+        f32x8 a[FM];
+        float b[8][FN];
 #pragma unroll
-        for (int e = 0; e < KL; ++e)
+        for (int i = 0; i < FM; ++i) {
+            const int row = 32 * i + li;
+            const int sw = (row >> 2) & 3;
+            const f32x4 lo = *(__attribute__((address_space(3))) f32x4 *)(sa + row * 64 + 16 * ((2 * lg) ^ sw));
+            const f32x4 hi = *(__attribute__((address_space(3))) f32x4 *)(sa + row * 64 + 16 * ((2 * lg + 1) ^ sw));
+            a[i] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        }
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            const int k = 8 * lg + t;
+            lds_char *brow = sb + (k / RB) * B_CHUNK + (k % RB) * B_ROW;
+#pragma unroll
+            for (int j = 0; j < FN; ++j) b[t][j] = *(__attribute__((address_space(3))) float *)(brow + 4 * (32 * j + li));
+        }
+#pragma unroll
+        for (int t = 0; t < 8; ++t)
 #pragma unroll
             for (int i = 0; i < FM; ++i)
 #pragma unroll
-                for (int j = 0; j < FN; ++j) acc[i][j] = I::mma(ra[set][i][e >> 2][e & 3], rb[set][j][e], acc[i][j]);
+                for (int j = 0; j < FN; ++j) acc[i][j] = I::mma(a[i][t], b[t][j], acc[i][j]);
+        __builtin_amdgcn_sched_group_barrier(0x100, FM * 2 + 8 * FN, 0);   // all LDS reads first
+        __builtin_amdgcn_sched_group_barrier(0x008, 8 * FM * FN, 0);       // then the MFMAs
     };
 
-    // register ring: slab it is loaded PF iterations ahead; loads are
-    // unconditional (past the end they read the zero buffer)
 #pragma unroll
-    for (int u = 0; u < PF; ++u) gload(u, u);
-    for (int it0 = 0; it0 < nmine; it0 += PF) {
+    for (int u = 0; u < ST - 1; ++u) copy_slab(u, u);
+    for (int it0 = 0; it0 < nmine; it0 += ST) {
 #pragma unroll
-        for (int u = 0; u < PF; ++u) {
+        for (int u = 0; u < ST; ++u) {
             const int it = it0 + u;
+            // slab it has landed once at most the ST - 2 later slabs' copies
+            // are pending; this wave's reads of the stage about to be
+            // refilled (multiplied in the previous iteration) are complete
+            wait_vmcnt<(ST - 2) * NCOPY>();
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            copy_slab((u + ST - 1) % ST, it + ST - 1);
             if (it < nmine) compute(u);
-            gload(u, it + PF);
         }
     }
+    wait_vmcnt<0>();   // no copy may still target LDS when the region is reused
+    __syncthreads();
 
-    if constexpr (KS > 1) {
-        // slices 1 .. KS-1 hand their accumulators to slice 0 through LDS
-        __shared__ float red[(KS > 1 ? KS - 1 : 1) * CB * NREG * 64];
-        if (ks > 0) {
-            float *r = red + ((ks - 1) * CB + cb) * NREG * 64;
+    // every wave's partial tile to LDS, then wave w adds register slots
+    // [w NREG / KS, (w + 1) NREG / KS) of all KS partials in wave order
+    float *red = (float *)smem;
 #pragma unroll
-            for (int i = 0; i < FM; ++i)
+    for (int i = 0; i < FM; ++i)
 #pragma unroll
-                for (int j = 0; j < FN; ++j)
+        for (int j = 0; j < FN; ++j)
 #pragma unroll
-                    for (int q = 0; q < I::NR; ++q) r[((i * FN + j) * I::NR + q) * 64 + lane] = acc[i][j][q];
-        }
-        __syncthreads();
-        if (ks > 0) return;
-#pragma unroll
-        for (int g = 1; g < KS; ++g) {
-            const float *r = red + ((g - 1) * CB + cb) * NREG * 64;
-#pragma unroll
-            for (int i = 0; i < FM; ++i)
-#pragma unroll
-                for (int j = 0; j < FN; ++j)
-#pragma unroll
-                    for (int q = 0; q < I::NR; ++q) acc[i][j][q] += r[((i * FN + j) * I::NR + q) * 64 + lane];
-        }
-    }
+            for (int r = 0; r < I::NR; ++r) red[((wave * NREG) + (i * FN + j) * I::NR + r) * 64 + lane] = acc[i][j][r];
+    __syncthreads();
 
     float *out = C;
     long long ldo = p.ldc;
@@ -442,33 +490,26 @@ gemm_f32_direct_kernel(GemmParams p)
         out = p.ws + ((long long)s * p.batch + z) * (long long)M * N;
         ldo = N;
     }
+    constexpr int SHARE = NREG / KS;
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+    for (int q = 0; q < SHARE; ++q) {
+        const int e = wave * SHARE + q;              // register slot (i, j, r)
+        float v = red[e * 64 + lane];
 #pragma unroll
-        for (int j = 0; j < FN; ++j)
-#pragma unroll
-            for (int r = 0; r < I::NR; ++r) {
-                const int row = m0 + i * MF + I::row_of(r, lg), col = n0 + j * MF + li;
-                if (row < M && col < N) out[(long long)row * ldo + col] = acc[i][j][r];
-            }
+        for (int w = 1; w < KS; ++w) v += red[(w * NREG + e) * 64 + lane];
+        const int i = e / (FN * I::NR), j = (e / I::NR) % FN, r = e % I::NR;
+        const int row = m0 + 32 * i + I::row_of(r, lg), col = n0 + 32 * j + li;
+        if (row < M && col < N) out[(long long)row * ldo + col] = v;
+    }
 }
 
-template <int WTM, int WTN, int KT, int CB, int MF, int PF, int KS, bool VEC>
-static hipError_t launch_gemm_f32_direct(const void *params, dim3 grid, hipStream_t stream)
+template <int MT, int NT, int KS, int ST>
+static hipError_t launch_gemm_f32w(const void *params, dim3 grid, hipStream_t stream)
 {
-    hipLaunchKernelGGL((gemm_f32_direct_kernel<WTM, WTN, KT, CB, MF, PF, KS, VEC>), grid, dim3(CB * KS * 64), 0, stream,
-                       *(const GemmParams *)params);
+    hipLaunchKernelGGL((gemm_f32w_kernel<MT, NT, KS, ST>), grid, dim3(KS * 64), 0, stream, *(const GemmParams *)params);
     return hipGetLastError();
 }
 
-// Register estimate of the Table 1 formula Reg_thread = x0*r0 + r0*y0 + x0*y0
-// for one lane: the accumulator tile (x0*y0 over 64 lanes), the A and B
-// fragments of one K step (r0*y0, r0*x0), the global->LDS staging registers,
-// and a fixed overhead for addresses and indices.
-constexpr int est_regs_f32(int mt, int nt, int kt, int wm, int wn, int mf, int pf) {
-    return (mt / wm) * (nt / wn) / 64 + 4 * ((mt / wm) / mf) + ((nt / wn) / mf) +
-           pf * ((mt * kt + kt * nt) / (wm * wn * 64)) + 28;
-}
 constexpr int lds_f32(int mt, int nt, int kt, int st, int ks) {
     return (ks * st * (mt * (kt == 16 ? kt : kt + 4) + kt * (nt + 4)) > (ks - 1) * mt * nt
                 ? ks * st * (mt * (kt == 16 ? kt : kt + 4) + kt * (nt + 4))
@@ -482,37 +523,42 @@ constexpr int lds_f32(int mt, int nt, int kt, int st, int ks) {
      (const void *)&gemm_f32_kernel<MT, NT, KT, WM, WN, MF, ST, PF, KS, VEC>,                                 \
      &launch_gemm_f32<MT, NT, KT, WM, WN, MF, ST, PF, KS, VEC>}
 
-// Direct variants: macro tile = WTM x (CB * WTN); waves = CB x KS; no LDS
-// staging (only the final K-slice reduction); registers = accumulators +
-// PF x (A + B fragments of one slab) + overhead.
-constexpr int est_regs_f32d(int wtm, int wtn, int kt, int mf, int pf) {
-    return wtm * wtn / 64 + pf * ((wtm / mf) * (kt / (64 / mf)) + (wtn / mf) * (kt / (64 / mf))) + 24;
+// Register estimate of the Table 1 formula Reg_thread = x0*r0 + r0*y0 + x0*y0
+// for one lane: the accumulator tile (x0*y0 over 64 lanes), the A and B
+// fragments of one K step (r0*y0, r0*x0), the global->LDS staging registers,
+// and a fixed overhead for addresses and indices.
+constexpr int est_regs_f32(int mt, int nt, int kt, int wm, int wn, int mf, int pf) {
+    return (mt / wm) * (nt / wn) / 64 + 4 * ((mt / wm) / mf) + ((nt / wn) / mf) +
+           pf * ((mt * kt + kt * nt) / (wm * wn * 64)) + 28;
 }
-#define NNJIT_F32D_VARIANT(WTM, WTN, KT, CB, MF, PF, KS, VEC)                                                  \
-    {"gemm_f32d_" #WTM "x" #WTN "x" #KT "_c" #CB "_m" #MF "_p" #PF "_k" #KS "_v" #VEC, FAM_GEMM_F32, MF,          \
-     (MF == 32 ? 2 : 4), WTM, CB * WTN, KT, 1, CB, 0, PF, KS, (VEC ? 16 : 4), 0, 0, CB * KS * 64,                \
-     (KS > 1 ? (KS - 1) * CB * WTM * WTN * 4 : 4), est_regs_f32d(WTM, WTN, KT, MF, PF),                         \
-     (const void *)&gemm_f32_direct_kernel<WTM, WTN, KT, CB, MF, PF, KS, VEC>,                                   \
-     &launch_gemm_f32_direct<WTM, WTN, KT, CB, MF, PF, KS, VEC>}
 
-#define NNJIT_F32D_LIST(X) \
-    X(32, 32, 16, 4, 16, 4, 4, true) \
-    X(32, 32, 16, 4, 16, 2, 4, true) \
-    X(32, 32, 16, 2, 16, 4, 4, true) \
-    X(32, 32, 16, 2, 32, 4, 4, true) \
-    X(32, 32, 16, 4, 32, 4, 4, true) \
-    X(16, 16, 16, 4, 16, 4, 4, true) \
-    X(16, 16, 16, 4, 16, 8, 4, true) \
-    X(32, 16, 16, 4, 16, 4, 4, true) \
-    X(16, 32, 16, 4, 16, 4, 4, true) \
-    X(32, 64, 16, 2, 32, 4, 4, true) \
-    X(64, 32, 16, 2, 32, 4, 4, true) \
-    X(32, 32, 32, 4, 16, 2, 4, true) \
-    X(32, 32, 32, 2, 32, 2, 4, true)
+// Wave-private variants: accumulators, one slab of A fragments (8 k) and B
+// values, three registers of copy state per copy, and a fixed overhead.
+constexpr int est_regs_f32w(int mt, int nt) {
+    return (mt / 32) * (nt / 32) * 16 + (mt / 32) * 8 + (nt / 32) + 3 * (mt / 16 + 16 * nt / 256) + 24;
+}
+constexpr int lds_f32w(int mt, int nt, int ks, int st) {
+    return ks * st * (mt * 64 + (16 / (256 / nt)) * (1024 + 16 * (256 / nt))) > ks * (mt / 32) * (nt / 32) * 16 * 256
+               ? ks * st * (mt * 64 + (16 / (256 / nt)) * (1024 + 16 * (256 / nt)))
+               : ks * (mt / 32) * (nt / 32) * 16 * 256;
+}
+#define NNJIT_F32W_VARIANT(MT, NT, KS, ST)                                                                   \
+    {"gemm_f32w_" #MT "x" #NT "x16_k" #KS "_s" #ST, FAM_GEMM_F32, 32, 2, MT, NT, 16, 1, 1, ST, ST - 1, KS, 16,  \
+     0, 0, KS * 64, lds_f32w(MT, NT, KS, ST), est_regs_f32w(MT, NT), (const void *)&gemm_f32w_kernel<MT, NT, KS, ST>, \
+     &launch_gemm_f32w<MT, NT, KS, ST>, 1}
 
-#define NNJIT_F32D_INST(WTM, WTN, KT, CB, MF, PF, KS, VEC) \
-    template __global__ void gemm_f32_direct_kernel<WTM, WTN, KT, CB, MF, PF, KS, VEC>(GemmParams);
-NNJIT_F32D_LIST(NNJIT_F32D_INST)
+#define NNJIT_F32W_LIST(X) \
+    X(64, 32, 4, 4) \
+    X(64, 32, 8, 3) \
+    X(32, 32, 4, 4) \
+    X(32, 32, 8, 4) \
+    X(32, 64, 4, 4) \
+    X(64, 64, 4, 3) \
+    X(128, 32, 4, 3) \
+    X(32, 128, 4, 3)
+
+#define NNJIT_F32W_INST(MT, NT, KS, ST) template __global__ void gemm_f32w_kernel<MT, NT, KS, ST>(GemmParams);
+NNJIT_F32W_LIST(NNJIT_F32W_INST)
 
 // The compiled fp32 configurations (the family's full set; the lite space of
 // a shape is a pruned, ordered subset).  Tile edges are powers of two
@@ -602,8 +648,8 @@ NNJIT_F32_LIST(NNJIT_F32_INST)
 
 #if !defined(__HIP_DEVICE_COMPILE__)
 #define NNJIT_F32_ENTRY(...) NNJIT_F32_VARIANT(__VA_ARGS__),
-#define NNJIT_F32D_ENTRY(...) NNJIT_F32D_VARIANT(__VA_ARGS__),
-const Variant kGemmF32Variants[] = {NNJIT_F32_LIST(NNJIT_F32_ENTRY) NNJIT_F32D_LIST(NNJIT_F32D_ENTRY)};
+#define NNJIT_F32W_ENTRY(...) NNJIT_F32W_VARIANT(__VA_ARGS__),
+const Variant kGemmF32Variants[] = {NNJIT_F32_LIST(NNJIT_F32_ENTRY) NNJIT_F32W_LIST(NNJIT_F32W_ENTRY)};
 const int kNumGemmF32Variants = sizeof(kGemmF32Variants) / sizeof(kGemmF32Variants[0]);
 #endif
 

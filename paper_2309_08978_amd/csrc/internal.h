@@ -50,8 +50,8 @@ struct Variant {
     int mfma_m, mfma_k;   // matrix-core instruction shape (0 for GEMV)
     int mt, nt, kt;       // macro tile (GEMV: mt = 1, nt = columns per WG, kt = rows per pass)
     int wm, wn;           // wave grid of the workgroup (GEMV: wm = waves, wn = 1)
-    int stages;           // LDS buffers for the K loop (1 or 2; GEMV 0)
-    int prefetch;         // K slabs in flight in registers (GEMM; GEMV 0)
+    int stages;           // LDS buffers for the K loop (GEMV 0)
+    int prefetch;         // K slabs in flight (in registers, or in LDS for direct-copy variants; GEMV 0)
     int kslices;          // K groups of waves inside a workgroup (GEMM; GEMV 1)
     int vec_bytes;        // bytes per global load of one lane (16, or the element size)
     int lanes_seg;        // GEMV: lanes across one row segment
@@ -61,6 +61,7 @@ struct Variant {
     int est_regs;         // VGPR+AGPR estimate per lane (the Table 1 register formula)
     const void *kernel;   // device function (attribute queries)
     LaunchFn launch;
+    int direct_copy;      // 1: slabs go global -> LDS by direct copies (staging in LDS, not registers)
 };
 
 // Variant tables, one per family (defined in the kernel sources).

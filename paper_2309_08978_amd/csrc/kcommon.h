@@ -23,4 +23,36 @@ __device__ __forceinline__ int xcd_remap(int flat, int G) {
     return (xcd < r) ? xcd * (q + 1) + local : r * (q + 1) + (xcd - r) * q + local;
 }
 
+// Wait until at most N vector memory operations of this wave are pending.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt()
+{
+    static_assert(N >= 0 && N <= 63, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// 16 bytes per lane from global memory to LDS: lane l's bytes land at LDS
+// address lds + 16 l (lds must be wave-uniform).  Issued as inline assembly
+// so that the compiler does not treat the copy as an LDS store of unknown
+// target and wait for every copy in flight before each LDS read; the kernel
+// orders the copies against the reads itself (counted vmcnt waits plus a
+// barrier).  Vector memory loads complete in issue order, so the compiler's
+// own vmcnt waits stay correct with these extra loads in the queue.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"   // m0 is written on purpose
+__device__ __forceinline__ void copy16_to_lds(const void *src, unsigned lds)
+{
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// Workgroup barrier for the copy pipeline: this wave's LDS reads are complete
+// and every wave has arrived.  Global memory ordering is not needed here (the
+// copies are waited for by count), so unlike __syncthreads() it does not
+// wait for all outstanding vector memory operations.
+__device__ __forceinline__ void lds_barrier()
+{
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 }  // namespace nnjit

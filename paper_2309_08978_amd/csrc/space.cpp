@@ -235,24 +235,37 @@ LiteResult lite_space(const Shape &s, const nnjit_device_limits &d, const std::v
     if (cands.empty()) cands = unfit;
 
     // heuristic 7: keep register-bound candidates (Block_core == RegLimit),
-    // relaxed when too few survive
+    // relaxed when too few survive.  A direct-copy variant keeps its staging
+    // (the slabs in flight, a register term of Table 1 for the others) in
+    // LDS, so for it the bound that plays this role is L1Limit.
     std::vector<Cand> kept;
-    for (const Cand &c : cands)
-        if (c.r.wg_per_cu == c.r.reg_limit) kept.push_back(c);
+    for (const Cand &c : cands) {
+        const bool direct = configs()[c.id].v->direct_copy != 0;
+        if (c.r.wg_per_cu == (direct ? c.r.lds_limit : c.r.reg_limit)) kept.push_back(c);
+    }
     if ((int)kept.size() < kMinSurvivors) kept = cands;
 
     // evaluation order: most workgroups per CU first, then fuller last wave,
-    // larger tile, smaller split, lower id
-    std::stable_sort(kept.begin(), kept.end(), [](const Cand &a, const Cand &b) {
+    // larger tile, smaller split, lower id -- within each staging kind
+    // (registers / LDS direct copies), the two orders merged in turn so that
+    // the cap below never drops one kind wholesale
+    auto before = [](const Cand &a, const Cand &b) {
         if (a.r.wg_per_cu != b.r.wg_per_cu) return a.r.wg_per_cu > b.r.wg_per_cu;
         if (std::fabs(a.eff - b.eff) > 1e-9) return a.eff > b.eff;
         if (a.area != b.area) return a.area > b.area;
         if (a.split != b.split) return a.split < b.split;
         return a.id < b.id;
-    });
+    };
+    std::vector<Cand> by_kind[2];
+    for (const Cand &c : kept) by_kind[configs()[c.id].v->direct_copy != 0 ? 1 : 0].push_back(c);
+    for (auto &v : by_kind) std::stable_sort(v.begin(), v.end(), before);
+    std::vector<Cand> order;
+    for (size_t i = 0; i < std::max(by_kind[0].size(), by_kind[1].size()); ++i)
+        for (auto &v : by_kind)
+            if (i < v.size()) order.push_back(v[i]);
     // the lite space is the head of that order: at most kMaxTimed candidates
     // are ever evaluated on the device
-    for (const Cand &c : kept) {
+    for (const Cand &c : order) {
         if ((int)out.ids.size() >= kMaxTimed) break;
         out.ids.push_back(c.id);
     }

@@ -121,16 +121,17 @@ def test_lite_space_is_dozens_and_ordered(lib, name, index):
     assert n_naive > (10 * n if op.kind != "gemv" else 2 * n)
     cfgs = nj.configs()
     fam = ("gemv_" if op.kind == "gemv" else "gemm_") + op.dtype
-    prev = None
+    prev = {}
     for i in ids:
         c = cfgs[i]
         assert c["family"] == fam
         r = nj.nnjit_config_resources(i, d)
         assert c["threads"] <= d.max_threads_per_wg       # heuristic 5
         assert r["lds_per_wg"] <= d.lds_per_wg           # heuristic 6
-        if prev is not None:
-            assert r["wg_per_cu"] <= prev                # evaluated from max to min Block_core
-        prev = r["wg_per_cu"]
+        kind = c.get("direct", 0)                        # staging in registers / LDS direct copies
+        if kind in prev:
+            assert r["wg_per_cu"] <= prev[kind]          # evaluated from max to min Block_core, per kind
+        prev[kind] = r["wg_per_cu"]
         if op.kind != "gemv":
             assert c["Mt"] <= max(16, 1 << (op.M - 1).bit_length())
     # deterministic
@@ -140,9 +141,14 @@ def test_lite_space_is_dozens_and_ordered(lib, name, index):
 def test_heuristic7_prefers_register_bound(lib):
     d = nj.mi355x_limits()
     ids, n, _, _ = nj.nnjit_lite_space(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, 1024, 1024, 1024, d)
+    cfgs = nj.configs()
     rs = [nj.nnjit_config_resources(i, d) for i in ids]
-    bound = [r["wg_per_cu"] == r["reg_limit"] for r in rs]
+    # register-staged configurations are register bound; direct-copy ones,
+    # whose staging lives in LDS, are LDS bound
+    bound = [r["wg_per_cu"] == (r["lds_limit"] if cfgs[i]["direct"] else r["reg_limit"]) for i, r in zip(ids, rs)]
     assert all(bound) or n >= 8
+    # both staging kinds are evaluated when both survive
+    assert any(cfgs[i]["direct"] for i in ids) and any(not cfgs[i]["direct"] for i in ids)
 
 
 def test_more_lds_never_shrinks_limits(lib):
