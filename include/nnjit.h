@@ -96,7 +96,9 @@ int nnjit_batched_matmul(int64_t batch, int64_t M, int64_t N, int64_t K,
  * launches whose per-launch median is the candidate's cost; the burst length
  * (8, 2 or 1) is set once per shape from the first candidate's single launch;
  * a candidate whose single launch is more than 1.5x the fastest single launch
- * so far is dropped; at most 96 candidates and about 900 ms of evaluation), keeps the fastest in the per-shape cache and
+ * so far is dropped; at most 96 candidates and about 900 ms of evaluation;
+ * an M = 1 (GEMV) shape is timed on weights streamed from HBM: the weight
+ * operand rotates over scratch copies of >= 512 MiB together), keeps the fastest in the per-shape cache and
  * returns its configuration id (>= 0).  Synchronous; uses its own stream and
  * a library-owned scratch buffer.  Re-tuning a cached shape replaces the
  * incumbent only if the new winner is at least 3% faster.  Wall time and

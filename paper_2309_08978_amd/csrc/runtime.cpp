@@ -146,7 +146,8 @@ int workspace_for(Device &d, hipStream_t stream, int64_t ws_floats, Workspace **
         if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
         const int64_t nf = std::max(w.ws_floats, ws_floats + ws_floats / 4);
         if (w.ws) (void)hipFree(w.ws);
-        w = Workspace{};
+        w.ws = nullptr;
+        w.ws_floats = 0;
         e = hipMalloc((void **)&w.ws, (size_t)std::max<int64_t>(nf, 1) * sizeof(float));
         if (e != hipSuccess) {
             (void)hipGetLastError();
@@ -390,11 +391,18 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
     t_stats.n_lite = (int)lr.ids.size();
     if (lr.ids.empty()) return fail(NNJIT_ENOCFG, "no configuration fits this shape");
 
-    // scratch operands of this exact shape, filled on the device
+    // scratch operands of this exact shape, filled on the device.  A GEMV is
+    // bandwidth bound and runs on weights streamed from HBM, so it is timed
+    // that way: its weight operand rotates over enough copies (>= 512 MiB
+    // together) that the 256 MB last-level cache cannot hold them.
     const size_t a_bytes = (size_t)(batch * M * K) * elt, b_bytes = (size_t)(batch * K * N) * elt;
     const size_t c_bytes = (size_t)(batch * M * N) * 4;
     auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
-    const size_t need = up(a_bytes) + up(b_bytes) + up(c_bytes);
+    const size_t kColdBytes = (size_t)512 << 20;
+    const int b_copies = kind == NNJIT_KIND_GEMV
+                             ? (int)std::min<size_t>(16, std::max<size_t>(1, (kColdBytes + up(b_bytes) - 1) / up(b_bytes)))
+                             : 1;
+    const size_t need = up(a_bytes) + (size_t)b_copies * up(b_bytes) + up(c_bytes);
     hipError_t e;
     if (d->scratch_bytes < need) {
         if (d->scratch) (void)hipFree(d->scratch);
@@ -408,13 +416,21 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
         d->scratch_bytes = need;
     }
     char *base = (char *)d->scratch;
+    char *b0 = base + up(a_bytes);
     c.A = base;
-    c.B = base + up(a_bytes);
-    c.C = base + up(a_bytes) + up(b_bytes);
+    c.B = b0;
+    c.C = b0 + (size_t)b_copies * up(b_bytes);
     c.stream = d->tune_stream;
-    if ((e = launch_fill_uniform((void *)c.A, batch * M * K, dtype, 1234u, c.stream)) != hipSuccess ||
-        (e = launch_fill_uniform((void *)c.B, batch * K * N, dtype, 5678u, c.stream)) != hipSuccess)
+    if ((e = launch_fill_uniform((void *)c.A, batch * M * K, dtype, 1234u, c.stream)) != hipSuccess)
         return hip_fail(e, "scratch fill");
+    for (int i = 0; i < b_copies; ++i)
+        if ((e = launch_fill_uniform(b0 + (size_t)i * up(b_bytes), batch * K * N, dtype, 5678u + i, c.stream)) != hipSuccess)
+            return hip_fail(e, "scratch fill");
+    int rot = 0;
+    auto launch_next = [&](const Config &cfg) {   // next weight copy, then launch
+        c.B = b0 + (size_t)(rot++ % b_copies) * up(b_bytes);
+        return launch(*d, cfg, c);
+    };
 
     const int reps = std::max(1, env_int("NNJIT_TUNE_REPS", 3));
     const double budget_ms = (double)env_int("NNJIT_TUNE_BUDGET_MS", 900);
@@ -442,10 +458,10 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
         const Config &cfg = configs()[lr.ids[i]];
         // warm-up launch (untimed: the first launch of a kernel pays one-time
         // costs), then one single timed launch that decides the early abort
-        rc = launch(*d, cfg, c);
+        rc = launch_next(cfg);
         if (rc == NNJIT_OK) {
             (void)hipEventRecord(ev[0], c.stream);
-            rc = launch(*d, cfg, c);
+            rc = launch_next(cfg);
             (void)hipEventRecord(ev[1], c.stream);
         }
         if (rc != NNJIT_OK) {
@@ -471,7 +487,7 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
         bool ok = true;
         for (int r = 0; r < reps && ok; ++r) {
             (void)hipEventRecord(ev[2 + 2 * r], c.stream);
-            for (int b = 0; b < burst && ok; ++b) ok = launch(*d, cfg, c) == NNJIT_OK;
+            for (int b = 0; b < burst && ok; ++b) ok = launch_next(cfg) == NNJIT_OK;
             (void)hipEventRecord(ev[3 + 2 * r], c.stream);
         }
         if (!ok) {
