@@ -272,9 +272,10 @@ static hipError_t launch_gemm_f16(const void *params, dim3 grid, hipStream_t str
 // layouts are therefore chosen by which global 16-byte chunk each lane
 // fetches.
 //
-// A slab: [Mt rows][128 bytes], chunk c of row r stored at slot
-//   c ^ ((r >> 1) & 7) (the conflict-free layout of the kernel above).
-// B slab: row-major [64 k rows][Nt halves], the 32-byte unit u of row k
+// A slab: [Mt rows][Kt halves], chunk c of row r stored at slot c ^ ((r >> 1)
+//   & 7) for 128-byte rows (the conflict-free layout of the kernel above),
+//   c ^ ((r >> 2) & 3) for 64-byte rows.
+// B slab: row-major [Kt k rows][Nt halves], the 32-byte unit u of row k
 //   stored at unit u ^ sB(k), sB(k) = ((k & 3) << 1) | ((k >> 3) & 1).
 //
 // B is read with ds_read_b64_tr_b16.  Measured on gfx950: within each group
@@ -305,19 +306,21 @@ __device__ __forceinline__ void interleave_mfma_ds()
     }
 }
 
-template <int MT, int NT, int WM, int WN, int MF, int ST>
+template <int MT, int NT, int KT, int WM, int WN, int MF, int ST>
 __global__ void __launch_bounds__(WM * WN * 64)
 gemm_f16t_kernel(GemmParams p)
 {
     typedef Mfma16<MF> I;
     typedef typename I::acc_t acc_t;
-    constexpr int KT = 64;
+    static_assert(KT == 32 || KT == 64, "K slab of 32 or 64 halves");
+    constexpr int A_ROW = KT * 2;               // bytes of one A row of the slab
+    constexpr int ACH = KT / 8;                 // 16-byte chunks per A row
     constexpr int NW = WM * WN;
     constexpr int WTM = MT / WM, WTN = NT / WN;
     constexpr int FM = WTM / MF, FN = WTN / MF;
     constexpr int KG = 64 / MF;                 // lane groups along k
     constexpr int NSTEP = KT / (8 * KG);        // instructions per slab and fragment pair
-    constexpr int A_BYTES = MT * 128;
+    constexpr int A_BYTES = MT * A_ROW;
     constexpr int B_ROW = NT * 2;
     constexpr int B_BYTES = KT * B_ROW;
     constexpr int STAGE = A_BYTES + B_BYTES;
@@ -327,11 +330,12 @@ gemm_f16t_kernel(GemmParams p)
     static_assert(FM >= 1 && FN >= 1 && WTM % MF == 0 && WTN % MF == 0, "wave tile");
     static_assert((ST - 2) * (LA + LB) <= 63, "copies in flight exceed the vmcnt range");
 
-    // one LDS object per stage, so that the compiler can tell which stage a
-    // fragment read depends on
-    __shared__ __attribute__((aligned(1024))) char smem0[STAGE];
-    __shared__ __attribute__((aligned(1024))) char smem1[STAGE];
-    __shared__ __attribute__((aligned(1024))) char smem2[ST > 2 ? STAGE : 1024];
+    // A slab swizzle: the 16-byte chunk c of row r sits at c ^ a_swz(r), so
+    // that 16 consecutive rows read at one chunk hit distinct bank groups
+    // (128-byte rows: (r >> 1) & 7; 64-byte rows: (r >> 2) & 3)
+    auto a_swz = [](int row) { return KT == 64 ? ((row >> 1) & 7) : ((row >> 2) & 3); };
+
+    __shared__ __attribute__((aligned(1024))) char smem[ST * STAGE];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -357,9 +361,7 @@ gemm_f16t_kernel(GemmParams p)
     const long long lda = p.lda, ldb = p.ldb;
     const unsigned short *zero = (const unsigned short *)p.zero;
     typedef __attribute__((address_space(3))) char lds_char;
-    auto stage_base = [&](int u) -> lds_char * {
-        return (lds_char *)(u == 0 ? smem0 : u == 1 ? smem1 : smem2);
-    };
+    auto stage_base = [&](int u) -> lds_char * { return (lds_char *)smem + u * STAGE; };
     const int wave_u = __builtin_amdgcn_readfirstlane(wave);
 
     // per-lane sources of this wave's copies for the split's first slab;
@@ -369,8 +371,8 @@ gemm_f16t_kernel(GemmParams p)
     bool a_ok[LA];
 #pragma unroll
     for (int j = 0; j < LA; ++j) {
-        const int row = 8 * (wave + j * NW) + (lane >> 3);
-        const int col = 8 * ((lane & 7) ^ ((row >> 1) & 7));
+        const int row = (1024 / A_ROW) * (wave + j * NW) + lane / ACH;
+        const int col = 8 * ((lane % ACH) ^ a_swz(row));
         a_ok[j] = m0 + row < M;
         a_k[j] = kbeg + col;
         a_src[j] = A + (long long)(a_ok[j] ? m0 + row : 0) * lda + kbeg + col;
@@ -427,7 +429,7 @@ gemm_f16t_kernel(GemmParams p)
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
             const int row = wm * WTM + i * MF + li;
-            a[i] = __builtin_bit_cast(f16x8, *(lds_u32x4 *)(sa + row * 128 + 16 * (chunk ^ ((row >> 1) & 7))));
+            a[i] = __builtin_bit_cast(f16x8, *(lds_u32x4 *)(sa + row * A_ROW + 16 * (chunk ^ a_swz(row))));
         }
         const int kc = st * KG + tr_g;                       // 8-row k chunk of this lane group
 #pragma unroll
@@ -501,10 +503,10 @@ gemm_f16t_kernel(GemmParams p)
             }
 }
 
-template <int MT, int NT, int WM, int WN, int MF, int ST>
+template <int MT, int NT, int KT, int WM, int WN, int MF, int ST>
 static hipError_t launch_gemm_f16t(const void *params, dim3 grid, hipStream_t stream)
 {
-    hipLaunchKernelGGL((gemm_f16t_kernel<MT, NT, WM, WN, MF, ST>), grid, dim3(WM * WN * 64), 0, stream,
+    hipLaunchKernelGGL((gemm_f16t_kernel<MT, NT, KT, WM, WN, MF, ST>), grid, dim3(WM * WN * 64), 0, stream,
                        *(const GemmParams *)params);
     return hipGetLastError();
 }
@@ -561,40 +563,46 @@ constexpr int lds_f16(int mt, int nt, int st) { return st * (mt + nt) * 128; }
 
 // Direct-copy family: accumulators, one K step of fragments, the per-lane
 // copy geometry (2 registers per copy) and a fixed overhead; no staging.
-constexpr int est_regs_f16t(int mt, int nt, int wm, int wn, int mf) {
+constexpr int est_regs_f16t(int mt, int nt, int kt, int wm, int wn, int mf) {
     return (mt / wm) * (nt / wn) / 64 + 4 * ((mt / wm) / mf) + 4 * ((nt / wn) / mf) +
-           2 * (mt * 128 / 1024 / (wm * wn) + nt * 128 / 1024 / (wm * wn)) + 32;
+           2 * ((mt + nt) * kt * 2 / 1024 / (wm * wn)) + 32;
 }
+constexpr int lds_f16t(int mt, int nt, int kt, int st) { return st * (mt + nt) * kt * 2; }
 
-#define NNJIT_F16T_VARIANT(MT, NT, WM, WN, MF, ST)                                                          \
-    {"gemm_f16t_" #MT "x" #NT "x64_w" #WM "x" #WN "_m" #MF "_s" #ST, FAM_GEMM_F16, MF, (MF == 32 ? 16 : 32),     \
-     MT, NT, 64, WM, WN, ST, ST - 1, 1, 16, 0, 0, WM * WN * 64, lds_f16(MT, NT, ST),                          \
-     est_regs_f16t(MT, NT, WM, WN, MF), (const void *)&gemm_f16t_kernel<MT, NT, WM, WN, MF, ST>,              \
-     &launch_gemm_f16t<MT, NT, WM, WN, MF, ST>, 1}
+#define NNJIT_F16T_VARIANT(MT, NT, KT, WM, WN, MF, ST)                                                      \
+    {"gemm_f16t_" #MT "x" #NT "x" #KT "_w" #WM "x" #WN "_m" #MF "_s" #ST, FAM_GEMM_F16, MF, (MF == 32 ? 16 : 32), \
+     MT, NT, KT, WM, WN, ST, ST - 1, 1, 16, 0, 0, WM * WN * 64, lds_f16t(MT, NT, KT, ST),                     \
+     est_regs_f16t(MT, NT, KT, WM, WN, MF), (const void *)&gemm_f16t_kernel<MT, NT, KT, WM, WN, MF, ST>,      \
+     &launch_gemm_f16t<MT, NT, KT, WM, WN, MF, ST>, 1}
 
 // The compiled direct-copy configurations (16-byte aligned operands, Nt >= 128).
 #define NNJIT_F16T_LIST(X) \
-    X(256, 256, 4, 2, 32, 2) \
-    X(256, 256, 2, 4, 32, 2) \
-    X(256, 128, 2, 2, 32, 2) \
-    X(256, 128, 2, 2, 32, 3) \
-    X(256, 128, 4, 2, 32, 2) \
-    X(256, 128, 4, 2, 32, 3) \
-    X(128, 256, 2, 2, 32, 2) \
-    X(128, 256, 2, 2, 32, 3) \
-    X(128, 256, 2, 4, 32, 2) \
-    X(128, 256, 2, 4, 32, 3) \
-    X(128, 128, 2, 2, 32, 2) \
-    X(128, 128, 2, 2, 32, 3) \
-    X(128, 128, 2, 2, 16, 2) \
-    X(128, 128, 2, 2, 16, 3) \
-    X(128, 128, 4, 2, 32, 3) \
-    X(64, 128, 2, 2, 32, 2) \
-    X(64, 128, 2, 2, 32, 3) \
-    X(64, 128, 1, 2, 32, 3)
+    X(256, 256, 64, 4, 2, 32, 2) \
+    X(256, 256, 64, 2, 4, 32, 2) \
+    X(256, 256, 32, 2, 4, 32, 4) \
+    X(256, 256, 32, 2, 4, 32, 5) \
+    X(256, 256, 32, 4, 2, 32, 4) \
+    X(256, 128, 64, 2, 2, 32, 2) \
+    X(256, 128, 64, 2, 2, 32, 3) \
+    X(256, 128, 64, 4, 2, 32, 2) \
+    X(256, 128, 64, 4, 2, 32, 3) \
+    X(256, 128, 32, 4, 2, 32, 5) \
+    X(128, 256, 64, 2, 2, 32, 2) \
+    X(128, 256, 64, 2, 2, 32, 3) \
+    X(128, 256, 64, 2, 4, 32, 2) \
+    X(128, 256, 64, 2, 4, 32, 3) \
+    X(128, 256, 32, 2, 4, 32, 5) \
+    X(128, 128, 64, 2, 2, 32, 2) \
+    X(128, 128, 64, 2, 2, 32, 3) \
+    X(128, 128, 64, 2, 2, 16, 2) \
+    X(128, 128, 64, 2, 2, 16, 3) \
+    X(128, 128, 64, 4, 2, 32, 3) \
+    X(64, 128, 64, 2, 2, 32, 2) \
+    X(64, 128, 64, 2, 2, 32, 3) \
+    X(64, 128, 64, 1, 2, 32, 3)
 
-#define NNJIT_F16T_INST(MT, NT, WM, WN, MF, ST) \
-    template __global__ void gemm_f16t_kernel<MT, NT, WM, WN, MF, ST>(GemmParams);
+#define NNJIT_F16T_INST(MT, NT, KT, WM, WN, MF, ST) \
+    template __global__ void gemm_f16t_kernel<MT, NT, KT, WM, WN, MF, ST>(GemmParams);
 NNJIT_F16T_LIST(NNJIT_F16T_INST)
 
 #define NNJIT_F16_INST(MT, NT, WM, WN, MF, ST, PF, VEC) \
