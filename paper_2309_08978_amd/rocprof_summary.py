@@ -109,10 +109,16 @@ def traffic(fetch_dir, write_dir, meta):
     out = {}
     for key, d, counter in (("fetch", fetch_dir, "FETCH_SIZE"), ("write", write_dir, "WRITE_SIZE")):
         rows = _pmc_dispatches(d, counter)
-        copies = [i for i, r in enumerate(rows) if "copyBuffer" in r[0] or "copy_kernel" in r[0]]
+        is_copy = lambda r: "copyBuffer" in r[0] or "copy_kernel" in r[0]
+        copies = [i for i, r in enumerate(rows) if is_copy(r)]
         if not copies:
             raise SystemExit(f"{d}: no reference copy dispatch found")
-        ref = statistics.mean(rows[i][2] for i in copies)
+        # the reference is the run of same-grid copies right before the
+        # product's launches (other copies, e.g. operand clones, may precede)
+        ref_ids = [copies[-1]]
+        while ref_ids[0] > 0 and is_copy(rows[ref_ids[0] - 1]) and rows[ref_ids[0] - 1][1] == rows[copies[-1]][1]:
+            ref_ids.insert(0, ref_ids[0] - 1)
+        ref = statistics.mean(rows[i][2] for i in ref_ids)
         factor = ref_bytes / (ref * 1024.0)
         after = [r for r in rows[copies[-1] + 1:] if "nnjit" in r[0]]
         kib = sum(r[2] for r in after) / meta["reps"]
