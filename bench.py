@@ -109,6 +109,34 @@ def measured_traffic(db_path, workload, op, config_info):
     return e["hbm_bytes_per_launch"]
 
 
+def online_curve(runs, nsteps):
+    """Per-step time of eager steps from an empty cache with online tuning on:
+    each step's calls measure one candidate per untuned shape, so the step
+    time falls as registered configurations improve, until every shape is
+    tuned (reproduces the paper's speed-up-over-time measurement)."""
+    import torch
+    nj.nnjit_cache_clear()
+    prev = nj.nnjit_set_online(True)
+    ms, tuned_at = [], None
+    try:
+        for k in range(nsteps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for r in runs:
+                r.call(k)
+            b.record()
+            torch.cuda.synchronize()
+            ms.append(round(a.elapsed_time(b), 5))
+            if tuned_at is None:
+                states = [nj.nnjit_online_status(_kind(r.op), _dt(r.op), r.op.batch, r.op.M, r.op.N, r.op.K)["state"]
+                          for r in runs]
+                if all(st == "tuned" for st in states):
+                    tuned_at = k + 1
+    finally:
+        nj.nnjit_set_online(prev)
+    return {"step_ms": ms, "steps_until_all_tuned": tuned_at, "first_ms": ms[0], "last_ms": ms[-1]}
+
+
 def cpu_baseline(name, budget_s: float):
     """The oracle (CPU, fp64) on the same workload: whole steps, repeated
     until about `budget_s` seconds of CPU work have run (at least one step)."""
@@ -154,6 +182,9 @@ def main(argv=None):
     ap.add_argument("--profile-op", default=None,
                     help="counter-collection mode: tune, run the reference copy, then launch only this product "
                          "--kernel-reps times and print one metadata line")
+    ap.add_argument("--online-steps", type=int, default=0,
+                    help="after the measurement, clear the tuned cache and run this many eager steps with online "
+                         "just-in-time tuning, reporting each step's time (the gradual speed-up curve)")
     ap.add_argument("--traffic-db", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="measured HBM traffic per launch (written from rocprofv3 counter runs)")
     args = ap.parse_args(argv)
@@ -384,6 +415,8 @@ def main(argv=None):
         "roofline": rl,
         "device": torch.cuda.get_device_name(0),
     }
+    if args.online_steps > 0:
+        out["online"] = online_curve(runs, args.online_steps)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(name, args.cpu_budget)
     print(json.dumps(out), flush=True)

@@ -201,6 +201,38 @@ int nnjit_last_tune_trace(int *ids, double *us, double *at_ms, int cap);
 /* Configuration id cached for a shape on the current device, or NNJIT_ENOCFG. */
 int nnjit_cached_config(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K);
 
+/* The ranked candidates kept for a tuned shape (Sec. 5.3: the best kernels of
+ * a device are shared with identical devices): up to 5 configuration ids and
+ * their measured per-launch times in us, the registered configuration first,
+ * then the fastest other candidates.  Writes min(count, cap) entries to ids
+ * and us (either may be NULL); returns the count, or NNJIT_ENOCFG if the
+ * shape is not tuned on the current device. */
+int nnjit_cached_ranked(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K, int *ids, double *us,
+                        int cap);
+
+/* Online just-in-time tuning (Sec. 3: while the application runs, candidates
+ * are measured between inferences and a significantly faster one is
+ * re-registered).  With enable = 1, an untuned shape is not served by its
+ * default configuration alone: each nnjit_matmul / nnjit_batched_matmul call
+ * on it runs the next candidate of its lite space -- every configuration
+ * computes the same product, so the call's result is the caller's result --
+ * timed by HIP events on the caller's stream and read back by a later call
+ * (never waited for).  A candidate at least 3% faster than the registered one
+ * replaces it; once every candidate has been measured the shape is cached as
+ * if nnjit_tune had run.  Calls during stream capture, calls whose operands
+ * need the element-load path and calls made while a measurement is still in
+ * flight are served by the registered configuration without measuring.  With
+ * enable = 0 no new measurement starts (shapes in progress keep their
+ * registered configuration).  Off by default.  Returns the previous setting. */
+int nnjit_set_online(int enable);
+
+/* Online progress of a shape on the current device: 0 while it is being tuned
+ * online (*measured candidates of *total so far, *registered = the
+ * configuration serving calls), 1 once it is tuned (*registered = its cached
+ * configuration), NNJIT_ENOCFG if neither.  Output pointers may be NULL. */
+int nnjit_online_status(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K, int *measured,
+                        int *total, int *registered);
+
 /* Forget every tuned shape and release the tuner's scratch.  Returns NNJIT_OK. */
 int nnjit_cache_clear(void);
 
@@ -208,16 +240,20 @@ int nnjit_cache_clear(void);
  * type, shape and device, Sec. 5.3): write every tuned shape of every
  * initialised device to a text file at `path` (one line per shape: device
  * signature = architecture name and CU count, kind, dtype, batch, M, N, K,
- * configuration name, split, measured time).  Configurations are stored by
- * name, not id, so a file stays valid across builds that reorder the table.
+ * then up to 5 ranked candidates as configuration name, split, measured
+ * time -- the registered one first).  Configurations are stored by name,
+ * not id, so a file stays valid across builds that reorder the table.
  * Returns the number of entries written, or NNJIT_EINVAL / NNJIT_EHIP. */
 int nnjit_cache_save(const char *path);
 
 /* Read such a file into the per-shape cache of the current device: entries
  * for another device signature, unknown configuration names, configurations
- * that do not fit the entry's kind and dtype, and malformed lines are skipped.
- * Loaded entries replace tuned ones.  Returns the number of entries loaded
- * (>= 0), or NNJIT_EINVAL (unreadable file) / NNJIT_EHIP. */
+ * that do not fit the entry's kind and dtype, and malformed lines are skipped
+ * (a line whose first candidate is unknown is skipped whole; unknown later
+ * candidates are dropped).  Loading merges: a shape already in the cache
+ * keeps whichever entry has the faster measured time, so databases from
+ * identical devices can be loaded one after another.  Returns the number of
+ * valid entries read (>= 0), or NNJIT_EINVAL (unreadable file) / NNJIT_EHIP. */
 int nnjit_cache_load(const char *path);
 
 /* Message for the last error on this thread ("" if none).  The pointer stays

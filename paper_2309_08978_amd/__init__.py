@@ -28,7 +28,8 @@ ERROR_NAMES = {-1: "NNJIT_EINVAL", -2: "NNJIT_EDTYPE", -3: "NNJIT_ENOCFG", -4: "
 
 EXPORTED = ["nnjit_matmul", "nnjit_batched_matmul", "nnjit_tune", "nnjit_tune_batched", "nnjit_matmul_config",
             "nnjit_num_configs", "nnjit_config_info", "nnjit_config_resources", "nnjit_lite_space",
-            "nnjit_last_tune_stats", "nnjit_last_tune_trace", "nnjit_cached_config", "nnjit_cache_clear",
+            "nnjit_last_tune_stats", "nnjit_last_tune_trace", "nnjit_cached_config", "nnjit_cached_ranked",
+            "nnjit_set_online", "nnjit_online_status", "nnjit_cache_clear",
             "nnjit_cache_save", "nnjit_cache_load", "nnjit_last_error", "nnjit_version"]
 
 
@@ -94,6 +95,10 @@ def load(build_if_missing: bool = False) -> ctypes.CDLL:
             "nnjit_last_tune_trace": [ctypes.POINTER(ci), ctypes.POINTER(ctypes.c_double),
                                       ctypes.POINTER(ctypes.c_double), ci],
             "nnjit_cached_config": [ci, ci, i64, i64, i64, i64],
+            "nnjit_cached_ranked": [ci, ci, i64, i64, i64, i64, ctypes.POINTER(ci), ctypes.POINTER(ctypes.c_double), ci],
+            "nnjit_set_online": [ci],
+            "nnjit_online_status": [ci, ci, i64, i64, i64, i64, ctypes.POINTER(ci), ctypes.POINTER(ci),
+                                    ctypes.POINTER(ci)],
             "nnjit_cache_clear": [],
             "nnjit_cache_save": [ctypes.c_char_p],
             "nnjit_cache_load": [ctypes.c_char_p],
@@ -198,6 +203,31 @@ def nnjit_last_tune_trace(cap: int = 256):
 
 def nnjit_cached_config(kind, dtype, batch, M, N, K) -> int:
     return load().nnjit_cached_config(kind, dtype, batch, M, N, K)
+
+
+def nnjit_cached_ranked(kind, dtype, batch, M, N, K, cap: int = 5):
+    """-> [(config id, us)] ranked candidates of a tuned shape (raises if not tuned)."""
+    ids = (ctypes.c_int * cap)()
+    us = (ctypes.c_double * cap)()
+    rc = load().nnjit_cached_ranked(kind, dtype, batch, M, N, K, ids, us, cap)
+    if rc < 0:
+        raise NnjitError(rc, nnjit_last_error())
+    return [(ids[i], us[i]) for i in range(min(rc, cap))]
+
+
+def nnjit_set_online(enable: bool) -> int:
+    """Switch online just-in-time tuning on or off; returns the previous setting."""
+    return load().nnjit_set_online(1 if enable else 0)
+
+
+def nnjit_online_status(kind, dtype, batch, M, N, K) -> dict:
+    """{'state': 'online'|'tuned', 'measured', 'total', 'registered'} (raises if neither)."""
+    m, t, r = ctypes.c_int(-1), ctypes.c_int(-1), ctypes.c_int(-1)
+    rc = load().nnjit_online_status(kind, dtype, batch, M, N, K, ctypes.byref(m), ctypes.byref(t), ctypes.byref(r))
+    if rc < 0:
+        raise NnjitError(rc, nnjit_last_error())
+    return {"state": "online" if rc == 0 else "tuned", "measured": m.value, "total": t.value,
+            "registered": r.value}
 
 
 def nnjit_cache_clear() -> int:

@@ -77,9 +77,33 @@ typedef std::tuple<int, int, int, int64_t, int64_t, int64_t, int64_t> ShapeKey;
 struct Tuned {
     int cfg;
     double us;
+    std::vector<std::pair<int, double>> ranked;   // up to kRanked (config, us): the registered one, then the fastest others
 };
+constexpr int kRanked = 5;
 std::map<ShapeKey, Tuned> g_tuned;
 std::map<ShapeKey, int> g_default;
+
+// Online just-in-time tuning (Sec. 3: a candidate is measured between
+// inferences and re-registered when significantly faster).  Per untuned shape:
+// the lite space in evaluation order, the configuration serving calls, and at
+// most one measurement in flight (its events are read back by a later call).
+struct OnlineShape {
+    std::vector<int> ids;
+    size_t next = 0;
+    int registered = -1;
+    double registered_us = 1e300;
+    int pending = -1;
+    hipEvent_t ev[2] = {nullptr, nullptr};
+    std::vector<std::pair<int, double>> times;
+};
+std::map<ShapeKey, OnlineShape> g_online;
+bool g_online_on = false;
+
+void online_drop(OnlineShape &o) {
+    for (auto &e : o.ev)
+        if (e) (void)hipEventDestroy(e);
+    o.ev[0] = o.ev[1] = nullptr;
+}
 
 int current_device(int *dev) {
     int n = 0;
@@ -305,6 +329,88 @@ int default_config(Device &d, int kind, const Call &c) {
     return lr.ids[0];
 }
 
+// One call on a shape that is being tuned online (caller holds g_mu).
+int online_call(Device &d, int kind, const ShapeKey &key, const Call &c) {
+    auto it = g_online.find(key);
+    if (it == g_online.end()) {
+        LiteResult lr = lite_space(shape_of(kind, c), d.limits, &d.regs, &d.spills);
+        if (lr.ids.empty()) return fail(NNJIT_ENOCFG, "no configuration fits this shape");
+        OnlineShape o;
+        o.ids = lr.ids;
+        o.registered = lr.ids[0];
+        it = g_online.emplace(key, std::move(o)).first;
+    }
+    OnlineShape &o = it->second;
+    hipError_t e;
+    // collect the measurement in flight, if its events have completed
+    if (o.pending >= 0) {
+        e = hipEventQuery(o.ev[1]);
+        if (e == hipSuccess) {
+            float ms = 0.f;
+            if (hipEventElapsedTime(&ms, o.ev[0], o.ev[1]) == hipSuccess) {
+                const double us = ms * 1e3;
+                o.times.emplace_back(o.pending, us);
+                if (o.pending == o.registered) {
+                    o.registered_us = us;
+                } else if (us < o.registered_us / 1.03) {   // significantly faster: re-register
+                    o.registered = o.pending;
+                    o.registered_us = us;
+                }
+            }
+            o.pending = -1;
+        } else if (e != hipErrorNotReady) {
+            (void)hipGetLastError();
+            o.pending = -1;
+        }
+    }
+    // every candidate measured: the shape becomes a tuned shape
+    if (o.pending < 0 && o.next >= o.ids.size()) {
+        Tuned tu{o.registered, o.registered_us, {{o.registered, o.registered_us}}};
+        std::vector<std::pair<double, int>> by_time;
+        for (const auto &t : o.times)
+            if (t.first != o.registered) by_time.emplace_back(t.second, t.first);
+        std::sort(by_time.begin(), by_time.end());
+        for (const auto &bt : by_time)
+            if ((int)tu.ranked.size() < kRanked) tu.ranked.emplace_back(bt.second, bt.first);
+        const int id = o.registered;
+        online_drop(o);
+        g_online.erase(it);
+        g_tuned[key] = tu;
+        const Config &cfg = configs()[id];
+        if (cfg.v->vec_bytes == 16 && !vec_aligned(c, kind == NNJIT_KIND_GEMV)) {
+            const Config *fb = fallback_config(family_of(kind, c.dtype), c, d);
+            if (!fb) return fail(NNJIT_ENOCFG, "no element-load fallback configuration");
+            return launch(d, *fb, c);
+        }
+        return launch(d, cfg, c);
+    }
+    // measure the next candidate on this call, unless measuring is off, one is
+    // still in flight, the stream is being captured or the operands need the
+    // element-load path
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    (void)hipStreamIsCapturing(c.stream, &cap);
+    const bool aligned = vec_aligned(c, kind == NNJIT_KIND_GEMV);
+    if (g_online_on && o.pending < 0 && cap == hipStreamCaptureStatusNone && aligned) {
+        if (!o.ev[0]) {
+            if ((e = hipEventCreate(&o.ev[0])) != hipSuccess || (e = hipEventCreate(&o.ev[1])) != hipSuccess)
+                return hip_fail(e, "hipEventCreate");
+        }
+        const int cand = o.ids[o.next++];
+        (void)hipEventRecord(o.ev[0], c.stream);
+        const int rc = launch(d, configs()[cand], c);
+        if (rc != NNJIT_OK) return rc;   // a failing candidate is not retried
+        (void)hipEventRecord(o.ev[1], c.stream);
+        o.pending = cand;
+        return NNJIT_OK;
+    }
+    const Config *cfg = &configs()[o.registered];
+    if (cfg->v->vec_bytes == 16 && !aligned) {
+        cfg = fallback_config(family_of(kind, c.dtype), c, d);
+        if (!cfg) return fail(NNJIT_ENOCFG, "no element-load fallback configuration");
+    }
+    return launch(d, *cfg, c);
+}
+
 int run(const Call &c, int forced) {
     int rc = validate(c);
     if (rc != NNJIT_OK) return rc;
@@ -334,9 +440,16 @@ int run(const Call &c, int forced) {
             configs()[env_force].v->family == family_of(kind, c.dtype))
             id = env_force;
         if (id < 0) {
-            auto it = g_tuned.find(key_of(d->ordinal, kind, c));
-            id = it != g_tuned.end() ? it->second.cfg : default_config(*d, kind, c);
-            if (id < 0) return id;
+            const ShapeKey key = key_of(d->ordinal, kind, c);
+            auto it = g_tuned.find(key);
+            if (it != g_tuned.end()) {
+                id = it->second.cfg;
+            } else if (g_online_on || g_online.count(key)) {
+                return online_call(*d, kind, key, c);
+            } else {
+                id = default_config(*d, kind, c);
+                if (id < 0) return id;
+            }
         }
         cfg = &configs()[id];
         if (cfg->v->vec_bytes == 16 && !vec_aligned(c, kind == NNJIT_KIND_GEMV)) {
@@ -525,7 +638,19 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
         best = incumbent;
         best_us = inc->second;
     }
-    g_tuned[key] = Tuned{best, best_us};
+    Tuned tu{best, best_us, {}};
+    tu.ranked.emplace_back(best, best_us);
+    {
+        std::vector<std::pair<double, int>> by_time;
+        for (const auto &kv : timed)
+            if (kv.first != best) by_time.emplace_back(kv.second, kv.first);
+        std::sort(by_time.begin(), by_time.end());
+        for (const auto &bt : by_time) {
+            if ((int)tu.ranked.size() >= kRanked) break;
+            tu.ranked.emplace_back(bt.second, bt.first);
+        }
+    }
+    g_tuned[key] = tu;
     t_stats.chosen = best;
     t_stats.best_us = best_us;
     t_stats.wall_ms = ms_since(t0);
@@ -672,9 +797,57 @@ int nnjit_cached_config(int kind, int dtype, int64_t batch, int64_t M, int64_t N
     return it->second.cfg;
 }
 
+int nnjit_cached_ranked(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K, int *ids, double *us,
+                        int cap) {
+    t_err.clear();
+    std::lock_guard<std::mutex> lk(g_mu);
+    int ord = -1;
+    int rc = current_device(&ord);
+    if (rc != NNJIT_OK) return rc;
+    auto it = g_tuned.find(ShapeKey(ord, kind, dtype, batch, M, N, K));
+    if (it == g_tuned.end()) return fail(NNJIT_ENOCFG, "shape not tuned");
+    const auto &r = it->second.ranked;
+    for (int i = 0; i < (int)r.size() && i < cap; ++i) {
+        if (ids) ids[i] = r[i].first;
+        if (us) us[i] = r[i].second;
+    }
+    return (int)r.size();
+}
+
+int nnjit_set_online(int enable) {
+    t_err.clear();
+    std::lock_guard<std::mutex> lk(g_mu);
+    const int prev = g_online_on ? 1 : 0;
+    g_online_on = enable != 0;
+    return prev;
+}
+
+int nnjit_online_status(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K, int *measured,
+                        int *total, int *registered) {
+    t_err.clear();
+    std::lock_guard<std::mutex> lk(g_mu);
+    int ord = -1;
+    int rc = current_device(&ord);
+    if (rc != NNJIT_OK) return rc;
+    const ShapeKey key(ord, kind, dtype, batch, M, N, K);
+    auto it = g_online.find(key);
+    if (it != g_online.end()) {
+        if (measured) *measured = (int)it->second.times.size();
+        if (total) *total = (int)it->second.ids.size();
+        if (registered) *registered = it->second.registered;
+        return 0;
+    }
+    auto tt = g_tuned.find(key);
+    if (tt == g_tuned.end()) return fail(NNJIT_ENOCFG, "shape neither tuned nor being tuned online");
+    if (registered) *registered = tt->second.cfg;
+    return 1;
+}
+
 int nnjit_cache_clear(void) {
     t_err.clear();
     std::lock_guard<std::mutex> lk(g_mu);
+    for (auto &kv : g_online) online_drop(kv.second);
+    g_online.clear();
     g_tuned.clear();
     g_default.clear();
     for (auto &kv : g_devices) {
@@ -698,17 +871,20 @@ int nnjit_cache_save(const char *path) {
     std::lock_guard<std::mutex> lk(g_mu);
     FILE *f = fopen(path, "w");
     if (!f) return fail(NNJIT_EINVAL, "cannot write %s", path);
-    fprintf(f, "# nnjit kernel database v1: signature kind dtype batch M N K config split us\n");
+    fprintf(f, "# nnjit kernel database v2: signature kind dtype batch M N K, then up to %d ranked (config split us), "
+               "the registered one first\n", kRanked);
     int n = 0;
     for (const auto &kv : g_tuned) {
         const int dev = std::get<0>(kv.first);
         auto di = g_devices.find(dev);
         if (di == g_devices.end() || !di->second.ready) continue;
-        const Config &c = configs()[kv.second.cfg];
-        fprintf(f, "%s:%d %d %d %lld %lld %lld %lld %s %d %.4f\n", di->second.arch.c_str(), di->second.limits.num_cus,
+        fprintf(f, "%s:%d %d %d %lld %lld %lld %lld", di->second.arch.c_str(), di->second.limits.num_cus,
                 std::get<1>(kv.first), std::get<2>(kv.first), (long long)std::get<3>(kv.first),
-                (long long)std::get<4>(kv.first), (long long)std::get<5>(kv.first), (long long)std::get<6>(kv.first),
-                c.v->name, c.split, kv.second.us);
+                (long long)std::get<4>(kv.first), (long long)std::get<5>(kv.first), (long long)std::get<6>(kv.first));
+        std::vector<std::pair<int, double>> ranked = kv.second.ranked;
+        if (ranked.empty()) ranked.emplace_back(kv.second.cfg, kv.second.us);
+        for (const auto &r : ranked) fprintf(f, " %s %d %.4f", configs()[r.first].v->name, configs()[r.first].split, r.second);
+        fprintf(f, "\n");
         ++n;
     }
     fclose(f);
@@ -726,28 +902,40 @@ int nnjit_cache_load(const char *path) {
     if (!f) return fail(NNJIT_EINVAL, "cannot read %s", path);
     char sig_want[160];
     snprintf(sig_want, sizeof sig_want, "%s:%d", d->arch.c_str(), d->limits.num_cus);
-    char line[512];
+    char line[4096];
     int n = 0;
+    auto find_id = [](const char *name, int split) {
+        for (const Config &c : configs())
+            if (c.split == split && strcmp(c.v->name, name) == 0) return c.id;
+        return -1;
+    };
     while (fgets(line, sizeof line, f)) {
         if (line[0] == '#') continue;
         char sig[160], name[160];
-        int kind, dtype, split;
+        int kind, dtype, split, used = 0;
         long long batch, M, N, K;
         double us;
-        if (sscanf(line, "%159s %d %d %lld %lld %lld %lld %159s %d %lf", sig, &kind, &dtype, &batch, &M, &N, &K, name,
-                   &split, &us) != 10)
+        if (sscanf(line, "%159s %d %d %lld %lld %lld %lld %159s %d %lf%n", sig, &kind, &dtype, &batch, &M, &N, &K, name,
+                   &split, &us, &used) != 10)
             continue;
         if (strcmp(sig, sig_want) != 0) continue;
         if (kind < NNJIT_KIND_GEMM || kind > NNJIT_KIND_GEMV || (dtype != NNJIT_F32 && dtype != NNJIT_F16)) continue;
         if (batch < 1 || M < 1 || N < 1 || K < 0) continue;
-        int id = -1;
-        for (const Config &c : configs())
-            if (c.split == split && strcmp(c.v->name, name) == 0) {
-                id = c.id;
-                break;
-            }
+        const int id = find_id(name, split);
         if (id < 0 || configs()[id].v->family != family_of(kind, dtype)) continue;
-        g_tuned[ShapeKey(d->ordinal, kind, dtype, batch, M, N, K)] = Tuned{id, us};
+        Tuned tu{id, us, {{id, us}}};
+        // the other ranked candidates (v2 lines); unknown names are skipped
+        const char *rest = line + used;
+        int more = 0;
+        while ((int)tu.ranked.size() < kRanked && sscanf(rest, "%159s %d %lf%n", name, &split, &us, &more) == 3) {
+            rest += more;
+            const int rid = find_id(name, split);
+            if (rid >= 0 && configs()[rid].v->family == family_of(kind, dtype)) tu.ranked.emplace_back(rid, us);
+        }
+        // merging databases: a shape already known keeps the faster measurement
+        const ShapeKey key(d->ordinal, kind, dtype, batch, M, N, K);
+        auto it = g_tuned.find(key);
+        if (it == g_tuned.end() || tu.us < it->second.us) g_tuned[key] = tu;
         ++n;
     }
     fclose(f);

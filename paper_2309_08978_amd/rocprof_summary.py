@@ -15,7 +15,9 @@ or of a ``--pmc`` run (``*_counter_collection.csv``), and prints:
 With --traffic FETCH_DIR WRITE_DIR --meta META [--db profiles/traffic.json] it
 turns two counter runs of ``bench.py --profile-op`` (``rocprofv3 --pmc
 FETCH_SIZE`` and ``--pmc WRITE_SIZE``) into HBM bytes per launch of the
-profiled product, scaled by the reference copy in the same run.
+profiled product, scaled by the reference copy in the same run.  With
+--mfma PMC_DIR --meta META it reports the matrix-core busy fraction of the
+product from a ``--pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE ...`` run.
 """
 from __future__ import annotations
 
@@ -131,6 +133,37 @@ def traffic(fetch_dir, write_dir, meta):
             "write": out["write"], "reps": meta["reps"], "copy_ref_mb": meta["copy_ref_mb"]}
 
 
+def mfma_busy(pmc_dir, meta, simds: int = 1024):
+    """Matrix-core busy fraction of the profiled product from one counter run
+    of SQ_VALU_MFMA_BUSY_CYCLES (summed over all SIMDs, in cycles) and
+    GRBM_GUI_ACTIVE (GPU busy cycles, summed over the 8 XCDs): busy /
+    (simds x GRBM_GUI_ACTIVE / 8), over the product's dispatches after the
+    reference copy."""
+    path = sorted(glob.glob(os.path.join(pmc_dir, "**", "*counter_collection.csv"), recursive=True))
+    if not path:
+        raise SystemExit(f"no counter_collection.csv under {pmc_dir}")
+    per = OrderedDict()
+    for r in _rows(path[0]):
+        d = int(r["Dispatch_Id"])
+        per.setdefault(d, {"name": r["Kernel_Name"], "grid": r.get("Grid_Size")})
+        per[d][r["Counter_Name"]] = per[d].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    rows = [v for _, v in sorted(per.items())]
+    last_copy = max(i for i, v in enumerate(rows) if "copyBuffer" in v["name"] or "copy_kernel" in v["name"])
+    mine = [v for v in rows[last_copy + 1:] if "nnjit" in v["name"]]
+    tot = {}
+    for v in mine:
+        for k, x in v.items():
+            if k not in ("name", "grid"):
+                tot[k] = tot.get(k, 0.0) + x
+    reps = meta["reps"]
+    busy = tot.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / reps
+    gui = tot.get("GRBM_GUI_ACTIVE", 0.0) / reps
+    out = {k: round(x / reps, 1) for k, x in sorted(tot.items())}
+    out["mfma_busy_fraction"] = round(busy / (simds * gui / 8.0), 4) if gui > 0 else None
+    out["kernels"] = sorted({_short(v["name"]) for v in mine})
+    return out
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("out_dir", nargs="?")
@@ -140,7 +173,16 @@ def main(argv=None) -> int:
                     help="counter runs of bench.py --profile-op: record HBM bytes per launch")
     ap.add_argument("--meta", help="file holding the metadata line bench.py --profile-op printed")
     ap.add_argument("--db", help="traffic database (JSON) to add the entry to")
+    ap.add_argument("--mfma", metavar="PMC_DIR",
+                    help="counter run of bench.py --profile-op with SQ_VALU_MFMA_BUSY_CYCLES and GRBM_GUI_ACTIVE: "
+                         "matrix-core busy fraction of the product")
     a = ap.parse_args(argv)
+    if a.mfma:
+        import json
+        with open(a.meta) as f:
+            meta = next(json.loads(l) for l in f if l.startswith("{"))
+        print(json.dumps(mfma_busy(a.mfma, meta), indent=1))
+        return 0
     if a.traffic:
         import json
         with open(a.meta) as f:

@@ -143,3 +143,80 @@ def test_kernel_database_roundtrip(tmp_path):
     assert nj.check(nj.nnjit_tune(op.M, op.N, op.K, nj.NNJIT_F32)) == cfg
     assert nj.nnjit_last_tune_stats()["cache_hit"] == 1
     assert nj.nnjit_cache_load(str(tmp_path / "missing.txt")) == nj.NNJIT_EINVAL
+
+
+def test_ranked_candidates_and_database_merge(tmp_path):
+    """The database keeps the top-ranked candidates of a shape (registered one
+    first) and merging two databases keeps the faster measurement."""
+    op = workloads.workload("bart_base_layer_seq128_f32")[1]
+    nj.nnjit_cache_clear()
+    cfg = nj.check(nj.nnjit_tune(op.M, op.N, op.K, nj.NNJIT_F32))
+    ranked = nj.nnjit_cached_ranked(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, op.M, op.N, op.K)
+    st = nj.nnjit_last_tune_stats()
+    assert ranked[0][0] == cfg and 1 <= len(ranked) <= 5
+    assert len(ranked) == min(5, st["n_timed"])
+    assert all(a[1] <= b[1] for a, b in zip(ranked[1:], ranked[2:]))     # the others by time
+    assert len({c for c, _ in ranked}) == len(ranked)
+    fast = tmp_path / "fast.txt"
+    nj.check(nj.nnjit_cache_save(str(fast)))
+    line = next(l for l in fast.read_text().splitlines() if not l.startswith("#"))
+    f = line.split()
+    assert len(f) == 7 + 3 * len(ranked)
+    # a second database from an "identical device" with a slower measurement of
+    # another configuration: merging keeps the faster one
+    other = ranked[1][0] if len(ranked) > 1 else cfg
+    slow = tmp_path / "slow.txt"
+    oc = nj.configs()[other]
+    slow.write_text(" ".join(f[:7] + [oc["name"], str(oc["split"]), f"{ranked[0][1] * 10:.4f}"]) + "\n")
+    assert nj.check(nj.nnjit_cache_load(str(slow))) == 1
+    assert nj.nnjit_cached_config(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, op.M, op.N, op.K) == cfg
+    nj.nnjit_cache_clear()
+    assert nj.check(nj.nnjit_cache_load(str(slow))) == 1
+    assert nj.nnjit_cached_config(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, op.M, op.N, op.K) == other
+    assert nj.check(nj.nnjit_cache_load(str(fast))) == 1                   # faster entry wins
+    assert nj.nnjit_cached_config(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, op.M, op.N, op.K) == cfg
+    back = nj.nnjit_cached_ranked(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, op.M, op.N, op.K)
+    assert [c for c, _ in back] == [c for c, _ in ranked]          # times are stored to 1e-4 us
+    assert all(abs(u - v) <= 1e-4 + 1e-6 * v for (_, u), (_, v) in zip(back, ranked))
+    nj.nnjit_cache_clear()
+
+
+def test_online_tuning_serves_every_call_and_converges():
+    """Online mode: every call returns the exact product while the lite space
+    is measured one candidate per call; once all are measured the shape is
+    cached, and turning the mode off leaves the cache in place."""
+    import torch
+    M, N, K = 96, 256, 384
+    A, B = workloads.small_int_operands(4242, 1, M, K, N, "f32")
+    R = oracle.matmul(A, B)
+    dA, dB = dev(A), dev(B)
+    nj.nnjit_cache_clear()
+    prev = nj.nnjit_set_online(True)
+    try:
+        calls, states = 0, []
+        for calls in range(1, 400):
+            C = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda:0")
+            nj.matmul(dA, dB, C)
+            assert np.array_equal(host(C), R), f"call {calls}"      # host() synchronises
+            st = nj.nnjit_online_status(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, M, N, K)
+            states.append(st)
+            if st["state"] == "tuned":
+                break
+        assert states[-1]["state"] == "tuned", states[-1]
+        first = states[0]
+        assert first["state"] == "online" and first["total"] >= 8
+        assert calls >= first["total"]                 # one candidate per call at most
+        measured = [s["measured"] for s in states if s["state"] == "online"]
+        assert measured == sorted(measured)           # progress is monotone
+        cfg = nj.nnjit_cached_config(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, M, N, K)
+        lite, _, _, _ = nj.nnjit_lite_space(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, M, N, K)
+        assert cfg in lite and cfg == states[-1]["registered"]
+        ranked = nj.nnjit_cached_ranked(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, M, N, K)
+        assert ranked[0][0] == cfg
+    finally:
+        nj.nnjit_set_online(prev)
+    # later calls use the cached configuration
+    C = torch.empty((M, N), dtype=torch.float32, device="cuda:0")
+    nj.matmul(dA, dB, C)
+    assert np.array_equal(host(C), R)
+    nj.nnjit_cache_clear()
