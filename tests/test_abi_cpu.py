@@ -168,3 +168,20 @@ def test_misaligned_shapes_get_element_load_configs(lib):
     assert n >= 1 and all(cfgs[i]["vec"] == 4 for i in ids)
     ids, n, _, _ = nj.nnjit_lite_space(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, 100, 104, 96, d)
     assert all(cfgs[i]["vec"] == 16 for i in ids)
+
+
+def test_microbench_groups_vary_one_primitive(lib):
+    """The offline microbenchmark compares only configurations that differ in
+    exactly one primitive (besides derived fields)."""
+    from paper_2309_08978_amd.microbench import groups_for, PRIMITIVES, DERIVED
+    cfgs = [c for c in nj.configs() if c["family"] == "gemm_f32"]
+    total = 0
+    for prim in PRIMITIVES:
+        for grp in groups_for(cfgs, prim):
+            total += 1
+            assert len({c[prim] for c in grp}) >= 2
+            for c in grp:
+                assert c["split"] == 1
+                rest = {k: v for k, v in c.items() if k not in DERIVED and k != prim}
+                assert rest == {k: v for k, v in grp[0].items() if k not in DERIVED and k != prim}
+    assert total >= 10
