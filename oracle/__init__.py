@@ -71,6 +71,8 @@ class Oracle:
         lib.oracle_f16_to_f64.restype = ctypes.c_double
         lib.oracle_f16_to_f64.argtypes = [ctypes.c_uint16]
         lib.oracle_max_threads.restype = ctypes.c_int
+        lib.oracle_gemv_q4.restype = ctypes.c_int
+        lib.oracle_gemv_q4.argtypes = [i64, i64, vp, vp, i64, vp, i64, i64, vp, ctypes.c_int]
         self.lib = lib
 
     def matmul(self, A: np.ndarray, B: np.ndarray, nthreads: int = 0) -> np.ndarray:
@@ -112,6 +114,24 @@ class Oracle:
         bits = np.asarray(bits, dtype=np.uint16).ravel()
         return np.array([self.lib.oracle_f16_to_f64(int(b)) for b in bits], dtype=np.float64)
 
+    def gemv_q4(self, x: np.ndarray, Wq: np.ndarray, S: np.ndarray, group: int, N: int,
+                nthreads: int = 0) -> np.ndarray:
+        """fp64 y[N] = x[K] . W for the 4-bit weight format of oracle.c:
+        x float16 [K], Wq uint32 [K, ldq] (eight codes per word along N),
+        S float16 [ceil(K/group), lds]."""
+        x = np.ascontiguousarray(x, dtype=np.float16)
+        Wq = np.ascontiguousarray(Wq, dtype=np.uint32)
+        S = np.ascontiguousarray(S, dtype=np.float16)
+        K = x.shape[0]
+        if Wq.shape[0] != K or S.shape[0] < (K + group - 1) // group:
+            raise ValueError("shape mismatch")
+        y = np.empty(N, dtype=np.float64)
+        rc = self.lib.oracle_gemv_q4(K, N, x.ctypes.data, Wq.ctypes.data, Wq.shape[1], S.ctypes.data,
+                                     S.shape[1], int(group), y.ctypes.data, int(nthreads))
+        if rc != 0:
+            raise RuntimeError(f"oracle_gemv_q4 returned {rc}")
+        return y
+
     def max_threads(self) -> int:
         return int(self.lib.oracle_max_threads())
 
@@ -134,6 +154,10 @@ def elements(A: np.ndarray, B: np.ndarray, idx) -> np.ndarray:
 
 def f16_to_f64(bits) -> np.ndarray:
     return default().f16_to_f64(bits)
+
+
+def gemv_q4(x, Wq, S, group: int, N: int, nthreads: int = 0) -> np.ndarray:
+    return default().gemv_q4(x, Wq, S, group, N, nthreads)
 
 
 def max_threads() -> int:
