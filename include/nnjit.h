@@ -56,8 +56,12 @@ extern "C" {
 enum nnjit_dtype { NNJIT_F32 = 0, NNJIT_F16 = 1 };
 
 /* Operator kinds: the key "t" (kernel type) of the paper's kernel database
- * (Sec. 5.3).  GEMV is the M == 1, batch == 1 case of MatMul. */
-enum nnjit_kind { NNJIT_KIND_GEMM = 0, NNJIT_KIND_BATCHED = 1, NNJIT_KIND_GEMV = 2 };
+ * (Sec. 5.3).  GEMV is the M == 1, batch == 1 case of MatMul.  GEMV_Q4 is
+ * the GEMV of a 4-bit weight-only quantised matrix (nnjit_gemv_q4); every
+ * function below that takes (kind, dtype, batch, M, N, K) identifies such a
+ * shape as (NNJIT_KIND_GEMV_Q4, NNJIT_F16, group, 1, N, K): the group size
+ * stands in the batch position (the product has no batch dimension). */
+enum nnjit_kind { NNJIT_KIND_GEMM = 0, NNJIT_KIND_BATCHED = 1, NNJIT_KIND_GEMV = 2, NNJIT_KIND_GEMV_Q4 = 3 };
 
 #define NNJIT_OK 0
 #define NNJIT_EINVAL (-1)  /* bad dimension, leading dim, stride, NULL pointer, config id */
@@ -112,13 +116,49 @@ int nnjit_tune_batched(int64_t batch, int64_t M, int64_t N, int64_t K, int dtype
 /* Run one forced configuration `cfg` (test and report helper): any kind's
  * configuration may be forced as long as it belongs to this dtype; GEMV
  * configurations additionally need batch == 1 and M == 1; a vector-load
- * configuration needs the 16-byte alignment described above.  A mismatch is
- * NNJIT_EINVAL. */
+ * configuration needs the 16-byte alignment described above.  A mismatch,
+ * or a configuration of the 4-bit GEMV family, is NNJIT_EINVAL. */
 int nnjit_matmul_config(int cfg, int64_t batch, int64_t M, int64_t N, int64_t K,
                         const void *A, int64_t lda, int64_t strideA,
                         const void *B, int64_t ldb, int64_t strideB,
                         void *C, int64_t ldc, int64_t strideC,
                         int dtype, void *stream);
+
+/* y = x . W for a 4-bit weight-only quantised W (the 4-bit Llama-2-7B
+ * decode workload of Sec. 7, whose quantisation format the paper does not
+ * give; this library reads it as symmetric 4-bit codes with one fp16 scale
+ * per group of `group` consecutive rows and column):
+ *     W[k][n] = (q[k][n] - 8) * scales[(k / group) * lds + n]
+ *     q[k][n] = (Wq[k * ldq + n / 8] >> (4 * (n % 8))) & 15
+ *     y[n]    = sum_k x[k] * W[k][n],   0 <= n < N,  0 <= k < K
+ * x: IEEE binary16 [K]; Wq: uint32 words, K rows of ldq words, eight codes
+ * per word along n, low nibble first; scales: binary16, ceil(K / group)
+ * rows of lds; y: fp32 [N], overwritten.  Products and sums in fp32 (each
+ * group's codes summed, then multiplied by its scale); the order of the
+ * additions is fixed, so results are deterministic.
+ * Preconditions: N, K >= 0 (< 2^31); group >= 1; ldq >= ceil(N / 8);
+ * lds >= N; NULL only for an operand with no elements.  N == 0 is a no-op;
+ * K == 0 writes zeros.  All pointers are DEVICE pointers owned by the
+ * caller.  Errors: NNJIT_EINVAL for bad arguments, as for nnjit_matmul.
+ * 16-byte loads are used when N % 32 == 0, ldq % 4 == 0, lds % 8 == 0 and
+ * Wq, scales are 16-byte aligned; otherwise a word-load configuration runs
+ * (correct, slower).  Uses the tuned configuration of (N, K, group) if
+ * nnjit_tune_gemv_q4 ran for it, else the first of its lite space; online
+ * tuning (nnjit_set_online) applies as for nnjit_matmul. */
+int nnjit_gemv_q4(int64_t N, int64_t K, int64_t group, const void *x, const void *Wq, int64_t ldq,
+                  const void *scales, int64_t lds, void *y, void *stream);
+
+/* Just-in-time tuning of a 4-bit GEMV shape, as nnjit_tune (the weights
+ * and scales are timed streamed from HBM, rotating over copies of >= 512 MiB
+ * together).  Returns the chosen configuration id or an error code. */
+int nnjit_tune_gemv_q4(int64_t N, int64_t K, int64_t group);
+
+/* nnjit_gemv_q4 with a forced configuration `cfg` of the 4-bit GEMV family
+ * (test and report helper); another family's id, or a 16-byte-load
+ * configuration for operands that do not meet its conditions, is
+ * NNJIT_EINVAL. */
+int nnjit_gemv_q4_config(int cfg, int64_t N, int64_t K, int64_t group, const void *x, const void *Wq, int64_t ldq,
+                         const void *scales, int64_t lds, void *y, void *stream);
 
 /* Number of configurations (ids are 0 .. n-1, fixed for a build). */
 int nnjit_num_configs(void);

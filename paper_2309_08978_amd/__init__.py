@@ -22,11 +22,12 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libnnjit.so")
 
 NNJIT_F32, NNJIT_F16 = 0, 1
-NNJIT_KIND_GEMM, NNJIT_KIND_BATCHED, NNJIT_KIND_GEMV = 0, 1, 2
+NNJIT_KIND_GEMM, NNJIT_KIND_BATCHED, NNJIT_KIND_GEMV, NNJIT_KIND_GEMV_Q4 = 0, 1, 2, 3
 NNJIT_OK, NNJIT_EINVAL, NNJIT_EDTYPE, NNJIT_ENOCFG, NNJIT_EHIP, NNJIT_ENOMEM = 0, -1, -2, -3, -4, -5
 ERROR_NAMES = {-1: "NNJIT_EINVAL", -2: "NNJIT_EDTYPE", -3: "NNJIT_ENOCFG", -4: "NNJIT_EHIP", -5: "NNJIT_ENOMEM"}
 
 EXPORTED = ["nnjit_matmul", "nnjit_batched_matmul", "nnjit_tune", "nnjit_tune_batched", "nnjit_matmul_config",
+            "nnjit_gemv_q4", "nnjit_tune_gemv_q4", "nnjit_gemv_q4_config",
             "nnjit_num_configs", "nnjit_config_info", "nnjit_config_resources", "nnjit_lite_space",
             "nnjit_last_tune_stats", "nnjit_last_tune_trace", "nnjit_cached_config", "nnjit_cached_ranked",
             "nnjit_set_online", "nnjit_online_status", "nnjit_cache_clear",
@@ -86,6 +87,9 @@ def load(build_if_missing: bool = False) -> ctypes.CDLL:
             "nnjit_tune": [i64, i64, i64, ci],
             "nnjit_tune_batched": [i64, i64, i64, i64, ci],
             "nnjit_matmul_config": [ci, i64, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64, i64, ci, vp],
+            "nnjit_gemv_q4": [i64, i64, i64, vp, vp, i64, vp, i64, vp, vp],
+            "nnjit_tune_gemv_q4": [i64, i64, i64],
+            "nnjit_gemv_q4_config": [ci, i64, i64, i64, vp, vp, i64, vp, i64, vp, vp],
             "nnjit_num_configs": [],
             "nnjit_config_info": [ci, ctypes.c_char_p, i64],
             "nnjit_config_resources": [ci, ctypes.POINTER(DeviceLimits), ctypes.POINTER(Resources)],
@@ -153,6 +157,19 @@ def nnjit_matmul_config(cfg, batch, M, N, K, A, lda, strideA, B, ldb, strideB, C
                         stream=None) -> int:
     return load().nnjit_matmul_config(cfg, batch, M, N, K, _ptr(A), lda, strideA, _ptr(B), ldb, strideB,
                                       _ptr(C), ldc, strideC, dtype, _stream(stream))
+
+
+def nnjit_gemv_q4(N, K, group, x, Wq, ldq, scales, lds, y, stream=None) -> int:
+    return load().nnjit_gemv_q4(N, K, group, _ptr(x), _ptr(Wq), ldq, _ptr(scales), lds, _ptr(y), _stream(stream))
+
+
+def nnjit_tune_gemv_q4(N, K, group) -> int:
+    return load().nnjit_tune_gemv_q4(N, K, group)
+
+
+def nnjit_gemv_q4_config(cfg, N, K, group, x, Wq, ldq, scales, lds, y, stream=None) -> int:
+    return load().nnjit_gemv_q4_config(cfg, N, K, group, _ptr(x), _ptr(Wq), ldq, _ptr(scales), lds, _ptr(y),
+                                       _stream(stream))
 
 
 def nnjit_num_configs() -> int:
@@ -320,6 +337,26 @@ def batched_matmul(A, B, C=None, stream=None, cfg: Optional[int] = None):
     else:
         check(nnjit_matmul_config(cfg, batch, M, N, K, A, _ld(A), sA, B, _ld(B), sB, C, _ld(C), sC, dt, stream))
     return C
+
+
+def gemv_q4(x, Wq, scales, group: int, N: int, y=None, stream=None, cfg: Optional[int] = None):
+    """y = x . W for a 4-bit weight-only W (include/nnjit.h, nnjit_gemv_q4):
+    x fp16 [K], Wq int32 [K, ldq] (uint32 code words, reinterpreted), scales
+    fp16 [ceil(K / group), lds]; y fp32 [N] (allocated if None)."""
+    import torch
+    K = int(x.shape[0])
+    if Wq.dim() != 2 or Wq.shape[0] != K or scales.dim() != 2:
+        raise ValueError(f"shape mismatch x {tuple(x.shape)}, Wq {tuple(Wq.shape)}, scales {tuple(scales.shape)}")
+    if x.dtype != torch.float16 or scales.dtype != torch.float16 or Wq.element_size() != 4:
+        raise TypeError("x and scales must be float16, Wq 32-bit words")
+    if y is None:
+        y = torch.empty((N,), dtype=torch.float32, device=x.device)
+    ldq, lds = _ld(Wq), _ld(scales)
+    if cfg is None:
+        check(nnjit_gemv_q4(N, K, group, x, Wq, ldq, scales, lds, y, stream))
+    else:
+        check(nnjit_gemv_q4_config(cfg, N, K, group, x, Wq, ldq, scales, lds, y, stream))
+    return y
 
 
 def configs() -> list:

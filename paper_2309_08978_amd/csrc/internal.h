@@ -9,7 +9,7 @@ namespace nnjit {
 
 // Kernel families.  A family fixes the operand dtype and the kernel template;
 // the configurations of a family differ in their tiling parameters.
-enum Family { FAM_GEMM_F32 = 0, FAM_GEMM_F16 = 1, FAM_GEMV_F32 = 2, FAM_GEMV_F16 = 3, FAM_COUNT = 4 };
+enum Family { FAM_GEMM_F32 = 0, FAM_GEMM_F16 = 1, FAM_GEMV_F32 = 2, FAM_GEMV_F16 = 3, FAM_GEMV_Q4 = 4, FAM_COUNT = 5 };
 
 // Arguments of the GEMM / BatchMatMul kernels (one product per grid.z slice).
 struct GemmParams {
@@ -38,6 +38,24 @@ struct GemvParams {
     int kchunk;       // rows of W per split
     int segs;         // column segments
     float *ws;        // S > 1: partial rows, [S][N]
+};
+
+// Arguments of the 4-bit weight-only GEMV: y[N] = x[K] . W[K][N] with
+// W[k][n] = (q[k][n] - 8) * S[k / G][n], q packed eight per 32-bit word
+// along n (low nibble first), S fp16, x fp16, y fp32.
+struct GemvQ4Params {
+    const void *x;        // fp16 [K]
+    const void *Wq;       // uint32 [K][ldq]
+    const void *S;        // fp16 [ngroups][lds]
+    float *y;
+    long long ldq, lds;
+    int K, N, G;
+    int ngroups;          // ceil(K / G)
+    int gchunk;           // groups per split
+    int nsplit;           // splits (workgroups per column segment)
+    int segs;             // column segments
+    int xpair;            // 1: G even and x 4-byte aligned (x pairs load as one word)
+    float *ws;            // nsplit > 1: partial rows, [nsplit][N]
 };
 
 typedef hipError_t (*LaunchFn)(const void *params, dim3 grid, hipStream_t stream);
@@ -71,6 +89,8 @@ extern const Variant kGemmF16Variants[];
 extern const int kNumGemmF16Variants;
 extern const Variant kGemvVariants[];
 extern const int kNumGemvVariants;
+extern const Variant kGemvQ4Variants[];
+extern const int kNumGemvQ4Variants;
 
 // Device helper kernels: the fixed-order split-K reduction
 //   C[z][i][j] = ws[0][z][i][j] + ws[1][z][i][j] + ... + ws[S-1][z][i][j]

@@ -195,9 +195,28 @@ struct Call {
     int64_t ldc, sC;
     int dtype;
     hipStream_t stream;
+    // 4-bit GEMV (q4 = true): A = x, B = the code words (ldb = ldq), Sc =
+    // the scales (leading dimension lds), batch = the group size, M = 1
+    bool q4 = false;
+    const void *Sc = nullptr;
+    int64_t lds = 0;
 };
 
+int validate_q4(const Call &c) {
+    if (c.N < 0 || c.K < 0) return fail(NNJIT_EINVAL, "negative dimension (N=%lld K=%lld)", (long long)c.N, (long long)c.K);
+    if (c.N > INT32_MAX || c.K > INT32_MAX) return fail(NNJIT_EINVAL, "dimension above 2^31-1");
+    if (c.batch < 1 || c.batch > INT32_MAX) return fail(NNJIT_EINVAL, "group=%lld must be in [1, 2^31)", (long long)c.batch);
+    if (c.ldb < (c.N + 7) / 8) return fail(NNJIT_EINVAL, "ldq=%lld < ceil(N/8)=%lld", (long long)c.ldb, (long long)((c.N + 7) / 8));
+    if (c.lds < c.N) return fail(NNJIT_EINVAL, "lds=%lld < N=%lld", (long long)c.lds, (long long)c.N);
+    if (c.N > 0) {
+        if (c.K > 0 && (!c.A || !c.B || !c.Sc)) return fail(NNJIT_EINVAL, "x, Wq or scales is NULL");
+        if (!c.C) return fail(NNJIT_EINVAL, "y is NULL");
+    }
+    return NNJIT_OK;
+}
+
 int validate(const Call &c) {
+    if (c.q4) return validate_q4(c);
     if (c.dtype != NNJIT_F32 && c.dtype != NNJIT_F16) return fail(NNJIT_EDTYPE, "unknown dtype %d", c.dtype);
     if (c.batch < 0 || c.M < 0 || c.N < 0 || c.K < 0)
         return fail(NNJIT_EINVAL, "negative dimension (batch=%lld M=%lld N=%lld K=%lld)", (long long)c.batch,
@@ -219,6 +238,7 @@ int validate(const Call &c) {
 bool is_noop(const Call &c) { return c.batch == 0 || c.M == 0 || c.N == 0; }
 
 int kind_of(const Call &c) {
+    if (c.q4) return NNJIT_KIND_GEMV_Q4;
     if (c.batch == 1 && c.M == 1) return NNJIT_KIND_GEMV;
     return c.batch == 1 ? NNJIT_KIND_GEMM : NNJIT_KIND_BATCHED;
 }
@@ -234,6 +254,18 @@ bool vec_aligned(const Call &c, bool gemv) {
     return c.K % V == 0 && c.lda % V == 0 && al(c.A) && (c.batch <= 1 || c.sA % V == 0);
 }
 
+// Can a 16-byte-load 4-bit GEMV configuration run these operands?
+bool vec_aligned_q4(const Call &c) {
+    auto al = [](const void *p) { return ((uintptr_t)p & 15u) == 0; };
+    return c.N % 32 == 0 && c.ldb % 4 == 0 && c.lds % 8 == 0 && al(c.B) && al(c.Sc);
+}
+
+// vector-load eligibility for the family a call runs on
+bool aligned_for(int kind, const Call &c) {
+    if (kind == NNJIT_KIND_GEMV_Q4) return vec_aligned_q4(c);
+    return vec_aligned(c, kind == NNJIT_KIND_GEMV);
+}
+
 // ------------------------------------------------------------------ launch
 
 int launch(Device &d, const Config &cfg, const Call &c) {
@@ -247,7 +279,26 @@ int launch(Device &d, const Config &cfg, const Call &c) {
         if (rc != NNJIT_OK) return rc;
     }
     hipError_t e = hipSuccess;
-    if (!family_is_gemv(v.family)) {
+    if (family_is_q4(v.family)) {
+        GemvQ4Params p{};
+        p.x = c.A;
+        p.Wq = c.B;
+        p.S = c.Sc;
+        p.y = (float *)c.C;
+        p.ldq = c.ldb;
+        p.lds = c.lds;
+        p.K = (int)c.K;
+        p.N = (int)c.N;
+        p.G = (int)g.group;
+        p.ngroups = (int)g.ngroups;
+        p.gchunk = g.kchunk;
+        p.nsplit = g.split;
+        p.segs = g.tiles_n;
+        p.xpair = (g.group % 2 == 0 && ((uintptr_t)c.A & 3u) == 0) ? 1 : 0;
+        p.ws = w ? w->ws : nullptr;
+        e = v.launch(&p, dim3((unsigned)g.wgs), c.stream);
+        if (e == hipSuccess && g.split > 1) e = launch_splitk_reduce(p.ws, g.split, 1, 1, p.N, p.y, p.N, 0, c.stream);
+    } else if (!family_is_gemv(v.family)) {
         GemmParams p{};
         p.lda = c.lda;
         p.ldb = c.ldb;
@@ -301,6 +352,12 @@ const Config *fallback_config(int family, const Call &c, const Device &d) {
     const Config *best = nullptr;
     for (const Config &cfg : configs()) {
         if (cfg.v->family != family || cfg.v->vec_bytes == 16) continue;
+        if (family_is_q4(family)) {
+            const Geometry g = geometry_of(cfg, c.batch, c.M, c.N, c.K);
+            if (g.split != cfg.split) continue;
+            if (!best || g.wgs <= 2LL * d.limits.num_cus) best = &cfg;
+            continue;
+        }
         if (!family_is_gemv(family)) {
             if (cfg.split == 1) return &cfg;
             continue;
@@ -377,7 +434,7 @@ int online_call(Device &d, int kind, const ShapeKey &key, const Call &c) {
         g_online.erase(it);
         g_tuned[key] = tu;
         const Config &cfg = configs()[id];
-        if (cfg.v->vec_bytes == 16 && !vec_aligned(c, kind == NNJIT_KIND_GEMV)) {
+        if (cfg.v->vec_bytes == 16 && !aligned_for(kind, c)) {
             const Config *fb = fallback_config(family_of(kind, c.dtype), c, d);
             if (!fb) return fail(NNJIT_ENOCFG, "no element-load fallback configuration");
             return launch(d, *fb, c);
@@ -389,7 +446,7 @@ int online_call(Device &d, int kind, const ShapeKey &key, const Call &c) {
     // element-load path
     hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
     (void)hipStreamIsCapturing(c.stream, &cap);
-    const bool aligned = vec_aligned(c, kind == NNJIT_KIND_GEMV);
+    const bool aligned = aligned_for(kind, c);
     if (g_online_on && o.pending < 0 && cap == hipStreamCaptureStatusNone && aligned) {
         if (!o.ev[0]) {
             if ((e = hipEventCreate(&o.ev[0])) != hipSuccess || (e = hipEventCreate(&o.ev[1])) != hipSuccess)
@@ -417,11 +474,15 @@ int run(const Call &c, int forced) {
     if (forced >= 0) {
         if (forced >= (int)configs().size()) return fail(NNJIT_EINVAL, "config id %d out of range", forced);
         const Config &cfg = configs()[forced];
+        if (family_is_q4(cfg.v->family) != c.q4)
+            return fail(NNJIT_EINVAL, "config %d is %s, %s", forced, family_name(cfg.v->family),
+                        c.q4 ? "not a 4-bit GEMV configuration" : "a 4-bit GEMV configuration");
         if (family_dtype(cfg.v->family) != c.dtype)
             return fail(NNJIT_EINVAL, "config %d is %s, not dtype %d", forced, family_name(cfg.v->family), c.dtype);
         if (family_is_gemv(cfg.v->family) && !(c.batch <= 1 && c.M <= 1))
             return fail(NNJIT_EINVAL, "config %d is a GEMV configuration (needs batch == 1, M == 1)", forced);
-        if (cfg.v->vec_bytes == 16 && !is_noop(c) && !vec_aligned(c, family_is_gemv(cfg.v->family)))
+        const bool al = c.q4 ? vec_aligned_q4(c) : vec_aligned(c, family_is_gemv(cfg.v->family));
+        if (cfg.v->vec_bytes == 16 && !is_noop(c) && !al)
             return fail(NNJIT_EINVAL, "config %d needs 16-byte aligned operands", forced);
     }
     if (is_noop(c)) return NNJIT_OK;
@@ -452,7 +513,7 @@ int run(const Call &c, int forced) {
             }
         }
         cfg = &configs()[id];
-        if (cfg->v->vec_bytes == 16 && !vec_aligned(c, kind == NNJIT_KIND_GEMV)) {
+        if (cfg->v->vec_bytes == 16 && !aligned_for(kind, c)) {
             cfg = fallback_config(family_of(kind, c.dtype), c, *d);
             if (!cfg) return fail(NNJIT_ENOCFG, "no element-load fallback configuration");
         }
@@ -477,8 +538,16 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
     t_stats.chosen = -1;
     t_trace.clear();
     const int elt = dtype == NNJIT_F16 ? 2 : 4;
+    const bool q4 = kind == NNJIT_KIND_GEMV_Q4;
     Call c{batch, M, N, K, nullptr, std::max<int64_t>(1, K), M * K, nullptr, std::max<int64_t>(1, N), K * N,
            nullptr, std::max<int64_t>(1, N), M * N, dtype, nullptr};
+    if (q4) {
+        // 4-bit GEMV scratch layout: rows of ceil(N/8) words and N scales,
+        // padded to 16 bytes
+        c.q4 = true;
+        c.ldb = ((N + 7) / 8 + 3) / 4 * 4;
+        c.lds = (N + 7) / 8 * 8;
+    }
     if (dtype != NNJIT_F32 && dtype != NNJIT_F16) return fail(NNJIT_EDTYPE, "unknown dtype %d", dtype);
     if (batch < 1 || M < 1 || N < 1 || K < 0) return fail(NNJIT_EINVAL, "tune needs batch, M, N >= 1 and K >= 0");
     if (M > INT32_MAX || N > INT32_MAX || K > INT32_MAX || batch > INT32_MAX)
@@ -508,11 +577,19 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
     // bandwidth bound and runs on weights streamed from HBM, so it is timed
     // that way: its weight operand rotates over enough copies (>= 512 MiB
     // together) that the 256 MB last-level cache cannot hold them.
-    const size_t a_bytes = (size_t)(batch * M * K) * elt, b_bytes = (size_t)(batch * K * N) * elt;
-    const size_t c_bytes = (size_t)(batch * M * N) * 4;
+    // (4-bit GEMV: x [K] fp16; per copy the code words [K][ldq] followed by
+    // the scales [ceil(K/G)][lds]; y [N])
+    const int64_t q4_groups = q4 ? (K + std::min<int64_t>(batch, std::max<int64_t>(K, 1)) - 1) /
+                                       std::min<int64_t>(batch, std::max<int64_t>(K, 1))
+                                 : 0;
+    const size_t q4_codes = q4 ? (size_t)(K * c.ldb) * 4 : 0;
+    const size_t a_bytes = q4 ? (size_t)K * 2 : (size_t)(batch * M * K) * elt;
+    const size_t b_bytes = q4 ? ((q4_codes + 255) & ~(size_t)255) + (size_t)(q4_groups * c.lds) * 2
+                              : (size_t)(batch * K * N) * elt;
+    const size_t c_bytes = q4 ? (size_t)N * 4 : (size_t)(batch * M * N) * 4;
     auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
     const size_t kColdBytes = (size_t)512 << 20;
-    const int b_copies = kind == NNJIT_KIND_GEMV
+    const int b_copies = (kind == NNJIT_KIND_GEMV || q4)
                              ? (int)std::min<size_t>(16, std::max<size_t>(1, (kColdBytes + up(b_bytes) - 1) / up(b_bytes)))
                              : 1;
     const size_t need = up(a_bytes) + (size_t)b_copies * up(b_bytes) + up(c_bytes);
@@ -534,14 +611,23 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
     c.B = b0;
     c.C = b0 + (size_t)b_copies * up(b_bytes);
     c.stream = d->tune_stream;
-    if ((e = launch_fill_uniform((void *)c.A, batch * M * K, dtype, 1234u, c.stream)) != hipSuccess)
+    if ((e = launch_fill_uniform((void *)c.A, q4 ? K : batch * M * K, dtype, 1234u, c.stream)) != hipSuccess)
         return hip_fail(e, "scratch fill");
-    for (int i = 0; i < b_copies; ++i)
-        if ((e = launch_fill_uniform(b0 + (size_t)i * up(b_bytes), batch * K * N, dtype, 5678u + i, c.stream)) != hipSuccess)
-            return hip_fail(e, "scratch fill");
+    for (int i = 0; i < b_copies; ++i) {
+        char *dst = b0 + (size_t)i * up(b_bytes);
+        // 4-bit codes: any bit pattern is a valid code word, so the words are
+        // filled as fp32 values; the scales follow as fp16
+        e = q4 ? launch_fill_uniform(dst, K * c.ldb, NNJIT_F32, 5678u + i, c.stream)
+               : launch_fill_uniform(dst, batch * K * N, dtype, 5678u + i, c.stream);
+        if (e == hipSuccess && q4)
+            e = launch_fill_uniform(dst + up(q4_codes), q4_groups * c.lds, NNJIT_F16, 9012u + i, c.stream);
+        if (e != hipSuccess) return hip_fail(e, "scratch fill");
+    }
     int rot = 0;
     auto launch_next = [&](const Config &cfg) {   // next weight copy, then launch
-        c.B = b0 + (size_t)(rot++ % b_copies) * up(b_bytes);
+        c.B = b0 + (size_t)(rot % b_copies) * up(b_bytes);
+        if (q4) c.Sc = (const char *)c.B + up(q4_codes);
+        ++rot;
         return launch(*d, cfg, c);
     };
 
@@ -703,6 +789,29 @@ int nnjit_tune_batched(int64_t batch, int64_t M, int64_t N, int64_t K, int dtype
     return tune(NNJIT_KIND_BATCHED, dtype, batch, M, N, K);
 }
 
+int nnjit_gemv_q4(int64_t N, int64_t K, int64_t group, const void *x, const void *Wq, int64_t ldq,
+                  const void *scales, int64_t lds, void *y, void *stream) {
+    t_err.clear();
+    Call c{group, 1, N, K, x, std::max<int64_t>(1, K), 0, Wq, ldq, 0, y, std::max<int64_t>(1, N), 0, NNJIT_F16,
+           (hipStream_t)stream, true, scales, lds};
+    return run(c, -1);
+}
+
+int nnjit_gemv_q4_config(int cfg, int64_t N, int64_t K, int64_t group, const void *x, const void *Wq, int64_t ldq,
+                         const void *scales, int64_t lds, void *y, void *stream) {
+    t_err.clear();
+    if (cfg < 0) return fail(NNJIT_EINVAL, "config id %d out of range", cfg);
+    Call c{group, 1, N, K, x, std::max<int64_t>(1, K), 0, Wq, ldq, 0, y, std::max<int64_t>(1, N), 0, NNJIT_F16,
+           (hipStream_t)stream, true, scales, lds};
+    return run(c, cfg);
+}
+
+int nnjit_tune_gemv_q4(int64_t N, int64_t K, int64_t group) {
+    t_err.clear();
+    if (group < 1 || group > INT32_MAX) return fail(NNJIT_EINVAL, "group=%lld must be in [1, 2^31)", (long long)group);
+    return tune(NNJIT_KIND_GEMV_Q4, NNJIT_F16, group, 1, N, K);
+}
+
 int nnjit_num_configs(void) { return (int)configs().size(); }
 
 int nnjit_config_info(int cfg, char *buf, int64_t len) {
@@ -712,7 +821,7 @@ int nnjit_config_info(int cfg, char *buf, int64_t len) {
     const Variant &v = *c.v;
     char tmp[512];
     int n;
-    if (!family_is_gemv(v.family))
+    if (!family_is_gemv(v.family) && !family_is_q4(v.family))
         n = snprintf(tmp, sizeof tmp,
                      "id=%d family=%s name=%s mfma=%dx%dx%d Mt=%d Nt=%d Kt=%d waves=%dx%d stages=%d prefetch=%d kslices=%d "
                      "vec=%d split=%d threads=%d lds=%d est_regs=%d direct=%d",
@@ -751,8 +860,10 @@ int nnjit_config_resources(int cfg, const nnjit_device_limits *dev, nnjit_resour
 int nnjit_lite_space(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K,
                      const nnjit_device_limits *dev, int *ids, int cap, int *n_enumerated, int64_t *n_naive) {
     t_err.clear();
-    if (kind < NNJIT_KIND_GEMM || kind > NNJIT_KIND_GEMV) return fail(NNJIT_EINVAL, "unknown kind %d", kind);
+    if (kind < NNJIT_KIND_GEMM || kind > NNJIT_KIND_GEMV_Q4) return fail(NNJIT_EINVAL, "unknown kind %d", kind);
     if (dtype != NNJIT_F32 && dtype != NNJIT_F16) return fail(NNJIT_EDTYPE, "unknown dtype %d", dtype);
+    if (kind == NNJIT_KIND_GEMV_Q4 && (dtype != NNJIT_F16 || M != 1))
+        return fail(NNJIT_EINVAL, "a 4-bit GEMV shape is (NNJIT_F16, group, 1, N, K)");
     if (batch < 1 || M < 1 || N < 1 || K < 0 || cap < 0) return fail(NNJIT_EINVAL, "bad shape");
     Shape s{kind, dtype, batch, M, N, K};
     LiteResult lr;
@@ -919,7 +1030,7 @@ int nnjit_cache_load(const char *path) {
                    &split, &us, &used) != 10)
             continue;
         if (strcmp(sig, sig_want) != 0) continue;
-        if (kind < NNJIT_KIND_GEMM || kind > NNJIT_KIND_GEMV || (dtype != NNJIT_F32 && dtype != NNJIT_F16)) continue;
+        if (kind < NNJIT_KIND_GEMM || kind > NNJIT_KIND_GEMV_Q4 || (dtype != NNJIT_F32 && dtype != NNJIT_F16)) continue;
         if (batch < 1 || M < 1 || N < 1 || K < 0) continue;
         const int id = find_id(name, split);
         if (id < 0 || configs()[id].v->family != family_of(kind, dtype)) continue;

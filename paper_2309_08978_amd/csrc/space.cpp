@@ -15,16 +15,20 @@ static const Variant *variant_at(int gi) {
     gi -= kNumGemmF32Variants;
     if (gi < kNumGemmF16Variants) return &kGemmF16Variants[gi];
     gi -= kNumGemmF16Variants;
-    return &kGemvVariants[gi];
+    if (gi < kNumGemvVariants) return &kGemvVariants[gi];
+    gi -= kNumGemvVariants;
+    return &kGemvQ4Variants[gi];
 }
 
-int total_variants() { return kNumGemmF32Variants + kNumGemmF16Variants + kNumGemvVariants; }
+int total_variants() { return kNumGemmF32Variants + kNumGemmF16Variants + kNumGemvVariants + kNumGemvQ4Variants; }
 
 int variant_index(const Variant *v) {
     if (v >= kGemmF32Variants && v < kGemmF32Variants + kNumGemmF32Variants) return (int)(v - kGemmF32Variants);
     if (v >= kGemmF16Variants && v < kGemmF16Variants + kNumGemmF16Variants)
         return kNumGemmF32Variants + (int)(v - kGemmF16Variants);
-    return kNumGemmF32Variants + kNumGemmF16Variants + (int)(v - kGemvVariants);
+    if (v >= kGemvVariants && v < kGemvVariants + kNumGemvVariants)
+        return kNumGemmF32Variants + kNumGemmF16Variants + (int)(v - kGemvVariants);
+    return kNumGemmF32Variants + kNumGemmF16Variants + kNumGemvVariants + (int)(v - kGemvQ4Variants);
 }
 
 const std::vector<int> &gemm_splits() {
@@ -36,9 +40,13 @@ const std::vector<int> &gemv_splits() {
     return s;
 }
 
-int family_dtype(int family) { return (family == FAM_GEMM_F16 || family == FAM_GEMV_F16) ? NNJIT_F16 : NNJIT_F32; }
+int family_dtype(int family) {
+    return (family == FAM_GEMM_F16 || family == FAM_GEMV_F16 || family == FAM_GEMV_Q4) ? NNJIT_F16 : NNJIT_F32;
+}
 bool family_is_gemv(int family) { return family == FAM_GEMV_F32 || family == FAM_GEMV_F16; }
+bool family_is_q4(int family) { return family == FAM_GEMV_Q4; }
 int family_of(int kind, int dtype) {
+    if (kind == NNJIT_KIND_GEMV_Q4) return FAM_GEMV_Q4;
     if (kind == NNJIT_KIND_GEMV) return dtype == NNJIT_F16 ? FAM_GEMV_F16 : FAM_GEMV_F32;
     return dtype == NNJIT_F16 ? FAM_GEMM_F16 : FAM_GEMM_F32;
 }
@@ -48,6 +56,7 @@ const char *family_name(int family) {
     case FAM_GEMM_F16: return "gemm_f16";
     case FAM_GEMV_F32: return "gemv_f32";
     case FAM_GEMV_F16: return "gemv_f16";
+    case FAM_GEMV_Q4: return "gemv_q4";
     default: return "?";
     }
 }
@@ -58,7 +67,8 @@ const std::vector<Config> &configs() {
         const int nv = total_variants();
         for (int gi = 0; gi < nv; ++gi) {
             const Variant *v = variant_at(gi);
-            const std::vector<int> &splits = family_is_gemv(v->family) ? gemv_splits() : gemm_splits();
+            const std::vector<int> &splits =
+                (family_is_gemv(v->family) || family_is_q4(v->family)) ? gemv_splits() : gemm_splits();
             for (int s : splits) out.push_back(Config{(int)out.size(), v, s});
         }
         return out;
@@ -117,6 +127,20 @@ Geometry geometry_of(const Config &c, int64_t batch, int64_t M, int64_t N, int64
     Geometry g;
     const Variant &v = *c.v;
     g.split = c.split;
+    if (family_is_q4(v.family)) {
+        // batch carries the group size; splits cover whole groups
+        const int64_t G = std::max<int64_t>(1, std::min<int64_t>(batch, std::max<int64_t>(K, 1)));
+        const int64_t ngroups = ceil_div(K, G);
+        g.group = G;
+        g.ngroups = ngroups;
+        g.tiles_m = 1;
+        g.tiles_n = (int)ceil_div(std::max<int64_t>(N, 1), v.nt);
+        g.kchunk = (int)std::max<int64_t>(1, ceil_div(ngroups, c.split));
+        g.split = ngroups > 0 ? (int)ceil_div(ngroups, g.kchunk) : 1;
+        g.wgs = (int64_t)g.tiles_n * g.split;
+        g.ws_floats = g.split > 1 ? (int64_t)g.split * std::max<int64_t>(N, 1) : 0;
+        return g;
+    }
     if (!family_is_gemv(v.family)) {
         g.tiles_m = (int)ceil_div(std::max<int64_t>(M, 1), v.mt);
         g.tiles_n = (int)ceil_div(std::max<int64_t>(N, 1), v.nt);
@@ -150,11 +174,14 @@ LiteResult lite_space(const Shape &s, const nnjit_device_limits &d, const std::v
     LiteResult out;
     const int fam = family_of(s.kind, s.dtype);
     const bool gemv = family_is_gemv(fam);
+    const bool q4 = family_is_q4(fam);
     const int V = vec_elems(s.dtype);
-    const bool vec_ok = gemv ? (s.N % V == 0) : (s.K % V == 0 && s.N % V == 0);
+    const bool vec_ok = q4 ? (s.N % 32 == 0) : gemv ? (s.N % V == 0) : (s.K % V == 0 && s.N % V == 0);
 
     // size of the unpruned parameter space over the same axes
-    if (!gemv) {
+    if (q4) {
+        out.n_naive = 3 /*L*/ * 3 /*threads*/ * 3 /*U*/ * (int64_t)gemv_splits().size();
+    } else if (!gemv) {
         const int64_t kt_choices = fam == FAM_GEMM_F32 ? 2 : 1;
         out.n_naive = 2 /*mfma*/ * 5 /*Mt*/ * 5 /*Nt*/ * kt_choices * 3 /*WM*/ * 3 /*WN*/ * 2 /*stages*/ *
                       (int64_t)gemm_splits().size();
@@ -183,10 +210,36 @@ LiteResult lite_space(const Shape &s, const nnjit_device_limits &d, const std::v
         cd.r = r;
         const int64_t waves = ceil_div(std::max<int64_t>(g.wgs, 1), slots);
         cd.eff = (double)g.wgs / (double)(waves * slots);
-        cd.area = (int64_t)v.mt * v.nt * (gemv ? v.kt : 1);
+        cd.area = (int64_t)v.mt * v.nt * ((gemv || q4) ? v.kt : 1);
         cd.split = c.split;
         bool fit = true;
-        if (!gemv) {
+        if (q4) {
+            if (v.nt > std::max<int64_t>(512, pow2ceil(s.N))) fit = false;
+            // items (U row pairs of one group) per split must cover the row slots
+            const int64_t items_per_group = ceil_div((g.group + 1) / 2, v.unroll);
+            const int64_t R = v.threads / v.lanes_seg;
+            auto useful = [&](int split) {
+                if (split <= 1) return true;
+                const Config cs{c.id, c.v, split}, ch{c.id, c.v, split / 2};
+                const Geometry gs = geometry_of(cs, s.batch, s.M, s.N, s.K);
+                if (gs.split == geometry_of(ch, s.batch, s.M, s.N, s.K).split) return false;  // same launch as split / 2
+                return (int64_t)gs.kchunk * items_per_group >= R;
+            };
+            if (c.split > 1) {
+                if (!useful(c.split)) continue;
+                int smax = 1;
+                for (int sp : gemv_splits())
+                    if (useful(sp)) smax = sp;
+                if (g.tiles_n >= d.num_cus) continue;
+                int64_t sfill = 1;
+                while (g.tiles_n * sfill < d.num_cus) sfill <<= 1;
+                if ((c.split < sfill || c.split > 2 * sfill) && c.split != smax) continue;
+                if (g.wgs > 4 * slots) continue;                                  // over-split
+                if (g.wgs < d.num_cus / 2 && c.split != smax) continue;           // under-filled
+                const int64_t wg_here = std::min<int64_t>(r.wg_per_cu, ceil_div(g.wgs, d.num_cus));
+                if (wg_here * v.threads * (int64_t)v.unroll * 32 < 8192 && c.split != smax) continue;
+            }
+        } else if (!gemv) {
             // shape fit: no macro tile wider than the (power-of-two rounded) matrix
             if (v.mt > std::max<int64_t>(16, pow2ceil(s.M)) || v.nt > std::max<int64_t>(16, pow2ceil(s.N))) fit = false;
             const int64_t tiles = s.batch * g.tiles_m * (int64_t)g.tiles_n;

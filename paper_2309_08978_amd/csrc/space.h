@@ -25,7 +25,8 @@ const std::vector<int> &gemm_splits();
 const std::vector<int> &gemv_splits();
 
 int family_dtype(int family);       // NNJIT_F32 / NNJIT_F16
-bool family_is_gemv(int family);
+bool family_is_gemv(int family);    // fp32 / fp16 GEMV (not the 4-bit one)
+bool family_is_q4(int family);      // 4-bit weight-only GEMV
 int family_of(int kind, int dtype);  // family whose kernels run this kind/dtype
 const char *family_name(int family);
 
@@ -46,7 +47,7 @@ constexpr int kMinSurvivors = 8;     // heuristic 7 is relaxed below this many
 struct Shape {
     int kind;
     int dtype;
-    int64_t batch, M, N, K;
+    int64_t batch, M, N, K;   // 4-bit GEMV: batch = group size, M = 1
 };
 
 struct LiteResult {
@@ -67,6 +68,8 @@ struct Geometry {
     int kchunk = 0;
     int64_t wgs = 0;               // workgroups over the whole launch
     int64_t ws_floats = 0;         // split-K partial storage (S x batch x M x N floats)
+    int64_t group = 0, ngroups = 0;  // 4-bit GEMV: group size (clamped to K) and groups;
+                                     // kchunk = groups per split, split = splits launched
 };
 Geometry geometry_of(const Config &c, int64_t batch, int64_t M, int64_t N, int64_t K);
 

@@ -50,6 +50,21 @@ def test_validation_without_gpu(lib):
     assert nj.nnjit_matmul_config(nj.nnjit_num_configs(), 1, 4, 4, 4, 1, 4, 0, 2, 4, 0, 3, 4, 0, 0, None) == nj.NNJIT_EINVAL
     assert nj.nnjit_tune(64, 64, 64, 5) == nj.NNJIT_EDTYPE
     assert nj.nnjit_tune(0, 64, 64, 0) == nj.NNJIT_EINVAL
+    # 4-bit GEMV: (N, K, group, x, Wq, ldq, scales, lds, y, stream)
+    assert nj.nnjit_gemv_q4(64, 64, 0, 1, 2, 8, 3, 64, 4, None) == nj.NNJIT_EINVAL      # group < 1
+    assert nj.nnjit_gemv_q4(64, 64, 32, 1, 2, 7, 3, 64, 4, None) == nj.NNJIT_EINVAL     # ldq < ceil(N/8)
+    assert nj.nnjit_gemv_q4(64, 64, 32, 1, 2, 8, 3, 63, 4, None) == nj.NNJIT_EINVAL     # lds < N
+    assert nj.nnjit_gemv_q4(-1, 64, 32, 1, 2, 8, 3, 64, 4, None) == nj.NNJIT_EINVAL
+    assert nj.nnjit_gemv_q4(64, 64, 32, 1, None, 8, 3, 64, 4, None) == nj.NNJIT_EINVAL
+    assert nj.nnjit_gemv_q4(64, 64, 32, 1, 2, 8, 3, 64, None, None) == nj.NNJIT_EINVAL
+    assert nj.nnjit_gemv_q4(0, 64, 32, 1, 2, 0, 3, 0, None, None) == nj.NNJIT_OK       # N == 0: no-op
+    assert nj.nnjit_tune_gemv_q4(64, 64, 0) == nj.NNJIT_EINVAL
+    cfgs = nj.configs()
+    q4 = next(c["id"] for c in cfgs if c["family"] == "gemv_q4")
+    f16 = next(c["id"] for c in cfgs if c["family"] == "gemm_f16")
+    # a 4-bit configuration is not a MatMul configuration, and the other way round
+    assert nj.nnjit_matmul_config(q4, 1, 4, 8, 8, 1, 8, 0, 2, 8, 0, 3, 8, 0, 1, None) == nj.NNJIT_EINVAL
+    assert nj.nnjit_gemv_q4_config(f16, 64, 64, 32, 1, 2, 8, 3, 64, 4, None) == nj.NNJIT_EINVAL
 
 
 def test_no_gpu_is_ehip_not_abort(lib):
@@ -69,7 +84,7 @@ def test_config_table(lib):
     assert len(cfgs) == nj.nnjit_num_configs() > 100
     assert [c["id"] for c in cfgs] == list(range(len(cfgs)))
     fams = {c["family"] for c in cfgs}
-    assert fams == {"gemm_f32", "gemm_f16", "gemv_f32", "gemv_f16"}
+    assert fams == {"gemm_f32", "gemm_f16", "gemv_f32", "gemv_f16", "gemv_q4"}
     p2 = lambda x: x > 0 and (x & (x - 1)) == 0
     for c in cfgs:
         assert c["vec"] <= 16                     # heuristic 1: at most 128-bit accesses
@@ -105,7 +120,8 @@ def test_resource_limits_follow_the_formula(lib):
 
 
 def _kind(op):
-    return {"gemm": nj.NNJIT_KIND_GEMM, "batched": nj.NNJIT_KIND_BATCHED, "gemv": nj.NNJIT_KIND_GEMV}[op.kind]
+    return {"gemm": nj.NNJIT_KIND_GEMM, "batched": nj.NNJIT_KIND_BATCHED, "gemv": nj.NNJIT_KIND_GEMV,
+            "gemv_q4": nj.NNJIT_KIND_GEMV_Q4}[op.kind]
 
 
 ALL_OPS = [(n, i) for n in workloads.WORKLOADS for i in range(len(workloads.workload(n)))]
@@ -115,12 +131,13 @@ ALL_OPS = [(n, i) for n in workloads.WORKLOADS for i in range(len(workloads.work
 def test_lite_space_is_dozens_and_ordered(lib, name, index):
     op = workloads.workload(name)[index]
     d = nj.mi355x_limits()
-    dt = nj.NNJIT_F16 if op.dtype == "f16" else nj.NNJIT_F32
-    ids, n, n_enum, n_naive = nj.nnjit_lite_space(_kind(op), dt, op.batch, op.M, op.N, op.K, d)
+    dt = nj.NNJIT_F16 if op.dtype in ("f16", "q4") else nj.NNJIT_F32
+    batch = op.group if op.kind == "gemv_q4" else op.batch   # a 4-bit GEMV is keyed by its group size
+    ids, n, n_enum, n_naive = nj.nnjit_lite_space(_kind(op), dt, batch, op.M, op.N, op.K, d)
     assert 8 <= n <= 100, n            # "dozens", never empty
-    assert n_naive > (10 * n if op.kind != "gemv" else 2 * n)
+    assert n_naive > (10 * n if op.kind in ("gemm", "batched") else 2 * n)
     cfgs = nj.configs()
-    fam = ("gemv_" if op.kind == "gemv" else "gemm_") + op.dtype
+    fam = "gemv_q4" if op.kind == "gemv_q4" else ("gemv_" if op.kind == "gemv" else "gemm_") + op.dtype
     prev = {}
     for i in ids:
         c = cfgs[i]
@@ -132,10 +149,10 @@ def test_lite_space_is_dozens_and_ordered(lib, name, index):
         if kind in prev:
             assert r["wg_per_cu"] <= prev[kind]          # evaluated from max to min Block_core, per kind
         prev[kind] = r["wg_per_cu"]
-        if op.kind != "gemv":
+        if op.kind in ("gemm", "batched"):
             assert c["Mt"] <= max(16, 1 << (op.M - 1).bit_length())
     # deterministic
-    assert nj.nnjit_lite_space(_kind(op), dt, op.batch, op.M, op.N, op.K, d)[0] == ids
+    assert nj.nnjit_lite_space(_kind(op), dt, batch, op.M, op.N, op.K, d)[0] == ids
 
 
 def test_heuristic7_prefers_register_bound(lib):
@@ -185,3 +202,39 @@ def test_microbench_groups_vary_one_primitive(lib):
                 rest = {k: v for k, v in c.items() if k not in DERIVED and k != prim}
                 assert rest == {k: v for k, v in grp[0].items() if k not in DERIVED and k != prim}
     assert total >= 10
+
+
+@pytest.mark.parametrize("N,K,G", [(4096, 4096, 128), (12288, 4096, 128), (4096, 11008, 128), (32000, 4096, 128),
+                                   (4096, 4096, 32), (4096, 4096, 1), (4096, 300, 7), (520, 300, 64)])
+def test_q4_lite_space(lib, N, K, G):
+    """4-bit GEMV lite space: only its own family; 16-byte configurations
+    exactly when N % 32 == 0; every split launches a distinct number of
+    splits, each with a work item for every row slot (except the one
+    unsplit fallback); evaluation order by workgroups per CU."""
+    d = nj.mi355x_limits()
+    ids, n, n_enum, n_naive = nj.nnjit_lite_space(nj.NNJIT_KIND_GEMV_Q4, nj.NNJIT_F16, G, 1, N, K, d)
+    assert 1 <= n <= 96 and n_naive > n
+    cfgs = nj.configs()
+    ngroups = -(-K // min(G, K))
+    items_per_group = lambda u: -(-(-(-min(G, K) // 2)) // u)
+    seen, prev = set(), None
+    for i in ids:
+        c = cfgs[i]
+        assert c["family"] == "gemv_q4"
+        assert (c["vec"] == 16) == (N % 32 == 0)
+        gchunk = -(-ngroups // c["split"])
+        launched = -(-ngroups // gchunk)
+        if c["split"] > 1:
+            half = -(-ngroups // -(-ngroups // (c["split"] // 2)))
+            assert launched != half, c
+            assert gchunk * items_per_group(c["unroll"]) >= c["threads"] // c["lanes_per_seg"], c
+        key = (c["name"], launched)
+        assert key not in seen
+        seen.add(key)
+        r = nj.nnjit_config_resources(i, d)
+        if prev is not None:
+            assert r["wg_per_cu"] <= prev
+        prev = r["wg_per_cu"]
+    assert nj.nnjit_lite_space(nj.NNJIT_KIND_GEMV_Q4, nj.NNJIT_F16, G, 1, N, K, d)[0] == ids
+    with pytest.raises(nj.NnjitError):
+        nj.nnjit_lite_space(nj.NNJIT_KIND_GEMV_Q4, nj.NNJIT_F32, G, 1, N, K, d)

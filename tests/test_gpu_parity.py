@@ -119,7 +119,8 @@ def _sample_idx(rng, shape, n=1500):
 
 FULL_ORACLE_FLOPS = 1.5e9
 
-WL_OPS = [(name, i) for name in workloads.WORKLOADS for i in range(len(workloads.workload(name)))]
+WL_OPS = [(name, i) for name in workloads.WORKLOADS for i in range(len(workloads.workload(name)))
+          if workloads.workload(name)[i].dtype != workloads.Q4]   # 4-bit GEMV: tests/test_gpu_q4.py
 
 
 @pytest.mark.parametrize("name,index", WL_OPS, ids=[f"{n}-{workloads.workload(n)[i].name}" for n, i in WL_OPS])

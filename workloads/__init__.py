@@ -23,6 +23,15 @@ in for real weights and activations):
                product of such matrices is an integer below 2^24, so any
                summation order gives the same fp32 result
 
+4-bit weight-only GEMV (dtype ``q4``; the paper's Llama-2-7B decode runs on
+4-bit weights, Sec. 7, without giving the format): x fp16 [K]; the weight
+codes are 32-bit words [K][ldq], eight 4-bit codes per word along N, drawn
+as uniformly random words (every code uniform in 0..15); one fp16 scale per
+group of ``group`` rows and column, uniform in [0.002, 0.01) -- the size of
+max|w| / 7 over a 128-row group of N(0, 0.02) weights.  The exact-arithmetic
+recipe (``q4_int``) takes x in {-8..8} and scales in {1/2, 1, 2, 4}: every
+partial sum is then a multiple of 1/2 below 2^23, exact in fp32.
+
 fp16 inputs are drawn in fp32 and rounded once, round-to-nearest-even
 (numpy ``astype(float16)``); the GPU and the oracle consume the same bits.
 """
@@ -35,6 +44,7 @@ import numpy as np
 
 F32 = "f32"
 F16 = "f16"
+Q4 = "q4"
 _NP = {F32: np.float32, F16: np.float16}
 
 
@@ -50,9 +60,12 @@ class Op:
     a_dist: str = "act"
     b_dist: str = "w"
     dtype: str = F32
+    group: int = 0          # q4: rows per scale group
 
     @property
     def kind(self) -> str:
+        if self.dtype == Q4:
+            return "gemv_q4"
         if self.batch > 1:
             return "batched"
         return "gemv" if self.M == 1 else "gemm"
@@ -66,8 +79,17 @@ class Op:
         return 2 if self.dtype == F16 else 4
 
     @property
+    def weight_bytes(self) -> int:
+        """Bytes of the B operand (q4: code words plus scales)."""
+        if self.dtype == Q4:
+            return self.K * (-(-self.N // 8)) * 4 + (-(-self.K // self.group)) * self.N * 2
+        return self.batch * self.K * self.N * self.elt
+
+    @property
     def bytes(self) -> int:
         """Compulsory HBM bytes: read A and B once, write fp32 C once."""
+        if self.dtype == Q4:
+            return self.K * 2 + self.weight_bytes + self.N * 4
         return self.batch * ((self.M * self.K + self.K * self.N) * self.elt + self.M * self.N * 4)
 
     def with_dtype(self, dtype: str) -> "Op":
@@ -112,6 +134,10 @@ def _llama_prefill(dtype: str) -> List[Op]:
     return [dataclasses.replace(op, dtype=dtype) for op in ops]
 
 
+def _llama_decode_q4(group: int) -> List[Op]:
+    return [dataclasses.replace(op, dtype=Q4, group=group) for op in _linears("llama.decode", 1, _LLAMA_LIN)]
+
+
 def _paper_kernels() -> List[Op]:
     # Table 3 of the paper: K0 RoBERTa, K1 GPT-2 MatMuls; K2 BART, K3 GPT-2 BatchMatMuls
     return [Op("K0", 384, 768, 768), Op("K1", 640, 768, 3072),
@@ -127,6 +153,7 @@ WORKLOADS: Dict[str, Tuple[int, List[Op]]] = {
     "t5_large_layer_b4s256_f32": (2, _t5_large_b4s256()),
     "llama2_7b_decode_f32": (3, _llama_decode(F32)),
     "llama2_7b_decode_f16": (3, _llama_decode(F16)),
+    "llama2_7b_decode_q4": (3, _llama_decode_q4(128)),
     "llama2_7b_prefill512_f32": (4, _llama_prefill(F32)),
     "llama2_7b_prefill512_f16": (4, _llama_prefill(F16)),
     "paper_table3_f32": (5, _paper_kernels()),
@@ -168,10 +195,13 @@ def _shape(batch: int, rows: int, cols: int) -> Tuple[int, ...]:
     return (batch, rows, cols) if batch > 1 else (rows, cols)
 
 
-def op_inputs(name: str, op_index: int) -> Tuple[np.ndarray, np.ndarray]:
+def op_inputs(name: str, op_index: int) -> Tuple[np.ndarray, ...]:
     """(A, B) for op ``op_index`` of workload ``name``: contiguous row-major
-    arrays in the op's dtype. A is [batch,]M x K, B is [batch,]K x N."""
+    arrays in the op's dtype. A is [batch,]M x K, B is [batch,]K x N.
+    A q4 op gives (x, Wq, scales) as ``q4_operands`` does."""
     op = workload(name)[op_index]
+    if op.dtype == Q4:
+        return q4_operands(_rng_for(name, op_index, 0), op.K, op.N, op.group)
     if WORKLOADS[name][0] == 0:
         # the single 64x768x768 product: one generator seeded 0, A drawn first, then B
         rng = np.random.default_rng(0)
@@ -199,3 +229,30 @@ def small_int_operands(seed, batch: int, M: int, K: int, N: int,
                        dtype: str = F32) -> Tuple[np.ndarray, np.ndarray]:
     """Entries uniform in {-8..8}: all partial sums are exact in fp32."""
     return random_operands(seed, batch, M, K, N, dtype, a_dist="int8", b_dist="int8")
+
+
+def q4_operands(seed, K: int, N: int, group: int, ldq: int | None = None, lds: int | None = None,
+                recipe: str = "q4") -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """(x fp16 [K], Wq uint32 [K, ldq], scales fp16 [ceil(K / group), lds])
+    for a 4-bit weight-only GEMV, from ``default_rng(seed)`` (or a Generator):
+    x first, then the code words, then the scales.  ``ldq`` defaults to
+    ceil(N / 8) and ``lds`` to N; padding words and scales are random too.
+    recipe ``q4``: x N(0, 1), scales uniform [0.002, 0.01); ``q4_int``: x in
+    {-8..8}, scales in {1/2, 1, 2, 4} (every partial sum is exact in fp32
+    for K below 2^16)."""
+    rng = seed if isinstance(seed, np.random.Generator) else np.random.default_rng(seed)
+    ldq = -(-N // 8) if ldq is None else ldq
+    lds = N if lds is None else lds
+    ngroups = -(-K // group) if K > 0 else 0
+    if recipe == "q4":
+        x = rng.standard_normal(K, dtype=np.float32).astype(np.float16)
+    elif recipe == "q4_int":
+        x = rng.integers(-8, 9, size=K).astype(np.float16)
+    else:
+        raise ValueError(f"unknown q4 recipe {recipe!r}")
+    Wq = rng.integers(0, 1 << 32, size=(K, ldq), dtype=np.uint32)
+    if recipe == "q4":
+        S = (rng.random((ngroups, lds), dtype=np.float32) * np.float32(0.008) + np.float32(0.002)).astype(np.float16)
+    else:
+        S = rng.choice(np.array([0.5, 1.0, 2.0, 4.0], dtype=np.float16), size=(ngroups, lds))
+    return np.ascontiguousarray(x), np.ascontiguousarray(Wq), np.ascontiguousarray(S)
