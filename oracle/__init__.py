@@ -117,14 +117,17 @@ class Oracle:
     def gemv_q4(self, x: np.ndarray, Wq: np.ndarray, S: np.ndarray, group: int, N: int,
                 nthreads: int = 0) -> np.ndarray:
         """fp64 y[N] = x[K] . W for the 4-bit weight format of oracle.c:
-        x float16 [K], Wq uint32 [K, ldq] (eight codes per word along N),
-        S float16 [ceil(K/group), lds]."""
+        x float16 [K], Wq uint32 [N, ldq] (eight codes per word along K),
+        S float16 [N, lds] (one scale per output and group of ``group``
+        inputs)."""
         x = np.ascontiguousarray(x, dtype=np.float16)
         Wq = np.ascontiguousarray(Wq, dtype=np.uint32)
         S = np.ascontiguousarray(S, dtype=np.float16)
         K = x.shape[0]
-        if Wq.shape[0] != K or S.shape[0] < (K + group - 1) // group:
+        if Wq.ndim != 2 or S.ndim != 2 or Wq.shape[0] < N or S.shape[0] < N:
             raise ValueError("shape mismatch")
+        if Wq.shape[1] < (K + 7) // 8 or S.shape[1] < (K + group - 1) // group:
+            raise ValueError("rows too short for K")
         y = np.empty(N, dtype=np.float64)
         rc = self.lib.oracle_gemv_q4(K, N, x.ctypes.data, Wq.ctypes.data, Wq.shape[1], S.ctypes.data,
                                      S.shape[1], int(group), y.ctypes.data, int(nthreads))

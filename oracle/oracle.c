@@ -125,14 +125,16 @@ double oracle_element(int64_t K, const void *A, int64_t a_off, const void *B,
 }
 
 /* Weight-only 4-bit GEMV (the paper runs Llama-2 decode with 4-bit weights,
- * Sec. 7, without giving the format; this is the format the library reads):
+ * Sec. 7, without giving the format; this is the format the library reads,
+ * the layout of a linear layer's weight: one row per output feature n,
+ * quantised along the input features k in groups of G):
  *
- *     y[n] = sum_{k=0}^{K-1} x[k] * W[k][n],   W[k][n] = (q[k][n] - 8) * s[k / G][n]
+ *     y[n] = sum_{k=0}^{K-1} x[k] * W[k][n],   W[k][n] = (q[n][k] - 8) * s[n][k / G]
  *
- * q[k][n] is an unsigned 4-bit code, eight per 32-bit word along n: column n
- * of row k is bits 4 (n % 8) .. 4 (n % 8) + 3 of word n / 8 of that row (ldq
- * words per row); s is a binary16 scale per group of G consecutive rows and
- * per column (lds halves per group row); x is binary16.  Every weight and
+ * q[n][k] is an unsigned 4-bit code, eight per 32-bit word along k: input k
+ * of output n is bits 4 (k % 8) .. 4 (k % 8) + 3 of word k / 8 of row n (ldq
+ * words per row); s is a binary16 scale per output and group of G
+ * consecutive inputs (lds halves per row); x is binary16.  Every weight and
  * every product x[k] W[k][n] is exact in fp64 (at most 11 + 15 significand
  * bits), so, as in oracle_matmul, only the k-ascending additions round. */
 int oracle_gemv_q4(int64_t K, int64_t N, const uint16_t *x, const uint32_t *Wq, int64_t ldq,
@@ -140,31 +142,23 @@ int oracle_gemv_q4(int64_t K, int64_t N, const uint16_t *x, const uint32_t *Wq, 
 {
     if (K < 0 || N < 0 || G < 1)
         return -1;
-    if (N == 0)
-        return 0;
-    if (ldq < (N + 7) / 8 || lds < N)
+    if (ldq < (K + 7) / 8 || lds < (K + G - 1) / G)
         return -1;
-    const int64_t ntasks = (N + COLS_PER_TASK - 1) / COLS_PER_TASK;
 #ifdef _OPENMP
     if (nthreads <= 0)
         nthreads = omp_get_max_threads();
-#pragma omp parallel for schedule(dynamic, 1) num_threads(nthreads)
+#pragma omp parallel for schedule(dynamic, 64) num_threads(nthreads)
 #endif
-    for (int64_t t = 0; t < ntasks; ++t) {
-        const int64_t j0 = t * COLS_PER_TASK;
-        const int64_t j1 = (j0 + COLS_PER_TASK < N) ? j0 + COLS_PER_TASK : N;
-        for (int64_t j = j0; j < j1; ++j)
-            y[j] = 0.0;
+    for (int64_t n = 0; n < N; ++n) {
+        const uint32_t *row = Wq + n * ldq;
+        const uint16_t *srow = S + n * lds;
+        double acc = 0.0;
         for (int64_t k = 0; k < K; ++k) {
-            const double xv = oracle_f16_to_f64(x[k]);
-            const uint32_t *row = Wq + k * ldq;
-            const uint16_t *srow = S + (k / G) * lds;
-            for (int64_t j = j0; j < j1; ++j) {
-                const int q = (int)((row[j / 8] >> (4 * (j % 8))) & 15u);
-                const double w = ((double)q - 8.0) * oracle_f16_to_f64(srow[j]);
-                y[j] += xv * w;
-            }
+            const int q = (int)((row[k / 8] >> (4 * (k % 8))) & 15u);
+            const double w = ((double)q - 8.0) * oracle_f16_to_f64(srow[k / G]);
+            acc += oracle_f16_to_f64(x[k]) * w;
         }
+        y[n] = acc;
     }
     (void)nthreads;
     return 0;

@@ -154,13 +154,13 @@ def pin_f16_decode(o):
 
 
 def _q4_pack(codes):
-    """uint32 words from integer codes [K, N] (N a multiple of 8), column n in
-    bits 4 (n % 8) .. of word n / 8 -- written independently of the oracle."""
+    """uint32 words [N, ceil(K / 8)] from integer codes [N, K]: input k of row n
+    in bits 4 (k % 8) .. of word k / 8 -- written independently of the oracle."""
     codes = np.asarray(codes, dtype=np.uint32)
-    K, N = codes.shape
-    words = np.zeros((K, N // 8), dtype=np.uint32)
-    for n in range(N):
-        words[:, n // 8] |= codes[:, n] << np.uint32(4 * (n % 8))
+    N, K = codes.shape
+    words = np.zeros((N, (K + 7) // 8), dtype=np.uint32)
+    for k in range(K):
+        words[:, k // 8] |= codes[:, k] << np.uint32(4 * (k % 8))
     return words
 
 
@@ -176,47 +176,47 @@ def pin_q4_golden(o):
 def pin_q4_zero_code(o):
     """Every code 8 encodes weight 0: y = 0 exactly for any x and scales."""
     rng = np.random.default_rng(31)
-    K, N, G = 37, 24, 8
+    N, K, G = 24, 37, 8
     x = rng.standard_normal(K).astype(np.float16)
-    S = rng.standard_normal(((K + G - 1) // G, N)).astype(np.float16)
-    y = o.gemv_q4(x, _q4_pack(np.full((K, N), 8)), S, G, N)
+    S = rng.standard_normal((N, (K + G - 1) // G)).astype(np.float16)
+    y = o.gemv_q4(x, _q4_pack(np.full((N, K), 8)), S, G, N)
     assert np.array_equal(y, np.zeros(N))
 
 
 def pin_q4_one_hot(o):
-    """A single non-zero weight: y[n0] = x[k0] (q - 8) s[k0 / G][n0], exact;
+    """A single non-zero weight: y[n0] = x[k0] (q - 8) s[n0][k0 / G], exact;
     every other output 0."""
-    K, N, G = 20, 16, 6
+    N, K, G = 16, 20, 6
     rng = np.random.default_rng(32)
     x = rng.standard_normal(K).astype(np.float16)
-    S = rng.standard_normal(((K + G - 1) // G, N)).astype(np.float16)
+    S = rng.standard_normal((N, (K + G - 1) // G)).astype(np.float16)
     for k0, n0, q in [(0, 0, 15), (13, 9, 0), (19, 15, 3)]:
-        codes = np.full((K, N), 8)
-        codes[k0, n0] = q
+        codes = np.full((N, K), 8)
+        codes[n0, k0] = q
         y = o.gemv_q4(x, _q4_pack(codes), S, G, N)
         want = np.zeros(N)
-        want[n0] = float(x[k0]) * (q - 8) * float(S[k0 // G, n0])
+        want[n0] = float(x[k0]) * (q - 8) * float(S[n0, k0 // G])
         assert np.array_equal(y, want), (k0, n0, q)
 
 
 def pin_q4_integers(o):
-    """Integer x and unit scales: the exact int64 product of x and (q - 8)."""
+    """Integer x and unit scales: the exact int64 product of (q - 8) and x."""
     rng = np.random.default_rng(33)
-    K, N, G = 130, 40, 32
+    N, K, G = 40, 130, 32
     x = rng.integers(-8, 9, K)
-    codes = rng.integers(0, 16, (K, N))
-    y = o.gemv_q4(x.astype(np.float16), _q4_pack(codes), np.ones(((K + G - 1) // G, N), np.float16), G, N)
-    assert np.array_equal(y, (x.astype(np.int64) @ (codes.astype(np.int64) - 8)).astype(np.float64))
+    codes = rng.integers(0, 16, (N, K))
+    y = o.gemv_q4(x.astype(np.float16), _q4_pack(codes), np.ones((N, (K + G - 1) // G), np.float16), G, N)
+    assert np.array_equal(y, ((codes.astype(np.int64) - 8) @ x.astype(np.int64)).astype(np.float64))
 
 
 def pin_q4_numpy(o):
     """Random codes and scales vs numpy: unpack, dequantise, float64 matmul."""
     rng = np.random.default_rng(34)
-    K, N, G = 300, 64, 128
+    N, K, G = 64, 300, 128
     x = rng.standard_normal(K).astype(np.float16)
-    codes = rng.integers(0, 16, (K, N))
-    S = (rng.standard_normal(((K + G - 1) // G, N)) * 0.01).astype(np.float16)
-    W = (codes - 8).astype(np.float64) * S.astype(np.float64)[np.arange(K) // G]
+    codes = rng.integers(0, 16, (N, K))
+    S = (rng.standard_normal((N, (K + G - 1) // G)) * 0.01).astype(np.float16)
+    W = ((codes - 8).astype(np.float64) * S.astype(np.float64)[:, np.arange(K) // G]).T   # W[k][n]
     ref = x.astype(np.float64) @ W
     y = o.gemv_q4(x, _q4_pack(codes), S, G, N)
     bound = 1e-13 * (np.abs(x.astype(np.float64)) @ np.abs(W))
@@ -301,11 +301,11 @@ MUTANTS = {
     "f16_subnormal_scale": ("(double)f / 1024.0 / 16384.0", "(double)f / 1024.0 / 32768.0"),
     "skip_batch_stride": ("const double a = load_elt(A, b * strideA", "const double a = load_elt(A, 0 * strideA"),
     "not_zeroed": ("r[j] = 0.0;", "r[j] = r[j] * 1.0 + 1.0;"),
-    "q4_nibble_order": ("(row[j / 8] >> (4 * (j % 8)))", "(row[j / 8] >> (4 * (7 - j % 8)))"),
+    "q4_nibble_order": ("(row[k / 8] >> (4 * (k % 8)))", "(row[k / 8] >> (4 * (7 - k % 8)))"),
     "q4_zero_point": ("((double)q - 8.0)", "((double)q - 7.0)"),
-    "q4_group_index": ("S + (k / G) * lds", "S + (((k / G) + 1) % ((K + G - 1) / G)) * lds"),
-    "q4_wrong_row": ("Wq + k * ldq", "Wq + ((k + 1) % K) * ldq"),
-    "q4_scale_column": ("oracle_f16_to_f64(srow[j])", "oracle_f16_to_f64(srow[(j + 1) % N])"),
+    "q4_group_index": ("srow[k / G]", "srow[(k / G + 1) % ((K + G - 1) / G)]"),
+    "q4_wrong_row": ("Wq + n * ldq", "Wq + ((n + 1) % N) * ldq"),
+    "q4_scale_row": ("S + n * lds", "S + ((n + 1) % N) * lds"),
 }
 
 
