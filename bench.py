@@ -43,11 +43,26 @@ def log(*a):
 
 
 def _kind(op):
-    return {"gemm": nj.NNJIT_KIND_GEMM, "batched": nj.NNJIT_KIND_BATCHED, "gemv": nj.NNJIT_KIND_GEMV}[op.kind]
+    return {"gemm": nj.NNJIT_KIND_GEMM, "batched": nj.NNJIT_KIND_BATCHED, "gemv": nj.NNJIT_KIND_GEMV,
+            "gemv_q4": nj.NNJIT_KIND_GEMV_Q4}[op.kind]
 
 
 def _dt(op):
-    return nj.NNJIT_F16 if op.dtype == "f16" else nj.NNJIT_F32
+    return nj.NNJIT_F16 if op.dtype in ("f16", "q4") else nj.NNJIT_F32
+
+
+def _key(op):
+    """(kind, dtype, batch, M, N, K) of a product in the tuned cache (a 4-bit
+    GEMV is keyed by its group size in the batch position)."""
+    return (_kind(op), _dt(op), op.group if op.dtype == "q4" else op.batch, op.M, op.N, op.K)
+
+
+def _tune(op):
+    if op.dtype == "q4":
+        return nj.nnjit_tune_gemv_q4(op.N, op.K, op.group)
+    if op.batch > 1:
+        return nj.nnjit_tune_batched(op.batch, op.M, op.N, op.K, _dt(op))
+    return nj.nnjit_tune(op.M, op.N, op.K, _dt(op))
 
 
 class OpRun:
@@ -55,14 +70,19 @@ class OpRun:
 
     def __init__(self, name, index, copies):
         import torch
-        self.op = workloads.workload(name)[index]
-        A, B = workloads.op_inputs(name, index)
-        self.A = torch.from_numpy(A).to("cuda:0")
-        B0 = torch.from_numpy(B).to("cuda:0")
+        self.op = op = workloads.workload(name)[index]
+        ins = workloads.op_inputs(name, index)
+        self.A = torch.from_numpy(ins[0]).to("cuda:0")
+        if op.dtype == "q4":
+            # the weight operand is (code words, scales)
+            w0 = (torch.from_numpy(ins[1].view(np.int32)).to("cuda:0"), torch.from_numpy(ins[2]).to("cuda:0"))
+            clone = lambda w: (w[0].clone(), w[1].clone())
+        else:
+            w0 = torch.from_numpy(ins[1]).to("cuda:0")
+            clone = lambda w: w.clone()
         # the weight operand is rotated over `copies` replicas (cold HBM protocol)
-        self.Bs = [B0] + [B0.clone() for _ in range(copies - 1)]
-        op = self.op
-        shape = (op.batch, op.M, op.N) if op.batch > 1 else (op.M, op.N)
+        self.Bs = [w0] + [clone(w0) for _ in range(copies - 1)]
+        shape = (op.batch, op.M, op.N) if op.batch > 1 else ((op.N,) if op.dtype == "q4" else (op.M, op.N))
         self.C = torch.empty(shape, dtype=torch.float32, device="cuda:0")
 
     def call(self, copy=0, stream=None):
@@ -71,7 +91,10 @@ class OpRun:
             stream = torch.cuda.current_stream()  # the capture stream while a graph is recorded
         op = self.op
         B = self.Bs[copy % len(self.Bs)]
-        if op.batch > 1:
+        if op.dtype == "q4":
+            Wq, S = B
+            rc = nj.nnjit_gemv_q4(op.N, op.K, op.group, self.A, Wq, Wq.shape[1], S, S.shape[1], self.C, stream)
+        elif op.batch > 1:
             rc = nj.nnjit_batched_matmul(op.batch, op.M, op.N, op.K, self.A, op.K, op.M * op.K, B, op.N,
                                          op.K * op.N, self.C, op.N, op.M * op.N, _dt(op), stream)
         else:
@@ -83,7 +106,7 @@ class OpRun:
 def roofline_of(op, us):
     dt = op.dtype
     ai = op.flops / op.bytes
-    if ai >= RIDGE[dt]:
+    if dt != "q4" and ai >= RIDGE[dt]:   # the 4-bit GEMV runs no MFMA: HBM is its roofline
         achieved = op.flops / (us * 1e-6) / 1e12
         return {"bound": "mfma", "achieved": achieved, "peak": PEAK_TFLOPS[dt], "unit": "TFLOP/s",
                 "frac": achieved / PEAK_TFLOPS[dt], "traffic": None}
@@ -128,8 +151,7 @@ def online_curve(runs, nsteps):
             torch.cuda.synchronize()
             ms.append(round(a.elapsed_time(b), 5))
             if tuned_at is None:
-                states = [nj.nnjit_online_status(_kind(r.op), _dt(r.op), r.op.batch, r.op.M, r.op.N, r.op.K)["state"]
-                          for r in runs]
+                states = [nj.nnjit_online_status(*_key(r.op))["state"] for r in runs]
                 if all(st == "tuned" for st in states):
                     tuned_at = k + 1
     finally:
@@ -147,14 +169,17 @@ def cpu_baseline(name, budget_s: float):
     for i, op in enumerate(ops):
         if op.flops > 5e9:
             continue  # larger products are left out of the CPU sample
-        inputs.append(workloads.op_inputs(name, i))
+        inputs.append((op, workloads.op_inputs(name, i)))
         flops += op.flops
     oracle.default()
     t0 = time.perf_counter()
     steps = 0
     while True:
-        for A, B in inputs:
-            oracle.matmul(A, B)
+        for op, ins in inputs:
+            if op.dtype == "q4":
+                oracle.gemv_q4(*ins, op.group, op.N)
+            else:
+                oracle.matmul(*ins)
         steps += 1
         if time.perf_counter() - t0 >= budget_s or steps >= 50:
             break
@@ -162,7 +187,7 @@ def cpu_baseline(name, budget_s: float):
     n_ops = len(inputs)
     return {"value": flops * steps / dt / 1e9, "unit": "GFLOP/s", "cores": oracle.max_threads(), "kind": "oracle",
             "sample": f"{steps} full step(s) of {n_ops}/{len(ops)} products ({flops / 1e9:.3f} GFLOP each step), "
-                      f"fp64 triple loop, {dt:.1f} s"}
+                      f"fp64 {'dequantise-and-sum loop' if ops[0].dtype == 'q4' else 'triple loop'}, {dt:.1f} s"}
 
 
 def main(argv=None):
@@ -205,8 +230,8 @@ def main(argv=None):
     ops = workloads.workload(name)
     log(f"[bench] workload {name}: {len(ops)} products")
 
-    weight_bytes = sum(op.batch * op.K * op.N * op.elt for op in ops)
-    cold = all(op.kind == "gemv" for op in ops)
+    weight_bytes = sum(op.weight_bytes for op in ops)
+    cold = all(op.kind in ("gemv", "gemv_q4") for op in ops)
     copies = max(1, math.ceil(COLD_BYTES / weight_bytes)) if cold else 1
     runs = [OpRun(name, i, copies) for i in range(len(ops))]
     torch.cuda.synchronize()
@@ -220,10 +245,7 @@ def main(argv=None):
     for r in runs:
         op = r.op
         t0 = time.perf_counter()
-        if op.batch > 1:
-            cfg = nj.check(nj.nnjit_tune_batched(op.batch, op.M, op.N, op.K, _dt(op)))
-        else:
-            cfg = nj.check(nj.nnjit_tune(op.M, op.N, op.K, _dt(op)))
+        cfg = nj.check(_tune(op))
         host_ms = (time.perf_counter() - t0) * 1e3
         st = nj.nnjit_last_tune_stats()
         info = nj.nnjit_config_info(cfg)
@@ -378,7 +400,9 @@ def main(argv=None):
         per_op.append({"op": op.name, "shape_MKN": [op.M, op.K, op.N], "batch": op.batch, "dtype": op.dtype,
                        "us_per_launch": round(us, 3), "us_per_launch_eager": round(eus, 3),
                        "us_single_launch": round(single, 3),
-                       "gflops": round(op.flops / us / 1e3, 1), "pct_mfma_peak": round(100 * op.flops / us / 1e6 / PEAK_TFLOPS[op.dtype], 2),
+                       "gflops": round(op.flops / us / 1e3, 1),
+                       "pct_mfma_peak": (round(100 * op.flops / us / 1e6 / PEAK_TFLOPS[op.dtype], 2)
+                                         if op.dtype in PEAK_TFLOPS else None),
                        "gbs": round(op.bytes / us / 1e3, 1), "pct_hbm": round(100 * op.bytes / us / 1e3 / PEAK_HBM_GBS, 2),
                        "bound": rl["bound"], "pct_roofline": round(100 * rl["frac"], 2)})
     dom = max(range(len(runs)), key=lambda i: per_op[i]["us_per_launch"])
@@ -387,6 +411,8 @@ def main(argv=None):
     dop = runs[dom].op
     if cfg_fields["family"].startswith("gemm"):
         wgs = -(-dop.M // int(cfg_fields["Mt"])) * -(-dop.N // int(cfg_fields["Nt"])) * int(cfg_fields["split"])
+    elif dop.dtype == "q4":
+        wgs = -(-dop.N // int(cfg_fields["rows_per_wg"]))
     else:
         wgs = -(-dop.N // int(cfg_fields["cols"])) * int(cfg_fields["split"])
     rl["traffic"] = measured_traffic(args.traffic_db, name, dop.name, tunes[dom]["config"])
@@ -405,7 +431,7 @@ def main(argv=None):
         "config": {"workload": name, "products": [[op.name, op.batch, op.M, op.K, op.N] for op in ops],
                    "timing": "graph replay" if graph is not None else "eager ABI calls",
                    "weight_replicas": copies, "steps_per_graph": per_graph if graph is not None else None},
-        "pct_mfma_peak": round(100 * value / 1e3 / PEAK_TFLOPS[dt], 2),
+        "pct_mfma_peak": round(100 * value / 1e3 / PEAK_TFLOPS[dt], 2) if dt in PEAK_TFLOPS else None,
         "gbs": round(total_bytes / (ms_per_step * 1e-3) / 1e9, 1),
         "eager_ms_per_step": round(eager_ms, 5),
         "wall_s": round(wall, 4),

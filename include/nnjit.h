@@ -126,23 +126,23 @@ int nnjit_matmul_config(int cfg, int64_t batch, int64_t M, int64_t N, int64_t K,
 
 /* y = x . W for a 4-bit weight-only quantised W (the 4-bit Llama-2-7B
  * decode workload of Sec. 7, whose quantisation format the paper does not
- * give; this library reads it as symmetric 4-bit codes with one fp16 scale
- * per group of `group` consecutive rows and column):
- *     W[k][n] = (q[k][n] - 8) * scales[(k / group) * lds + n]
- *     q[k][n] = (Wq[k * ldq + n / 8] >> (4 * (n % 8))) & 15
+ * give; this library reads it as a linear layer's weight: one row per output
+ * n, symmetric 4-bit codes with one fp16 scale per output and group of
+ * `group` consecutive inputs):
+ *     W[k][n] = (q[n][k] - 8) * scales[n * lds + k / group]
+ *     q[n][k] = (Wq[n * ldq + k / 8] >> (4 * (k % 8))) & 15
  *     y[n]    = sum_k x[k] * W[k][n],   0 <= n < N,  0 <= k < K
- * x: IEEE binary16 [K]; Wq: uint32 words, K rows of ldq words, eight codes
- * per word along n, low nibble first; scales: binary16, ceil(K / group)
- * rows of lds; y: fp32 [N], overwritten.  Products and sums in fp32 (each
- * group's codes summed, then multiplied by its scale); the order of the
- * additions is fixed, so results are deterministic.
- * Preconditions: N, K >= 0 (< 2^31); group >= 1; ldq >= ceil(N / 8);
- * lds >= N; NULL only for an operand with no elements.  N == 0 is a no-op;
- * K == 0 writes zeros.  All pointers are DEVICE pointers owned by the
- * caller.  Errors: NNJIT_EINVAL for bad arguments, as for nnjit_matmul.
- * 16-byte loads are used when N % 32 == 0, ldq % 4 == 0, lds % 8 == 0 and
- * Wq, scales are 16-byte aligned; otherwise a word-load configuration runs
- * (correct, slower).  Uses the tuned configuration of (N, K, group) if
+ * x: IEEE binary16 [K]; Wq: uint32 words, N rows of ldq words, eight codes
+ * per word along k, low nibble first; scales: binary16, N rows of lds;
+ * y: fp32 [N], overwritten.  Products are exact, sums in fp32 in a fixed
+ * order, so results are deterministic.
+ * Preconditions: N, K >= 0 (< 2^31); group >= 1; ldq >= ceil(K / 8);
+ * lds >= ceil(K / group); NULL only for an operand with no elements.  N == 0
+ * is a no-op; K == 0 writes zeros.  All pointers are DEVICE pointers owned by
+ * the caller.  Errors: NNJIT_EINVAL for bad arguments, as for nnjit_matmul.
+ * 16-byte loads are used when group % 32 == 0, ldq % 4 == 0 and x, Wq are
+ * 16-byte aligned; otherwise a word-load configuration runs (correct,
+ * slower).  Uses the tuned configuration of (N, K, group) if
  * nnjit_tune_gemv_q4 ran for it, else the first of its lite space; online
  * tuning (nnjit_set_online) applies as for nnjit_matmul. */
 int nnjit_gemv_q4(int64_t N, int64_t K, int64_t group, const void *x, const void *Wq, int64_t ldq,

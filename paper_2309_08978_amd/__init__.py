@@ -341,11 +341,11 @@ def batched_matmul(A, B, C=None, stream=None, cfg: Optional[int] = None):
 
 def gemv_q4(x, Wq, scales, group: int, N: int, y=None, stream=None, cfg: Optional[int] = None):
     """y = x . W for a 4-bit weight-only W (include/nnjit.h, nnjit_gemv_q4):
-    x fp16 [K], Wq int32 [K, ldq] (uint32 code words, reinterpreted), scales
-    fp16 [ceil(K / group), lds]; y fp32 [N] (allocated if None)."""
+    x fp16 [K], Wq int32 [N, ldq] (uint32 code words, reinterpreted), scales
+    fp16 [N, lds]; y fp32 [N] (allocated if None)."""
     import torch
     K = int(x.shape[0])
-    if Wq.dim() != 2 or Wq.shape[0] != K or scales.dim() != 2:
+    if Wq.dim() != 2 or scales.dim() != 2 or Wq.shape[0] < N or scales.shape[0] < N:
         raise ValueError(f"shape mismatch x {tuple(x.shape)}, Wq {tuple(Wq.shape)}, scales {tuple(scales.shape)}")
     if x.dtype != torch.float16 or scales.dtype != torch.float16 or Wq.element_size() != 4:
         raise TypeError("x and scales must be float16, Wq 32-bit words")

@@ -1,57 +1,66 @@
-// y[N] = x[K] . W[K][N] for a 4-bit weight-only quantised W (decode-time
-// linear layers of a 4-bit LLM, Sec. 7): x fp16, y fp32, and
-//   W[k][n] = (q[k][n] - 8) * s[k / G][n]
-// with q the 4-bit code of column n in 32-bit word n / 8 of row k (bits
-// 4 (n % 8) .. 4 (n % 8) + 3) and s the fp16 scale of row group k / G.
-// Bandwidth-bound: every code byte is read once, 16 bytes per lane per load
-// (32 columns of one row).
+// y[N] = x[K] . W for a 4-bit weight-only quantised W (decode-time linear
+// layers of a 4-bit LLM, Sec. 7), W stored as a linear layer's weight: one
+// row per output n, eight 4-bit codes per 32-bit word along the inputs k,
+// one fp16 scale per output and group of G inputs:
+//   W[k][n] = (q[n][k] - 8) * s[n][k / G],  x fp16, y fp32.
+// Bandwidth-bound: every code byte is read once, 16 bytes (32 codes) per lane
+// per load, a wave's load covering 2048 consecutive inputs of one row.
 //
-// Arithmetic.  Rows are taken in pairs (k, k+1) of one group.  A byte
-// permute puts the same byte of the two rows' words into the low and high
-// halves of one register; each half then holds two codes (two columns).  An
-// or with an fp16 exponent makes the halves exact fp16 numbers: the low
-// nibble under exponent 1024 reads 1024 + q, the high nibble (bits 4..7)
-// under exponent 64 reads 64 + q; a packed fp16 subtract of 1032 (resp. 72)
-// leaves exactly q - 8 for both rows.  v_dot2_f32_f16 then adds
-// x[k] (q[k] - 8) + x[k+1] (q[k+1] - 8) into an fp32 accumulator -- the
-// fp16 products are exact in fp32.  Seven VALU instructions per four codes.
+// Work decomposition.  A wave owns RW consecutive output rows; the KS waves
+// of a row group split the row's 2048-input blocks between them (block j to
+// wave j mod KS).  No output is shared between workgroups: one kernel, no
+// partial sums in device memory.  Sums: per lane over its blocks, then across
+// the 64 lanes (butterfly), then across the KS waves in wave order (LDS), a
+// fixed order, so results are deterministic.
 //
-// Work decomposition.  L lanes span a segment of 32 L columns; the
-// workgroup's other lanes are row slots (R = NTHR / L).  Split s of the K
-// axis covers whole groups [s gchunk, (s+1) gchunk).  A work item is U
-// consecutive row pairs of one group; row slot r takes items r, r + R, ...
-// of its split.  An item's codes are summed in fp32 and multiplied by the
-// group's scale once, into the lane's running sums (scale is linear, so a
-// group split over several items or row slots is still exact up to fp32
-// rounding).  Reduction over row slots, waves and splits is fixed-order, as
-// in the fp GEMV.
+// Arithmetic (16-byte configurations, G a multiple of 32, so the 32 codes of
+// a lane share one scale).  A word holds inputs k .. k+7 of one row.  Masking
+// with 0x000F000F puts the codes of k and k+4 in the low four bits of the two
+// fp16 halves; or-ing in the exponent of 1024 makes them the exact fp16
+// numbers 1024 + q, and a packed fp16 subtract of 1032 leaves q - 8 exactly.
+// Masking with 0x00F000F0 (codes of k+1, k+5 in bits 4..7) under the exponent
+// of 64 gives 64 + q, minus 72; a shift by 8 does the same for k+2, k+6 and
+// k+3, k+7.  The x values are regrouped once per block into the matching
+// pairs (x[k], x[k+4]) ..., shared by the wave's RW rows, and v_dot2_f32_f16
+// adds the two products into an fp32 sum.  Per 8 codes: 4 mask-and-or, 1
+// shift, 4 packed subtracts, 4 dot2.  Each item's sum times its scale goes
+// into the row's running fp32 sum.  (dot2 is exact to about one fp32 ulp for
+// normal fp16 operands; with subnormal ones -- codes read as q 2^-24 without
+// an exponent -- it was measured to keep only about 14 bits, so the codes are
+// always made normal numbers first.)
+//
+// The word-load configurations (any G, any alignment) take each code through
+// fp32: w = (q - 8) s exactly, y += x w.
 #include "kcommon.h"
 
 namespace nnjit {
 
 typedef _Float16 h2 __attribute__((ext_vector_type(2)));
 
-template <int L, int NTHR, int U, bool VEC>
+constexpr int kQ4Block = 2048;   // inputs per wave load: 64 lanes x 32 codes
+
+template <int RW, int NTHR, int KS, int UB>
 __global__ void __launch_bounds__(NTHR)
 gemv_q4_kernel(GemvQ4Params p)
 {
-    constexpr int R = NTHR / L;       // row slots per workgroup
-    constexpr int NW = NTHR / 64;     // waves
-    constexpr int CW = 32 * L;        // columns per workgroup
-    static_assert(NTHR % 64 == 0 && 64 % L == 0, "layout");
+    constexpr int NW = NTHR / 64;       // waves
+    constexpr int RG = NW / KS;         // row groups per workgroup
+    static_assert(NTHR % 64 == 0 && NW % KS == 0, "layout");
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int rg = wave / KS, ks = wave - rg * KS;
+    const int n0 = (blockIdx.x * RG + rg) * RW;
+    const int K = p.K, N = p.N, G = p.G;
+    const int nblk = (K + kQ4Block - 1) / kQ4Block;
 
-    const int tid = threadIdx.x;
-    const int c = tid % L, rs = tid / L;
-    const int seg = blockIdx.x % p.segs, sp = blockIdx.x / p.segs;
-    const int n = seg * CW + c * 32;          // first column of this lane
-    const int N = p.N, K = p.K, G = p.G;
-    const int g0 = sp * p.gchunk;
-    const int g1 = min(p.ngroups, g0 + p.gchunk);
-    const int P = (G + 1) >> 1;               // row pairs per group
-    const int C = (P + U - 1) / U;            // items per group
-    const int items = (g1 - g0) * C;
-    const int nwords = (N + 7) >> 3;          // words of a row that hold columns < N
-
+    const unsigned *wrow[RW];
+    const unsigned short *srow[RW];
+#pragma unroll
+    for (int r = 0; r < RW; ++r) {
+        const int n = min(n0 + r, N - 1);      // rows past N: read row N - 1, never stored
+        wrow[r] = (const unsigned *)p.Wq + (long long)n * p.ldq;
+        srow[r] = (const unsigned short *)p.S + (long long)n * p.lds;
+    }
+    const unsigned short *xs = (const unsigned short *)p.x;
     // fp16 exponent patterns, kept in VGPRs so that mask-and-or is one
     // v_and_or_b32 (a VOP3 instruction cannot take two literal constants)
     unsigned mag_lo, mag_hi;
@@ -60,178 +69,221 @@ gemv_q4_kernel(GemvQ4Params p)
     const h2 off_lo = {(_Float16)1032.0f, (_Float16)1032.0f};
     const h2 off_hi = {(_Float16)72.0f, (_Float16)72.0f};
 
-    const unsigned *Wq = (const unsigned *)p.Wq;
-    const unsigned short *xs = (const unsigned short *)p.x;
-    const unsigned short *S = (const unsigned short *)p.S;
-
-    auto codes = [&](int k) -> u32x4 {
-        const unsigned *src = Wq + (long long)k * p.ldq + (n >> 3);
-        if constexpr (VEC) {
-            return *(const u32x4 *)src;
-        } else {
-            u32x4 v = {0u, 0u, 0u, 0u};
+    float acc[RW];
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
-                if ((n >> 3) + j < nwords) v[j] = src[j];
-            return v;
-        }
-    };
+    for (int r = 0; r < RW; ++r) acc[r] = 0.f;
 
-    float acc[32];
+    const int klast = ((K - 1) >> 5) << 5;       // start of the last 32-input chunk
+    for (int j0 = ks; j0 < nblk; j0 += KS * UB) {
+        u32x4 wv[UB][RW];
+        unsigned sv[UB][RW];
+        u32x4 xv[UB][4];
+        // every load of UB blocks first.  Codes and scales are read from the
+        // chunk clamped into the row (always in bounds); a chunk past the row
+        // meets x = 0, so it adds exactly nothing
 #pragma unroll
-    for (int e = 0; e < 32; ++e) acc[e] = 0.f;
-
-    if (n < N) {
-        for (int t = rs; t < items; t += R) {
-            const int gl = t / C;
-            const int g = g0 + gl;
-            const int i0 = (t - gl * C) * U;
-            const int kb = g * G;
-            const int ke = (int)min((long long)kb + G, (long long)K);
-            // every load of the item first: U row pairs, the pairs' x, the
-            // group's 32 scales.  Rows past the group's end are clamped to
-            // its last row (in bounds) and meet x = 0.
-            u32x4 wa[U], wb[U];
+        for (int b = 0; b < UB; ++b) {
+            const int j = j0 + b * KS;
+            const int k0 = j * kQ4Block + lane * 32;
+            const bool live = j < nblk && k0 < K;
+            const int kc = min(k0, klast);
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int ka = kb + 2 * (i0 + u);
-                wa[u] = codes(min(ka, ke - 1));
-                wb[u] = codes(min(ka + 1, ke - 1));
+            for (int r = 0; r < RW; ++r) {
+                wv[b][r] = *(const u32x4 *)(wrow[r] + (kc >> 3));
+                sv[b][r] = srow[r][kc / G];
             }
-            unsigned sc[16];
-            const unsigned short *srow = S + (long long)g * p.lds + n;
-            if constexpr (VEC) {
+            if (live && k0 + 32 <= K) {
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const u32x4 v = *(const u32x4 *)(srow + 8 * j);
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) sc[4 * j + e] = v[e];
-                }
+                for (int m = 0; m < 4; ++m) xv[b][m] = *(const u32x4 *)(xs + k0 + 8 * m);
             } else {
+                // the row's last, partial block: inputs at or past K read as +0
 #pragma unroll
-                for (int j = 0; j < 16; ++j) {
-                    const unsigned lo = (n + 2 * j < N) ? srow[2 * j] : 0u;
-                    const unsigned hi = (n + 2 * j + 1 < N) ? srow[2 * j + 1] : 0u;
-                    sc[j] = lo | (hi << 16);
-                }
-            }
-            h2 xp[U];
+                for (int m = 0; m < 4; ++m)
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int ka = kb + 2 * (i0 + u);
-                unsigned bits;
-                if (p.xpair && ka + 1 < ke) {
-                    bits = *(const unsigned *)(xs + ka);    // ka even, x 4-byte aligned
-                } else {
-                    const unsigned lo = ka < ke ? xs[ka] : 0u;
-                    const unsigned hi = ka + 1 < ke ? xs[ka + 1] : 0u;
-                    bits = lo | (hi << 16);
-                }
-                xp[u] = __builtin_bit_cast(h2, bits);
-            }
-
-            float ag[32];
-#pragma unroll
-            for (int e = 0; e < 32; ++e) ag[e] = 0.f;
-#pragma unroll
-            for (int u = 0; u < U; ++u)
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-#pragma unroll
-                    for (int b = 0; b < 4; ++b) {
-                        // low half: byte b of row k's word, high half: of row k+1's
-                        const unsigned sel = 0x0c000c00u | ((4u + b) << 16) | (unsigned)b;
-                        const unsigned tw = __builtin_amdgcn_perm(wb[u][j], wa[u][j], sel);
-                        const h2 lo = __builtin_bit_cast(h2, (tw & 0x000F000Fu) | mag_lo) - off_lo;
-                        const h2 hi = __builtin_bit_cast(h2, (tw & 0x00F000F0u) | mag_hi) - off_hi;
-                        ag[8 * j + 2 * b] = __builtin_amdgcn_fdot2(lo, xp[u], ag[8 * j + 2 * b], false);
-                        ag[8 * j + 2 * b + 1] = __builtin_amdgcn_fdot2(hi, xp[u], ag[8 * j + 2 * b + 1], false);
+                    for (int e = 0; e < 4; ++e) {
+                        const int k = k0 + 8 * m + 2 * e;
+                        const unsigned lo = (live && k < K) ? xs[k] : 0u;
+                        const unsigned hi = (live && k + 1 < K) ? xs[k + 1] : 0u;
+                        xv[b][m][e] = lo | (hi << 16);
                     }
+            }
+        }
 #pragma unroll
-            for (int e = 0; e < 32; ++e) {
-                const h2 s2 = __builtin_bit_cast(h2, sc[e >> 1]);
-                acc[e] = __builtin_fmaf((float)s2[e & 1], ag[e], acc[e]);
+        for (int b = 0; b < UB; ++b) {
+            // x regrouped into the pairs that meet the decoded codes
+            h2 xp[4][4];
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+                const u32x4 d = xv[b][m];       // (x0,x1) (x2,x3) (x4,x5) (x6,x7)
+                xp[m][0] = __builtin_bit_cast(h2, __builtin_amdgcn_perm(d[2], d[0], 0x05040100u));  // (x0, x4)
+                xp[m][1] = __builtin_bit_cast(h2, __builtin_amdgcn_perm(d[2], d[0], 0x07060302u));  // (x1, x5)
+                xp[m][2] = __builtin_bit_cast(h2, __builtin_amdgcn_perm(d[3], d[1], 0x05040100u));  // (x2, x6)
+                xp[m][3] = __builtin_bit_cast(h2, __builtin_amdgcn_perm(d[3], d[1], 0x07060302u));  // (x3, x7)
+            }
+#pragma unroll
+            for (int r = 0; r < RW; ++r) {
+                float a = 0.f;
+#pragma unroll
+                for (int m = 0; m < 4; ++m) {
+                    const unsigned w = wv[b][r][m], t = w >> 8;
+                    const h2 q04 = __builtin_bit_cast(h2, (w & 0x000F000Fu) | mag_lo) - off_lo;
+                    const h2 q15 = __builtin_bit_cast(h2, (w & 0x00F000F0u) | mag_hi) - off_hi;
+                    const h2 q26 = __builtin_bit_cast(h2, (t & 0x000F000Fu) | mag_lo) - off_lo;
+                    const h2 q37 = __builtin_bit_cast(h2, (t & 0x00F000F0u) | mag_hi) - off_hi;
+                    a = __builtin_amdgcn_fdot2(q04, xp[m][0], a, false);
+                    a = __builtin_amdgcn_fdot2(q15, xp[m][1], a, false);
+                    a = __builtin_amdgcn_fdot2(q26, xp[m][2], a, false);
+                    a = __builtin_amdgcn_fdot2(q37, xp[m][3], a, false);
+                }
+                const _Float16 s = __builtin_bit_cast(_Float16, (unsigned short)sv[b][r]);
+                acc[r] = __builtin_fmaf((float)s, a, acc[r]);
             }
         }
     }
 
-    // 1. row slots inside a wave
+    // across the lanes of the wave
 #pragma unroll
-    for (int off = L; off < 64; off <<= 1)
+    for (int off = 32; off > 0; off >>= 1)
 #pragma unroll
-        for (int e = 0; e < 32; ++e) acc[e] += __shfl_xor(acc[e], off, 64);
+        for (int r = 0; r < RW; ++r) acc[r] += __shfl_xor(acc[r], off, 64);
 
-    // 2. waves of the workgroup, in wave order
-    if constexpr (NW > 1) {
-        __shared__ float red[NW][L][32];
-        const int wave = tid >> 6, lane = tid & 63;
-        if (lane < L)
+    // across the K-slice waves of the row group, in wave order
+    if constexpr (KS > 1) {
+        __shared__ float red[NW][RW];
+        if (lane == 0)
 #pragma unroll
-            for (int e = 0; e < 32; ++e) red[wave][lane][e] = acc[e];
+            for (int r = 0; r < RW; ++r) red[wave][r] = acc[r];
         __syncthreads();
-        if (tid < L) {
+        if (ks != 0) return;
 #pragma unroll
-            for (int e = 0; e < 32; ++e) {
-                float v = red[0][tid][e];
+        for (int r = 0; r < RW; ++r) {
+            float v = red[wave][r];
 #pragma unroll
-                for (int w = 1; w < NW; ++w) v += red[w][tid][e];
-                acc[e] = v;
-            }
+            for (int w = 1; w < KS; ++w) v += red[wave + w][r];
+            acc[r] = v;
         }
     }
-
-    if (tid >= L) return;
-    float *dst = p.nsplit == 1 ? p.y : p.ws + (long long)sp * N;
+    if (lane == 0)
 #pragma unroll
-    for (int e = 0; e < 32; ++e)
-        if (n + e < N) dst[n + e] = acc[e];
+        for (int r = 0; r < RW; ++r)
+            if (n0 + r < N) p.y[n0 + r] = acc[r];
 }
 
-template <int L, int NTHR, int U, bool VEC>
+// Word loads: any group size and alignment.  Lane l takes words l, l + 64, ...
+// of its rows; each code goes through fp32 with its own group's scale.
+template <int RW, int NTHR>
+__global__ void __launch_bounds__(NTHR)
+gemv_q4_words_kernel(GemvQ4Params p)
+{
+    constexpr int NW = NTHR / 64;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int n0 = (blockIdx.x * NW + wave) * RW;
+    const int K = p.K, N = p.N, G = p.G;
+    const int nwords = (K + 7) >> 3;
+    const unsigned *wrow[RW];
+    const unsigned short *srow[RW];
+#pragma unroll
+    for (int r = 0; r < RW; ++r) {
+        const int n = min(n0 + r, N - 1);
+        wrow[r] = (const unsigned *)p.Wq + (long long)n * p.ldq;
+        srow[r] = (const unsigned short *)p.S + (long long)n * p.lds;
+    }
+    const _Float16 *xh = (const _Float16 *)p.x;
+    const _Float16 *sh[RW];
+#pragma unroll
+    for (int r = 0; r < RW; ++r) sh[r] = (const _Float16 *)srow[r];
+    float acc[RW];
+#pragma unroll
+    for (int r = 0; r < RW; ++r) acc[r] = 0.f;
+    for (int wi = lane; wi < nwords; wi += 64) {
+        unsigned wd[RW];
+#pragma unroll
+        for (int r = 0; r < RW; ++r) wd[r] = wrow[r][wi];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int k = 8 * wi + i;
+            if (k < K) {
+                const float xk = (float)xh[k];
+#pragma unroll
+                for (int r = 0; r < RW; ++r) {
+                    const float q = (float)((int)((wd[r] >> (4 * i)) & 15u) - 8);
+                    acc[r] = __builtin_fmaf(xk, q * (float)sh[r][k / G], acc[r]);
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1)
+#pragma unroll
+        for (int r = 0; r < RW; ++r) acc[r] += __shfl_xor(acc[r], off, 64);
+    if (lane == 0)
+#pragma unroll
+        for (int r = 0; r < RW; ++r)
+            if (n0 + r < N) p.y[n0 + r] = acc[r];
+}
+
+template <int RW, int NTHR, int KS, int UB>
 static hipError_t launch_gemv_q4(const void *params, dim3 grid, hipStream_t stream)
 {
-    hipLaunchKernelGGL((gemv_q4_kernel<L, NTHR, U, VEC>), grid, dim3(NTHR), 0, stream,
+    hipLaunchKernelGGL((gemv_q4_kernel<RW, NTHR, KS, UB>), grid, dim3(NTHR), 0, stream,
                        *(const GemvQ4Params *)params);
     return hipGetLastError();
 }
 
-// Registers: 32 running sums, 32 item sums, U pairs of 16-byte code loads,
-// their x pairs, 16 scale words, plus a fixed overhead.  LDS: the cross-wave
-// reduction buffer.
-constexpr int est_regs_q4(int u) { return 104 + 9 * u; }
-constexpr int lds_q4(int nthr, int l) { return nthr > 64 ? (nthr / 64) * l * 32 * 4 : 4; }
+template <int RW, int NTHR>
+static hipError_t launch_gemv_q4_words(const void *params, dim3 grid, hipStream_t stream)
+{
+    hipLaunchKernelGGL((gemv_q4_words_kernel<RW, NTHR>), grid, dim3(NTHR), 0, stream,
+                       *(const GemvQ4Params *)params);
+    return hipGetLastError();
+}
 
-// The compiled configurations (L lanes per segment, NTHR threads, U row
-// pairs per item, 16-byte loads or word loads).
+// Registers: per block in flight, RW code loads (4 words) and scales, the
+// block's 16 x words and their 16 regrouped pairs; RW running sums; a fixed
+// overhead.  LDS: the cross-wave buffer of K-sliced configurations.
+constexpr int est_regs_q4(int rw, int ub) { return ub * (5 * rw + 32) + rw + 24; }
+constexpr int lds_q4(int nthr, int rw, int ks) { return ks > 1 ? (nthr / 64) * rw * 4 : 0; }
+
+// The compiled configurations: RW rows per wave, NTHR threads, KS K-slices
+// (waves per row group), UB blocks in flight.
 #define NNJIT_Q4_LIST(X) \
-    X(16, 256, 2, true)  \
-    X(16, 256, 4, true)  \
-    X(16, 256, 8, true)  \
-    X(32, 256, 2, true)  \
-    X(32, 256, 4, true)  \
-    X(32, 256, 8, true)  \
-    X(64, 256, 2, true)  \
-    X(64, 256, 4, true)  \
-    X(64, 256, 8, true)  \
-    X(16, 512, 2, true)  \
-    X(16, 512, 4, true)  \
-    X(16, 512, 8, true)  \
-    X(32, 512, 2, true)  \
-    X(32, 512, 4, true)  \
-    X(16, 1024, 2, true) \
-    X(16, 1024, 4, true) \
-    X(16, 256, 4, false) \
-    X(64, 256, 4, false)
+    X(2, 256, 1, 2)      \
+    X(4, 256, 1, 1)      \
+    X(4, 256, 1, 2)      \
+    X(8, 256, 1, 1)      \
+    X(8, 256, 1, 2)      \
+    X(2, 256, 2, 2)      \
+    X(4, 256, 2, 1)      \
+    X(4, 256, 2, 2)      \
+    X(8, 256, 2, 1)      \
+    X(1, 256, 4, 2)      \
+    X(2, 256, 4, 2)      \
+    X(4, 256, 4, 1)      \
+    X(4, 128, 1, 2)      \
+    X(8, 128, 1, 1)      \
+    X(4, 64, 1, 2)       \
+    X(8, 64, 1, 1)
 
-#define NNJIT_Q4_INST(L, NTHR, U, VEC) template __global__ void gemv_q4_kernel<L, NTHR, U, VEC>(GemvQ4Params);
+#define NNJIT_Q4_WORDS_LIST(X) \
+    X(1, 256)                  \
+    X(4, 256)
+
+#define NNJIT_Q4_INST(RW, NTHR, KS, UB) template __global__ void gemv_q4_kernel<RW, NTHR, KS, UB>(GemvQ4Params);
 NNJIT_Q4_LIST(NNJIT_Q4_INST)
+#define NNJIT_Q4_WORDS_INST(RW, NTHR) template __global__ void gemv_q4_words_kernel<RW, NTHR>(GemvQ4Params);
+NNJIT_Q4_WORDS_LIST(NNJIT_Q4_WORDS_INST)
 
 #if !defined(__HIP_DEVICE_COMPILE__)
-#define NNJIT_Q4_ENTRY(L, NTHR, U, VEC)                                                                              \
-    {"gemv_q4_L" #L "_t" #NTHR "_u" #U "_v" #VEC, FAM_GEMV_Q4, 0, 0, 1, 32 * L, 2 * (NTHR / L), NTHR / 64, 1, 0, 0, \
-     1, (VEC ? 16 : 4), L, U, NTHR, lds_q4(NTHR, L), est_regs_q4(U),                                             \
-     (const void *)&gemv_q4_kernel<L, NTHR, U, VEC>, &launch_gemv_q4<L, NTHR, U, VEC>, 0},
-const Variant kGemvQ4Variants[] = {NNJIT_Q4_LIST(NNJIT_Q4_ENTRY)};
+// Variant fields: mt = rows per wave, nt = rows per workgroup, kt = inputs per
+// wave load, wm = waves, kslices = K-slices, unroll = blocks in flight.
+#define NNJIT_Q4_ENTRY(RW, NTHR, KS, UB)                                                                            \
+    {"gemv_q4_r" #RW "_t" #NTHR "_k" #KS "_u" #UB, FAM_GEMV_Q4, 0, 0, RW, RW * (NTHR / 64) / KS, kQ4Block,       \
+     NTHR / 64, 1, 0, 0, KS, 16, 64, UB, NTHR, lds_q4(NTHR, RW, KS), est_regs_q4(RW, UB),                       \
+     (const void *)&gemv_q4_kernel<RW, NTHR, KS, UB>, &launch_gemv_q4<RW, NTHR, KS, UB>, 0},
+#define NNJIT_Q4_WORDS_ENTRY(RW, NTHR)                                                                               \
+    {"gemv_q4_words_r" #RW "_t" #NTHR, FAM_GEMV_Q4, 0, 0, RW, RW * (NTHR / 64), 512, NTHR / 64, 1, 0, 0, 1, 4, 64, 1, \
+     NTHR, 0, 3 * RW + 40, (const void *)&gemv_q4_words_kernel<RW, NTHR>, &launch_gemv_q4_words<RW, NTHR>, 0},
+const Variant kGemvQ4Variants[] = {NNJIT_Q4_LIST(NNJIT_Q4_ENTRY) NNJIT_Q4_WORDS_LIST(NNJIT_Q4_WORDS_ENTRY)};
 const int kNumGemvQ4Variants = sizeof(kGemvQ4Variants) / sizeof(kGemvQ4Variants[0]);
 #endif
 

@@ -40,22 +40,16 @@ struct GemvParams {
     float *ws;        // S > 1: partial rows, [S][N]
 };
 
-// Arguments of the 4-bit weight-only GEMV: y[N] = x[K] . W[K][N] with
-// W[k][n] = (q[k][n] - 8) * S[k / G][n], q packed eight per 32-bit word
-// along n (low nibble first), S fp16, x fp16, y fp32.
+// Arguments of the 4-bit weight-only GEMV: y[N] = x[K] . W with
+// W[k][n] = (q[n][k] - 8) * S[n][k / G]; row n of q packed eight codes per
+// 32-bit word along k (low nibble first), S fp16, x fp16, y fp32.
 struct GemvQ4Params {
     const void *x;        // fp16 [K]
-    const void *Wq;       // uint32 [K][ldq]
-    const void *S;        // fp16 [ngroups][lds]
-    float *y;
+    const void *Wq;       // uint32 [N][ldq]
+    const void *S;        // fp16 [N][lds]
+    float *y;             // fp32 [N]
     long long ldq, lds;
     int K, N, G;
-    int ngroups;          // ceil(K / G)
-    int gchunk;           // groups per split
-    int nsplit;           // splits (workgroups per column segment)
-    int segs;             // column segments
-    int xpair;            // 1: G even and x 4-byte aligned (x pairs load as one word)
-    float *ws;            // nsplit > 1: partial rows, [nsplit][N]
 };
 
 typedef hipError_t (*LaunchFn)(const void *params, dim3 grid, hipStream_t stream);

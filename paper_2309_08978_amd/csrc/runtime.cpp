@@ -195,8 +195,8 @@ struct Call {
     int64_t ldc, sC;
     int dtype;
     hipStream_t stream;
-    // 4-bit GEMV (q4 = true): A = x, B = the code words (ldb = ldq), Sc =
-    // the scales (leading dimension lds), batch = the group size, M = 1
+    // 4-bit GEMV (q4 = true): A = x, B = the code words [N][ldq] (ldb = ldq),
+    // Sc = the scales [N][lds], batch = the group size, M = 1
     bool q4 = false;
     const void *Sc = nullptr;
     int64_t lds = 0;
@@ -206,8 +206,9 @@ int validate_q4(const Call &c) {
     if (c.N < 0 || c.K < 0) return fail(NNJIT_EINVAL, "negative dimension (N=%lld K=%lld)", (long long)c.N, (long long)c.K);
     if (c.N > INT32_MAX || c.K > INT32_MAX) return fail(NNJIT_EINVAL, "dimension above 2^31-1");
     if (c.batch < 1 || c.batch > INT32_MAX) return fail(NNJIT_EINVAL, "group=%lld must be in [1, 2^31)", (long long)c.batch);
-    if (c.ldb < (c.N + 7) / 8) return fail(NNJIT_EINVAL, "ldq=%lld < ceil(N/8)=%lld", (long long)c.ldb, (long long)((c.N + 7) / 8));
-    if (c.lds < c.N) return fail(NNJIT_EINVAL, "lds=%lld < N=%lld", (long long)c.lds, (long long)c.N);
+    if (c.ldb < (c.K + 7) / 8) return fail(NNJIT_EINVAL, "ldq=%lld < ceil(K/8)=%lld", (long long)c.ldb, (long long)((c.K + 7) / 8));
+    if (c.lds < (c.K + c.batch - 1) / c.batch)
+        return fail(NNJIT_EINVAL, "lds=%lld < ceil(K/group)=%lld", (long long)c.lds, (long long)((c.K + c.batch - 1) / c.batch));
     if (c.N > 0) {
         if (c.K > 0 && (!c.A || !c.B || !c.Sc)) return fail(NNJIT_EINVAL, "x, Wq or scales is NULL");
         if (!c.C) return fail(NNJIT_EINVAL, "y is NULL");
@@ -257,7 +258,7 @@ bool vec_aligned(const Call &c, bool gemv) {
 // Can a 16-byte-load 4-bit GEMV configuration run these operands?
 bool vec_aligned_q4(const Call &c) {
     auto al = [](const void *p) { return ((uintptr_t)p & 15u) == 0; };
-    return c.N % 32 == 0 && c.ldb % 4 == 0 && c.lds % 8 == 0 && al(c.B) && al(c.Sc);
+    return c.batch % 32 == 0 && c.ldb % 4 == 0 && al(c.B) && al(c.A);
 }
 
 // vector-load eligibility for the family a call runs on
@@ -290,14 +291,7 @@ int launch(Device &d, const Config &cfg, const Call &c) {
         p.K = (int)c.K;
         p.N = (int)c.N;
         p.G = (int)g.group;
-        p.ngroups = (int)g.ngroups;
-        p.gchunk = g.kchunk;
-        p.nsplit = g.split;
-        p.segs = g.tiles_n;
-        p.xpair = (g.group % 2 == 0 && ((uintptr_t)c.A & 3u) == 0) ? 1 : 0;
-        p.ws = w ? w->ws : nullptr;
         e = v.launch(&p, dim3((unsigned)g.wgs), c.stream);
-        if (e == hipSuccess && g.split > 1) e = launch_splitk_reduce(p.ws, g.split, 1, 1, p.N, p.y, p.N, 0, c.stream);
     } else if (!family_is_gemv(v.family)) {
         GemmParams p{};
         p.lda = c.lda;
@@ -353,9 +347,10 @@ const Config *fallback_config(int family, const Call &c, const Device &d) {
     for (const Config &cfg : configs()) {
         if (cfg.v->family != family || cfg.v->vec_bytes == 16) continue;
         if (family_is_q4(family)) {
+            // the word-load configuration with the most workgroups that still
+            // fill at most two per CU (else the one with the most)
             const Geometry g = geometry_of(cfg, c.batch, c.M, c.N, c.K);
-            if (g.split != cfg.split) continue;
-            if (!best || g.wgs <= 2LL * d.limits.num_cus) best = &cfg;
+            if (!best || g.wgs >= 2LL * d.limits.num_cus) best = &cfg;
             continue;
         }
         if (!family_is_gemv(family)) {
@@ -542,11 +537,11 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
     Call c{batch, M, N, K, nullptr, std::max<int64_t>(1, K), M * K, nullptr, std::max<int64_t>(1, N), K * N,
            nullptr, std::max<int64_t>(1, N), M * N, dtype, nullptr};
     if (q4) {
-        // 4-bit GEMV scratch layout: rows of ceil(N/8) words and N scales,
-        // padded to 16 bytes
+        // 4-bit GEMV scratch layout: rows of ceil(K/8) words padded to 16
+        // bytes, rows of ceil(K/G) scales
         c.q4 = true;
-        c.ldb = ((N + 7) / 8 + 3) / 4 * 4;
-        c.lds = (N + 7) / 8 * 8;
+        c.ldb = ((K + 7) / 8 + 3) / 4 * 4;
+        c.lds = std::max<int64_t>(1, (K + batch - 1) / batch);
     }
     if (dtype != NNJIT_F32 && dtype != NNJIT_F16) return fail(NNJIT_EDTYPE, "unknown dtype %d", dtype);
     if (batch < 1 || M < 1 || N < 1 || K < 0) return fail(NNJIT_EINVAL, "tune needs batch, M, N >= 1 and K >= 0");
@@ -577,14 +572,11 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
     // bandwidth bound and runs on weights streamed from HBM, so it is timed
     // that way: its weight operand rotates over enough copies (>= 512 MiB
     // together) that the 256 MB last-level cache cannot hold them.
-    // (4-bit GEMV: x [K] fp16; per copy the code words [K][ldq] followed by
-    // the scales [ceil(K/G)][lds]; y [N])
-    const int64_t q4_groups = q4 ? (K + std::min<int64_t>(batch, std::max<int64_t>(K, 1)) - 1) /
-                                       std::min<int64_t>(batch, std::max<int64_t>(K, 1))
-                                 : 0;
-    const size_t q4_codes = q4 ? (size_t)(K * c.ldb) * 4 : 0;
+    // (4-bit GEMV: x [K] fp16; per copy the code words [N][ldq] followed by
+    // the scales [N][lds]; y [N])
+    const size_t q4_codes = q4 ? (size_t)(N * c.ldb) * 4 : 0;
     const size_t a_bytes = q4 ? (size_t)K * 2 : (size_t)(batch * M * K) * elt;
-    const size_t b_bytes = q4 ? ((q4_codes + 255) & ~(size_t)255) + (size_t)(q4_groups * c.lds) * 2
+    const size_t b_bytes = q4 ? ((q4_codes + 255) & ~(size_t)255) + (size_t)(N * c.lds) * 2
                               : (size_t)(batch * K * N) * elt;
     const size_t c_bytes = q4 ? (size_t)N * 4 : (size_t)(batch * M * N) * 4;
     auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
@@ -617,10 +609,10 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
         char *dst = b0 + (size_t)i * up(b_bytes);
         // 4-bit codes: any bit pattern is a valid code word, so the words are
         // filled as fp32 values; the scales follow as fp16
-        e = q4 ? launch_fill_uniform(dst, K * c.ldb, NNJIT_F32, 5678u + i, c.stream)
+        e = q4 ? launch_fill_uniform(dst, N * c.ldb, NNJIT_F32, 5678u + i, c.stream)
                : launch_fill_uniform(dst, batch * K * N, dtype, 5678u + i, c.stream);
         if (e == hipSuccess && q4)
-            e = launch_fill_uniform(dst + up(q4_codes), q4_groups * c.lds, NNJIT_F16, 9012u + i, c.stream);
+            e = launch_fill_uniform(dst + up(q4_codes), N * c.lds, NNJIT_F16, 9012u + i, c.stream);
         if (e != hipSuccess) return hip_fail(e, "scratch fill");
     }
     int rot = 0;
@@ -821,7 +813,13 @@ int nnjit_config_info(int cfg, char *buf, int64_t len) {
     const Variant &v = *c.v;
     char tmp[512];
     int n;
-    if (!family_is_gemv(v.family) && !family_is_q4(v.family))
+    if (family_is_q4(v.family))
+        n = snprintf(tmp, sizeof tmp,
+                     "id=%d family=%s name=%s rows_per_wave=%d rows_per_wg=%d kslices=%d unroll=%d vec=%d split=%d "
+                     "threads=%d lds=%d est_regs=%d",
+                     c.id, family_name(v.family), v.name, v.mt, v.nt, v.kslices, v.unroll, v.vec_bytes, c.split,
+                     v.threads, v.lds_bytes, v.est_regs);
+    else if (!family_is_gemv(v.family))
         n = snprintf(tmp, sizeof tmp,
                      "id=%d family=%s name=%s mfma=%dx%dx%d Mt=%d Nt=%d Kt=%d waves=%dx%d stages=%d prefetch=%d kslices=%d "
                      "vec=%d split=%d threads=%d lds=%d est_regs=%d direct=%d",

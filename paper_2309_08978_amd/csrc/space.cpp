@@ -67,8 +67,9 @@ const std::vector<Config> &configs() {
         const int nv = total_variants();
         for (int gi = 0; gi < nv; ++gi) {
             const Variant *v = variant_at(gi);
+            static const std::vector<int> no_split = {1};
             const std::vector<int> &splits =
-                (family_is_gemv(v->family) || family_is_q4(v->family)) ? gemv_splits() : gemm_splits();
+                family_is_q4(v->family) ? no_split : family_is_gemv(v->family) ? gemv_splits() : gemm_splits();
             for (int s : splits) out.push_back(Config{(int)out.size(), v, s});
         }
         return out;
@@ -128,17 +129,14 @@ Geometry geometry_of(const Config &c, int64_t batch, int64_t M, int64_t N, int64
     const Variant &v = *c.v;
     g.split = c.split;
     if (family_is_q4(v.family)) {
-        // batch carries the group size; splits cover whole groups
-        const int64_t G = std::max<int64_t>(1, std::min<int64_t>(batch, std::max<int64_t>(K, 1)));
-        const int64_t ngroups = ceil_div(K, G);
-        g.group = G;
-        g.ngroups = ngroups;
+        // one workgroup per nt output rows, no split (batch carries the group size)
+        g.group = std::max<int64_t>(1, batch);
         g.tiles_m = 1;
         g.tiles_n = (int)ceil_div(std::max<int64_t>(N, 1), v.nt);
-        g.kchunk = (int)std::max<int64_t>(1, ceil_div(ngroups, c.split));
-        g.split = ngroups > 0 ? (int)ceil_div(ngroups, g.kchunk) : 1;
-        g.wgs = (int64_t)g.tiles_n * g.split;
-        g.ws_floats = g.split > 1 ? (int64_t)g.split * std::max<int64_t>(N, 1) : 0;
+        g.kchunk = (int)std::max<int64_t>(K, 1);
+        g.split = 1;
+        g.wgs = g.tiles_n;
+        g.ws_floats = 0;
         return g;
     }
     if (!family_is_gemv(v.family)) {
@@ -176,11 +174,11 @@ LiteResult lite_space(const Shape &s, const nnjit_device_limits &d, const std::v
     const bool gemv = family_is_gemv(fam);
     const bool q4 = family_is_q4(fam);
     const int V = vec_elems(s.dtype);
-    const bool vec_ok = q4 ? (s.N % 32 == 0) : gemv ? (s.N % V == 0) : (s.K % V == 0 && s.N % V == 0);
+    const bool vec_ok = q4 ? (s.batch % 32 == 0) : gemv ? (s.N % V == 0) : (s.K % V == 0 && s.N % V == 0);
 
     // size of the unpruned parameter space over the same axes
     if (q4) {
-        out.n_naive = 3 /*L*/ * 3 /*threads*/ * 3 /*U*/ * (int64_t)gemv_splits().size();
+        out.n_naive = 4 /*rows per wave*/ * 3 /*threads*/ * 3 /*K-slices*/ * 2 /*blocks in flight*/;
     } else if (!gemv) {
         const int64_t kt_choices = fam == FAM_GEMM_F32 ? 2 : 1;
         out.n_naive = 2 /*mfma*/ * 5 /*Mt*/ * 5 /*Nt*/ * kt_choices * 3 /*WM*/ * 3 /*WN*/ * 2 /*stages*/ *
@@ -214,31 +212,12 @@ LiteResult lite_space(const Shape &s, const nnjit_device_limits &d, const std::v
         cd.split = c.split;
         bool fit = true;
         if (q4) {
-            if (v.nt > std::max<int64_t>(512, pow2ceil(s.N))) fit = false;
-            // items (U row pairs of one group) per split must cover the row slots
-            const int64_t items_per_group = ceil_div((g.group + 1) / 2, v.unroll);
-            const int64_t R = v.threads / v.lanes_seg;
-            auto useful = [&](int split) {
-                if (split <= 1) return true;
-                const Config cs{c.id, c.v, split}, ch{c.id, c.v, split / 2};
-                const Geometry gs = geometry_of(cs, s.batch, s.M, s.N, s.K);
-                if (gs.split == geometry_of(ch, s.batch, s.M, s.N, s.K).split) return false;  // same launch as split / 2
-                return (int64_t)gs.kchunk * items_per_group >= R;
-            };
-            if (c.split > 1) {
-                if (!useful(c.split)) continue;
-                int smax = 1;
-                for (int sp : gemv_splits())
-                    if (useful(sp)) smax = sp;
-                if (g.tiles_n >= d.num_cus) continue;
-                int64_t sfill = 1;
-                while (g.tiles_n * sfill < d.num_cus) sfill <<= 1;
-                if ((c.split < sfill || c.split > 2 * sfill) && c.split != smax) continue;
-                if (g.wgs > 4 * slots) continue;                                  // over-split
-                if (g.wgs < d.num_cus / 2 && c.split != smax) continue;           // under-filled
-                const int64_t wg_here = std::min<int64_t>(r.wg_per_cu, ceil_div(g.wgs, d.num_cus));
-                if (wg_here * v.threads * (int64_t)v.unroll * 32 < 8192 && c.split != smax) continue;
-            }
+            // no workgroup wider than the (power-of-two rounded) output count;
+            // K-slices and blocks in flight only where K has the blocks for them
+            if (v.nt > std::max<int64_t>(8, pow2ceil(s.N))) fit = false;
+            const int64_t nblk = std::max<int64_t>(1, ceil_div(s.K, v.kt));
+            if (v.kslices > 1 && nblk < v.kslices) fit = false;
+            if (v.unroll > 1 && ceil_div(nblk, v.kslices) < v.unroll) fit = false;
         } else if (!gemv) {
             // shape fit: no macro tile wider than the (power-of-two rounded) matrix
             if (v.mt > std::max<int64_t>(16, pow2ceil(s.M)) || v.nt > std::max<int64_t>(16, pow2ceil(s.N))) fit = false;

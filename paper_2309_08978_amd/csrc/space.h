@@ -68,8 +68,7 @@ struct Geometry {
     int kchunk = 0;
     int64_t wgs = 0;               // workgroups over the whole launch
     int64_t ws_floats = 0;         // split-K partial storage (S x batch x M x N floats)
-    int64_t group = 0, ngroups = 0;  // 4-bit GEMV: group size (clamped to K) and groups;
-                                     // kchunk = groups per split, split = splits launched
+    int64_t group = 0;             // 4-bit GEMV: the group size
 };
 Geometry geometry_of(const Config &c, int64_t batch, int64_t M, int64_t N, int64_t K);
 

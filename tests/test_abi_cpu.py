@@ -51,20 +51,20 @@ def test_validation_without_gpu(lib):
     assert nj.nnjit_tune(64, 64, 64, 5) == nj.NNJIT_EDTYPE
     assert nj.nnjit_tune(0, 64, 64, 0) == nj.NNJIT_EINVAL
     # 4-bit GEMV: (N, K, group, x, Wq, ldq, scales, lds, y, stream)
-    assert nj.nnjit_gemv_q4(64, 64, 0, 1, 2, 8, 3, 64, 4, None) == nj.NNJIT_EINVAL      # group < 1
-    assert nj.nnjit_gemv_q4(64, 64, 32, 1, 2, 7, 3, 64, 4, None) == nj.NNJIT_EINVAL     # ldq < ceil(N/8)
-    assert nj.nnjit_gemv_q4(64, 64, 32, 1, 2, 8, 3, 63, 4, None) == nj.NNJIT_EINVAL     # lds < N
-    assert nj.nnjit_gemv_q4(-1, 64, 32, 1, 2, 8, 3, 64, 4, None) == nj.NNJIT_EINVAL
-    assert nj.nnjit_gemv_q4(64, 64, 32, 1, None, 8, 3, 64, 4, None) == nj.NNJIT_EINVAL
-    assert nj.nnjit_gemv_q4(64, 64, 32, 1, 2, 8, 3, 64, None, None) == nj.NNJIT_EINVAL
-    assert nj.nnjit_gemv_q4(0, 64, 32, 1, 2, 0, 3, 0, None, None) == nj.NNJIT_OK       # N == 0: no-op
+    assert nj.nnjit_gemv_q4(64, 64, 0, 1, 2, 8, 3, 2, 4, None) == nj.NNJIT_EINVAL       # group < 1
+    assert nj.nnjit_gemv_q4(64, 64, 32, 1, 2, 7, 3, 2, 4, None) == nj.NNJIT_EINVAL      # ldq < ceil(K/8)
+    assert nj.nnjit_gemv_q4(64, 64, 32, 1, 2, 8, 3, 1, 4, None) == nj.NNJIT_EINVAL      # lds < ceil(K/group)
+    assert nj.nnjit_gemv_q4(-1, 64, 32, 1, 2, 8, 3, 2, 4, None) == nj.NNJIT_EINVAL
+    assert nj.nnjit_gemv_q4(64, 64, 32, 1, None, 8, 3, 2, 4, None) == nj.NNJIT_EINVAL
+    assert nj.nnjit_gemv_q4(64, 64, 32, 1, 2, 8, 3, 2, None, None) == nj.NNJIT_EINVAL
+    assert nj.nnjit_gemv_q4(0, 64, 32, 1, 2, 8, 3, 2, None, None) == nj.NNJIT_OK       # N == 0: no-op
     assert nj.nnjit_tune_gemv_q4(64, 64, 0) == nj.NNJIT_EINVAL
     cfgs = nj.configs()
     q4 = next(c["id"] for c in cfgs if c["family"] == "gemv_q4")
     f16 = next(c["id"] for c in cfgs if c["family"] == "gemm_f16")
     # a 4-bit configuration is not a MatMul configuration, and the other way round
     assert nj.nnjit_matmul_config(q4, 1, 4, 8, 8, 1, 8, 0, 2, 8, 0, 3, 8, 0, 1, None) == nj.NNJIT_EINVAL
-    assert nj.nnjit_gemv_q4_config(f16, 64, 64, 32, 1, 2, 8, 3, 64, 4, None) == nj.NNJIT_EINVAL
+    assert nj.nnjit_gemv_q4_config(f16, 64, 64, 32, 1, 2, 8, 3, 2, 4, None) == nj.NNJIT_EINVAL
 
 
 def test_no_gpu_is_ehip_not_abort(lib):
@@ -95,6 +95,9 @@ def test_config_table(lib):
             wm, wn = map(int, c["waves"].split("x"))
             assert c["Mt"] % wm == 0 and c["Nt"] % wn == 0
             assert c["threads"] == 64 * wm * wn * c["kslices"]
+        elif c["family"] == "gemv_q4":
+            assert p2(c["rows_per_wave"]) and p2(c["kslices"]) and p2(c["threads"]) and c["split"] == 1
+            assert c["rows_per_wg"] == c["rows_per_wave"] * (c["threads"] // 64) // c["kslices"]
         else:
             assert p2(c["cols"]) and p2(c["lanes_per_seg"]) and p2(c["threads"])
 
@@ -114,7 +117,8 @@ def test_resource_limits_follow_the_formula(lib):
         wps = min(8, 512 // regs)
         assert r["waves_per_wg"] == -(-c["threads"] // 64)
         assert r["reg_limit"] == 4 * wps // r["waves_per_wg"]
-        assert r["lds_limit"] == min(163840 // max(r["lds_per_wg"], 1), 1 << 20)
+        # L1Limit: LDS per CU over LDS per workgroup; a workgroup without LDS has no such limit
+        assert r["lds_limit"] == (min(163840 // r["lds_per_wg"], 1 << 20) if r["lds_per_wg"] > 0 else 1 << 20)
         assert r["wave_limit"] == 32 // r["waves_per_wg"]
         assert r["wg_per_cu"] == min(r["reg_limit"], r["lds_limit"], r["wave_limit"])
 
@@ -205,36 +209,29 @@ def test_microbench_groups_vary_one_primitive(lib):
 
 
 @pytest.mark.parametrize("N,K,G", [(4096, 4096, 128), (12288, 4096, 128), (4096, 11008, 128), (32000, 4096, 128),
-                                   (4096, 4096, 32), (4096, 4096, 1), (4096, 300, 7), (520, 300, 64)])
+                                   (4096, 4096, 32), (4096, 4096, 1), (4096, 300, 7), (5, 300, 64)])
 def test_q4_lite_space(lib, N, K, G):
-    """4-bit GEMV lite space: only its own family; 16-byte configurations
-    exactly when N % 32 == 0; every split launches a distinct number of
-    splits, each with a work item for every row slot (except the one
-    unsplit fallback); evaluation order by workgroups per CU."""
+    """4-bit GEMV lite space: only its own family, never split; 16-byte
+    configurations exactly when G % 32 == 0; K-slices and blocks in flight
+    only where K has blocks for them (else the unfit fallback); evaluation
+    order by workgroups per CU."""
     d = nj.mi355x_limits()
     ids, n, n_enum, n_naive = nj.nnjit_lite_space(nj.NNJIT_KIND_GEMV_Q4, nj.NNJIT_F16, G, 1, N, K, d)
     assert 1 <= n <= 96 and n_naive > n
     cfgs = nj.configs()
-    ngroups = -(-K // min(G, K))
-    items_per_group = lambda u: -(-(-(-min(G, K) // 2)) // u)
-    seen, prev = set(), None
+    nblk = -(-K // 2048)
+    fits = []
+    prev = None
     for i in ids:
         c = cfgs[i]
-        assert c["family"] == "gemv_q4"
-        assert (c["vec"] == 16) == (N % 32 == 0)
-        gchunk = -(-ngroups // c["split"])
-        launched = -(-ngroups // gchunk)
-        if c["split"] > 1:
-            half = -(-ngroups // -(-ngroups // (c["split"] // 2)))
-            assert launched != half, c
-            assert gchunk * items_per_group(c["unroll"]) >= c["threads"] // c["lanes_per_seg"], c
-        key = (c["name"], launched)
-        assert key not in seen
-        seen.add(key)
+        assert c["family"] == "gemv_q4" and c["split"] == 1
+        assert (c["vec"] == 16) == (G % 32 == 0)
+        fits.append(c["kslices"] <= nblk and (c["unroll"] == 1 or -(-nblk // c["kslices"]) >= c["unroll"]))
         r = nj.nnjit_config_resources(i, d)
         if prev is not None:
             assert r["wg_per_cu"] <= prev
         prev = r["wg_per_cu"]
+    assert all(fits) or not any(fits)
     assert nj.nnjit_lite_space(nj.NNJIT_KIND_GEMV_Q4, nj.NNJIT_F16, G, 1, N, K, d)[0] == ids
     with pytest.raises(nj.NnjitError):
         nj.nnjit_lite_space(nj.NNJIT_KIND_GEMV_Q4, nj.NNJIT_F32, G, 1, N, K, d)

@@ -2,12 +2,13 @@
 oracle, through the C-ABI.
 
 * every configuration id of the family, forced, on exact-arithmetic inputs
-  (x in {-8..8}, power-of-two scales varying by group and column) at ragged
-  shapes: a K that ends in a partial, odd group, several column segments and
-  a ragged column tail -- bit-exact, and identical when run twice;
+  (x in {-8..8}, power-of-two scales varying by output and group) at ragged
+  shapes: an output count that ends inside a workgroup, a K that ends inside
+  a word, a chunk and a 2048-input block, padding words holding random codes
+  -- bit-exact, and identical when run twice;
 * edge cases: odd and unit group sizes, a group larger than K, K = 0
-  (zeros), N = 0 (no-op), N not a multiple of 8, padded leading dimensions,
-  misaligned operands (word-load fallback);
+  (zeros), N = 0 (no-op), K = 1, padded leading dimensions, misaligned
+  operands (word-load fallback);
 * the Llama-2-7B decode shapes at full size, tuned, on the workload's own
   value recipe: the fp32 bar (rel-Frobenius 1e-5 and |err| <= 2e-6 K
   max|x| max|W| per element, max|W| <= 8 max|s|) on every output;
@@ -55,28 +56,32 @@ def q4_configs():
 
 
 def test_every_config_bit_exact(q4_configs):
-    K, G = 301, 64                       # 4 full groups, then 45 rows (odd)
+    N = 1037
     n_run = 0
-    for vec, N in ((True, 1056), (False, 1037)):
-        x, Wq, S = workloads.q4_operands(7, K, N, G, recipe="q4_int")
+    # 16-byte configurations: G a multiple of 32, rows padded to a multiple of 4
+    # words; word configurations: any G, unpadded rows
+    for vec, K, G, ldq in ((True, 4201, 64, 528), (False, 4201, 48, None)):
+        x, Wq, S = workloads.q4_operands(7, K, N, G, ldq=ldq, recipe="q4_int")
         R = oracle.gemv_q4(x, Wq, S, G, N)
         for c in q4_configs:
             if (c["vec"] == 16) != vec:
                 continue
-            print(f"cfg {c['id']} {c['name']} split={c['split']} N={N} K={K} G={G}", flush=True)
+            print(f"cfg {c['id']} {c['name']} N={N} K={K} G={G}", flush=True)
             y1 = _run(x, Wq, S, G, N, cfg=c["id"])
             y2 = _run(x, Wq, S, G, N, cfg=c["id"])
-            assert np.array_equal(y1, R), (c["name"], c["split"], np.flatnonzero(y1 != R)[:10])
+            assert np.array_equal(y1, R), (c["name"], np.flatnonzero(y1 != R)[:10])
             assert np.array_equal(y1, y2)
             n_run += 1
     assert n_run == len(q4_configs)
 
 
-@pytest.mark.parametrize("N,K,G", [(1056, 300, 7), (1056, 300, 1), (1056, 300, 1000), (1056, 1, 128),
-                                   (64, 4096, 128), (8, 77, 4), (13, 130, 32), (1, 33, 2), (4128, 2048, 64)])
-def test_edge_shapes_bit_exact(N, K, G):
-    print(f"N={N} K={K} G={G}", flush=True)
-    x, Wq, S = workloads.q4_operands(N * 7 + K, K, N, G, recipe="q4_int")
+@pytest.mark.parametrize("N,K,G,ldq", [(1037, 300, 7, None), (1037, 300, 1, None), (1037, 300, 1024, 40),
+                                       (1037, 1, 128, 4), (64, 4096, 128, None), (8, 77, 32, None),
+                                       (13, 130, 32, 20), (1, 33, 2, None), (4128, 2048, 64, None),
+                                       (300, 8192, 128, None), (700, 6200, 96, 776)])
+def test_edge_shapes_bit_exact(N, K, G, ldq):
+    print(f"N={N} K={K} G={G} ldq={ldq}", flush=True)
+    x, Wq, S = workloads.q4_operands(N * 7 + K, K, N, G, ldq=ldq, recipe="q4_int")
     R = oracle.gemv_q4(x, Wq, S, G, N)
     assert np.array_equal(_run(x, Wq, S, G, N), R)
 
@@ -84,25 +89,25 @@ def test_edge_shapes_bit_exact(N, K, G):
 def test_k_zero_writes_zeros_and_n_zero_is_noop():
     import torch
     y = torch.full((96,), 7.0, dtype=torch.float32, device="cuda:0")
-    nj.check(nj.nnjit_gemv_q4(96, 0, 128, None, None, 12, None, 96, y, None))
+    nj.check(nj.nnjit_gemv_q4(96, 0, 128, None, None, 0, None, 0, y, None))
     assert np.array_equal(host(y), np.zeros(96))
-    assert nj.nnjit_gemv_q4(0, 64, 32, None, None, 0, None, 0, None, None) == nj.NNJIT_OK
+    assert nj.nnjit_gemv_q4(0, 64, 32, None, None, 8, None, 2, None, None) == nj.NNJIT_OK
 
 
 def test_padded_leading_dimensions():
-    N, K, G = 1056, 300, 64
-    x, Wq, S = workloads.q4_operands(11, K, N, G, ldq=N // 8 + 4, lds=N + 24, recipe="q4_int")
+    N, K, G = 1037, 4200, 64
+    x, Wq, S = workloads.q4_operands(11, K, N, G, ldq=K // 8 + 7 * 4, lds=K // G + 9, recipe="q4_int")
     R = oracle.gemv_q4(x, Wq, S, G, N)
     assert np.array_equal(_run(x, Wq, S, G, N), R)
-    # padding that breaks the 16-byte conditions: the word-load configuration runs
-    x, Wq, S = workloads.q4_operands(12, K, N, G, ldq=N // 8 + 1, lds=N + 3, recipe="q4_int")
+    # a row length that breaks the 16-byte conditions: the word-load configuration runs
+    x, Wq, S = workloads.q4_operands(12, K, N, G, ldq=K // 8 + 1, lds=K // G + 3, recipe="q4_int")
     R = oracle.gemv_q4(x, Wq, S, G, N)
     assert np.array_equal(_run(x, Wq, S, G, N), R)
 
 
 @pytest.mark.parametrize("pad", [1, 3])
 def test_misaligned_operands_use_fallback(pad):
-    N, K, G = 1056, 300, 64
+    N, K, G = 1037, 4200, 64
     x, Wq, S = workloads.q4_operands(13, K, N, G, recipe="q4_int")
     R = oracle.gemv_q4(x, Wq, S, G, N)
     assert np.array_equal(_run(x, Wq, S, G, N, pad=pad), R)
@@ -110,7 +115,7 @@ def test_misaligned_operands_use_fallback(pad):
     import torch
     buf = torch.zeros(Wq.size + 1, dtype=torch.int32, device="cuda:0")
     y = torch.empty(N, dtype=torch.float32, device="cuda:0")
-    rc = nj.nnjit_gemv_q4_config(vec, N, K, G, dev(x), buf[1:], N // 8, dev(S), N, y, None)
+    rc = nj.nnjit_gemv_q4_config(vec, N, K, G, dev(x), buf[1:], K // 8, dev(S), K // G, y, None)
     assert rc == nj.NNJIT_EINVAL
 
 

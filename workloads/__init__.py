@@ -25,10 +25,11 @@ in for real weights and activations):
 
 4-bit weight-only GEMV (dtype ``q4``; the paper's Llama-2-7B decode runs on
 4-bit weights, Sec. 7, without giving the format): x fp16 [K]; the weight
-codes are 32-bit words [K][ldq], eight 4-bit codes per word along N, drawn
-as uniformly random words (every code uniform in 0..15); one fp16 scale per
-group of ``group`` rows and column, uniform in [0.002, 0.01) -- the size of
-max|w| / 7 over a 128-row group of N(0, 0.02) weights.  The exact-arithmetic
+is stored as a linear layer's weight, one row per output: codes are 32-bit
+words [N][ldq], eight 4-bit codes per word along K, drawn as uniformly
+random words (every code uniform in 0..15); one fp16 scale per output and
+group of ``group`` inputs ([N][lds]), uniform in [0.002, 0.01) -- the size of
+max|w| / 7 over a 128-input group of N(0, 0.02) weights.  The exact-arithmetic
 recipe (``q4_int``) takes x in {-8..8} and scales in {1/2, 1, 2, 4}: every
 partial sum is then a multiple of 1/2 below 2^23, exact in fp32.
 
@@ -82,7 +83,7 @@ class Op:
     def weight_bytes(self) -> int:
         """Bytes of the B operand (q4: code words plus scales)."""
         if self.dtype == Q4:
-            return self.K * (-(-self.N // 8)) * 4 + (-(-self.K // self.group)) * self.N * 2
+            return self.N * (-(-self.K // 8)) * 4 + self.N * (-(-self.K // self.group)) * 2
         return self.batch * self.K * self.N * self.elt
 
     @property
@@ -233,26 +234,26 @@ def small_int_operands(seed, batch: int, M: int, K: int, N: int,
 
 def q4_operands(seed, K: int, N: int, group: int, ldq: int | None = None, lds: int | None = None,
                 recipe: str = "q4") -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
-    """(x fp16 [K], Wq uint32 [K, ldq], scales fp16 [ceil(K / group), lds])
-    for a 4-bit weight-only GEMV, from ``default_rng(seed)`` (or a Generator):
-    x first, then the code words, then the scales.  ``ldq`` defaults to
-    ceil(N / 8) and ``lds`` to N; padding words and scales are random too.
+    """(x fp16 [K], Wq uint32 [N, ldq], scales fp16 [N, lds]) for a 4-bit
+    weight-only GEMV, from ``default_rng(seed)`` (or a Generator): x first,
+    then the code words, then the scales.  ``ldq`` defaults to ceil(K / 8) and
+    ``lds`` to ceil(K / group); padding words and scales are random too.
     recipe ``q4``: x N(0, 1), scales uniform [0.002, 0.01); ``q4_int``: x in
     {-8..8}, scales in {1/2, 1, 2, 4} (every partial sum is exact in fp32
     for K below 2^16)."""
     rng = seed if isinstance(seed, np.random.Generator) else np.random.default_rng(seed)
-    ldq = -(-N // 8) if ldq is None else ldq
-    lds = N if lds is None else lds
-    ngroups = -(-K // group) if K > 0 else 0
+    ldq = -(-K // 8) if ldq is None else ldq
+    ngroups = -(-K // group)
+    lds = ngroups if lds is None else lds
     if recipe == "q4":
         x = rng.standard_normal(K, dtype=np.float32).astype(np.float16)
     elif recipe == "q4_int":
         x = rng.integers(-8, 9, size=K).astype(np.float16)
     else:
         raise ValueError(f"unknown q4 recipe {recipe!r}")
-    Wq = rng.integers(0, 1 << 32, size=(K, ldq), dtype=np.uint32)
+    Wq = rng.integers(0, 1 << 32, size=(N, ldq), dtype=np.uint32)
     if recipe == "q4":
-        S = (rng.random((ngroups, lds), dtype=np.float32) * np.float32(0.008) + np.float32(0.002)).astype(np.float16)
+        S = (rng.random((N, lds), dtype=np.float32) * np.float32(0.008) + np.float32(0.002)).astype(np.float16)
     else:
-        S = rng.choice(np.array([0.5, 1.0, 2.0, 4.0], dtype=np.float16), size=(ngroups, lds))
+        S = rng.choice(np.array([0.5, 1.0, 2.0, 4.0], dtype=np.float16), size=(N, lds))
     return np.ascontiguousarray(x), np.ascontiguousarray(Wq), np.ascontiguousarray(S)
