@@ -58,7 +58,11 @@ gemv_kernel(GemvParams p)
 
     const int tid = threadIdx.x;
     const int c = tid % L, rs = tid / L;
-    const int seg = blockIdx.x % p.segs, s = blockIdx.x / p.segs;
+    // consecutive segments on one XCD: narrow segments (L * V * sizeof(T) <
+    // 128 bytes) share cache lines with their neighbours, read once into
+    // that XCD's L2
+    const int logical = xcd_remap(blockIdx.x, gridDim.x);
+    const int seg = logical % p.segs, s = logical / p.segs;
     const int n = seg * CW + c * V;
     const int kbeg = s * p.kchunk;
     const int kend = min(p.K, kbeg + p.kchunk);
@@ -205,6 +209,24 @@ constexpr int lds_gemv(int nthr, int l, int v) { return nthr > 64 ? (nthr / 64) 
     X(_Float16, 64, 256, 2, true) \
     X(_Float16, 64, 1024, 4, true) \
     X(_Float16, 64, 256, 4, false) \
+    X(_Float16, 8, 256, 8, true) \
+    X(_Float16, 8, 512, 8, true) \
+    X(_Float16, 8, 512, 4, true) \
+    X(_Float16, 8, 1024, 4, true) \
+    X(_Float16, 4, 256, 8, true) \
+    X(_Float16, 4, 512, 8, true) \
+    X(_Float16, 4, 512, 4, true) \
+    X(_Float16, 4, 1024, 4, true) \
+    X(float, 8, 256, 8, true) \
+    X(float, 8, 512, 8, true) \
+    X(float, 8, 512, 4, true) \
+    X(float, 8, 1024, 4, true) \
+    X(float, 4, 512, 8, true) \
+    X(float, 8, 1024, 8, true) \
+    X(float, 16, 1024, 8, true) \
+    X(_Float16, 4, 1024, 8, true) \
+    X(_Float16, 8, 1024, 8, true) \
+    X(_Float16, 2, 1024, 8, true) \
 
 #define NNJIT_GEMV_INST(T, L, NTHR, U, VEC) template __global__ void gemv_kernel<T, L, NTHR, U, VEC>(GemvParams);
 NNJIT_GEMV_LIST(NNJIT_GEMV_INST)
