@@ -594,6 +594,7 @@ NNJIT_F32W_LIST(NNJIT_F32W_INST)
     X(256, 256, 16, 2, 2, 32, 2, 1, 1, true) \
     X(256, 128, 16, 4, 2, 32, 2, 1, 1, true) \
     X(256, 128, 16, 4, 2, 32, 2, 2, 1, true) \
+    X(128, 128, 32, 2, 2, 32, 2, 2, 1, true) \
     X(128, 128, 16, 2, 2, 32, 2, 1, 1, true) \
     X(128, 128, 16, 2, 2, 32, 2, 2, 1, true) \
     X(128, 128, 32, 2, 2, 32, 2, 1, 1, true) \
