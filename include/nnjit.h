@@ -42,6 +42,13 @@
  *     threads.  Split-K scratch is kept per (device, stream), so concurrent
  *     calls on different streams do not share it; calls on one stream are
  *     ordered by the stream.
+ *   - Stream capture: a call may be recorded into a HIP graph.  A call whose
+ *     configuration needs more split-K scratch than any earlier call on that
+ *     stream grows it, which synchronises the stream and reallocates; during
+ *     capture such a call enqueues nothing and returns NNJIT_EHIP.  Run each
+ *     shape once on the stream before capturing it.
+ *   - A launch is limited to 2^31 - 1 workgroups (tiles x split x batch slices
+ *     of up to 65535): larger problems return NNJIT_EINVAL.
  *   - Errors: a negative return code; nnjit_last_error() gives a message.
  */
 #ifndef NNJIT_H

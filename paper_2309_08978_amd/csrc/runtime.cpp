@@ -166,6 +166,13 @@ int device_ready(Device **out) {
 int workspace_for(Device &d, hipStream_t stream, int64_t ws_floats, Workspace **out) {
     Workspace &w = d.workspaces[stream];
     if (w.ws_floats < ws_floats) {
+        // growing means waiting for the stream and reallocating, neither of
+        // which a stream under capture allows: refuse instead of breaking it
+        hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+        if (hipStreamIsCapturing(stream, &cap) != hipSuccess) (void)hipGetLastError();
+        if (cap != hipStreamCaptureStatusNone)
+            return fail(NNJIT_EHIP, "split-K scratch of %lld floats needed while the stream is being captured; "
+                                    "run this shape once on the stream outside capture first", (long long)ws_floats);
         hipError_t e = hipStreamSynchronize(stream);  // earlier launches may still use the old buffer
         if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
         const int64_t nf = std::max(w.ws_floats, ws_floats + ws_floats / 4);
@@ -310,6 +317,10 @@ int launch(Device &d, const Config &cfg, const Call &c) {
         p.ws = w ? w->ws : nullptr;
         p.zero = d.zero;
         const int64_t gx = (int64_t)g.tiles_m * g.tiles_n * cfg.split;
+        // the kernels number workgroups (x + gx * z) in 32-bit integers
+        if (gx * std::min<int64_t>(c.batch, 65535) > INT32_MAX)
+            return fail(NNJIT_EINVAL, "%lld workgroups per launch exceed 2^31-1; split the batch or the matrix",
+                        (long long)(gx * std::min<int64_t>(c.batch, 65535)));
         const int elt = c.dtype == NNJIT_F16 ? 2 : 4;
         for (int64_t b0 = 0; b0 < c.batch && e == hipSuccess; b0 += 65535) {
             const int64_t nb = std::min<int64_t>(65535, c.batch - b0);

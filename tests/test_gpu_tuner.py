@@ -121,6 +121,50 @@ def test_graph_replay_matches_eager():
             assert np.array_equal(host(c), e), f"replay {rep}"
 
 
+def test_capture_refuses_split_k_scratch_growth():
+    """A split-K call that would have to grow its stream's scratch while the
+    stream is being captured returns NNJIT_EHIP and enqueues nothing; after
+    one call outside capture the same call captures and every replay gives
+    the oracle's exact sums."""
+    import torch
+    cfg = next(c for c in nj.configs()
+               if c["family"] == "gemm_f32" and c["vec"] == 16 and c["split"] == 4 and not c.get("direct"))
+    M, N, K = 64, 192, 512
+    A, B = workloads.small_int_operands(4242, 1, M, K, N, "f32")
+    R = oracle.matmul(A, B)
+    dA, dB = dev(A), dev(B)
+    nj.matmul(dA, dB)                     # device state initialised outside any capture
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()            # a stream no call has used: no scratch yet
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        C = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda:0")
+    torch.cuda.synchronize()
+
+    def call():
+        return nj.nnjit_matmul_config(cfg["id"], 1, M, N, K, dA, K, 0, dB, N, 0, C, N, 0, nj.NNJIT_F32, side)
+
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        C.fill_(0.0)
+        rc = call()
+    assert rc == nj.NNJIT_EHIP, rc
+    assert "captur" in nj.nnjit_last_error()
+    with torch.cuda.stream(side):
+        assert call() == nj.NNJIT_OK      # outside capture: the scratch grows
+    torch.cuda.synchronize()
+    assert np.array_equal(host(C), R)
+    g2 = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g2, stream=side):
+        assert call() == nj.NNJIT_OK
+    for rep in range(3):
+        C.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g2.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(host(C), R), f"replay {rep}"
+
+
 def test_kernel_database_roundtrip(tmp_path):
     """Tuned shapes survive a save / clear / load cycle; foreign-device,
     unknown-configuration and malformed lines are skipped."""
