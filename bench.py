@@ -10,8 +10,8 @@ The timed steps replay a HIP graph captured from the eager ABI calls (the
 product is launch-bound at these sizes); the eager step time is reported
 beside it.  Inputs are resident in HBM when timing starts.
 
-Prints ONE JSON line.  ``--gpus N`` with N > 1 is refused: this build runs
-on one GPU.
+Prints ONE JSON line.  ``--gpus N`` with N > 1 is refused: the library runs
+on one GPU (products are not sharded across devices).
 """
 from __future__ import annotations
 
@@ -217,7 +217,7 @@ def main(argv=None):
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}, WORLD_SIZE {world}); "
-              "this build has no multi-GPU path", file=sys.stderr)
+              "the library has no multi-GPU path", file=sys.stderr)
         return 2
 
     import torch
