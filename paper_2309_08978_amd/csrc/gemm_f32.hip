@@ -510,6 +510,203 @@ static hipError_t launch_gemm_f32w(const void *params, dim3 grid, hipStream_t st
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Shared-slab direct-copy variant ("gemm_f32t") for large products: the
+// workgroup's waves share one A slab and one B slab per stage, as in
+// gemm_f32_kernel, but the slabs go global -> LDS by global_load_lds_dwordx4
+// (no staging registers, no LDS store instructions) and are waited for by
+// count, with ST stages and one barrier per slab (the register-staged kernel's
+// __syncthreads() drains every load in flight at each slab).
+//
+// Layouts (Kt = 16): A slab [Mt rows][16 floats] with the 16-byte piece p of
+// row r at slot p ^ ((r >> 2) & 3) (as in gemm_f32w); B slab [16 k rows][Nt
+// floats] with the 16-byte piece p of row k at slot p ^ (8 ((k >> 3) & 1)):
+// rows k and k + 8, which the two half-waves read in one ds_read_b32, then
+// sit on opposite halves of the 64 banks.  A copy writes 1 KiB contiguously
+// at a wave-uniform LDS base (lane l at base + 16 l), so both swizzles are
+// made by choosing which global piece each lane fetches.
+template <int MT, int NT, int WM, int WN, int ST>
+__global__ void __launch_bounds__(WM * WN * 64)
+gemm_f32t_kernel(GemmParams p)
+{
+    typedef Mfma32<32> I;
+    typedef typename I::acc_t acc_t;
+    constexpr int KT = 16;
+    constexpr int NW = WM * WN;
+    constexpr int WTM = MT / WM, WTN = NT / WN;
+    constexpr int FM = WTM / 32, FN = WTN / 32;
+    constexpr int A_BYTES = MT * KT * 4;
+    constexpr int B_ROW = NT * 4;
+    constexpr int B_BYTES = KT * B_ROW;
+    constexpr int STAGE = A_BYTES + B_BYTES;
+    constexpr int LA = A_BYTES / 1024 / NW, LB = B_BYTES / 1024 / NW;   // copies per wave and slab
+    constexpr int LC = LA + LB;
+    static_assert(LA * NW * 1024 == A_BYTES && LB * NW * 1024 == B_BYTES, "copies must split evenly over waves");
+    static_assert(NT >= 64 && (NT & (NT - 1)) == 0, "B rows of a power of two >= 256 bytes");
+    static_assert(FM >= 1 && FN >= 1 && WTM % 32 == 0 && WTN % 32 == 0, "wave tile");
+    static_assert(ST >= 2 && (ST - 2) * LC <= 63, "copies in flight exceed the vmcnt range");
+
+    __shared__ __attribute__((aligned(1024))) char smem[ST * STAGE];
+    typedef __attribute__((address_space(3))) char lds_char;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / WN, wn = wave % WN;
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+    const int li = lane & 31, lg = lane >> 5;
+
+    const int tiles = p.tiles_m * p.tiles_n;
+    const int gx = gridDim.x;
+    const int logical = xcd_remap(blockIdx.x + gx * blockIdx.z, gx * gridDim.z);
+    const int z = logical / gx;
+    const int rest = logical - z * gx;
+    const int s = rest / tiles;
+    const int tile = rest - s * tiles;
+    const int tm = tile % p.tiles_m, tn = tile / p.tiles_m;
+    const int m0 = tm * MT, n0 = tn * NT;
+    const int kbeg = s * p.kchunk;
+    const int kend = min(p.K, kbeg + p.kchunk);
+    const int nk = kend > kbeg ? (kend - kbeg + KT - 1) / KT : 0;
+
+    const float *A = (const float *)p.A + (long long)z * p.sA;
+    const float *B = (const float *)p.B + (long long)z * p.sB;
+    float *C = p.C + (long long)z * p.sC;
+    const int M = p.M, N = p.N;
+    const long long lda = p.lda, ldb = p.ldb;
+    const float *zero = (const float *)p.zero;
+    auto stage_base = [&](int u) -> lds_char * { return (lds_char *)smem + u * STAGE; };
+
+    // per-lane sources of this wave's copies for the split's first slab; copy
+    // j of the wave fills 1 KiB chunk c = wave + j NW of the A or B slab
+    const float *a_src[LA];
+    int a_k[LA];
+    bool a_ok[LA];
+#pragma unroll
+    for (int j = 0; j < LA; ++j) {
+        const int row = 16 * (wave + j * NW) + (lane >> 2);
+        const int piece = (lane & 3) ^ ((row >> 2) & 3);
+        a_ok[j] = m0 + row < M;
+        a_k[j] = kbeg + 4 * piece;
+        a_src[j] = A + (long long)(a_ok[j] ? m0 + row : 0) * lda + kbeg + 4 * piece;
+    }
+    const float *b_src[LB];
+    int b_k[LB];
+    bool b_ok[LB];
+#pragma unroll
+    for (int j = 0; j < LB; ++j) {
+        const int o = 1024 * (wave + j * NW) + 16 * lane;
+        const int k = o / B_ROW, slot = (o % B_ROW) >> 4;
+        const int col = 4 * (slot ^ (((k >> 3) & 1) << 3));
+        b_ok[j] = n0 + col < N;
+        b_k[j] = kbeg + k;
+        b_src[j] = B + (long long)(kbeg + k) * ldb + (b_ok[j] ? n0 + col : 0);
+    }
+
+    auto copy_slab = [&](int stage, int kk) {
+        const bool live = kk < nk;
+        const int dk = kk * KT;
+        const long long db = (long long)dk * ldb;
+#pragma unroll
+        for (int j = 0; j < LA; ++j) {
+            const bool ok = live && a_ok[j] && a_k[j] + dk < kend;
+            copy16_to_lds(ok ? a_src[j] + dk : zero, (unsigned)(uintptr_t)(stage_base(stage) + 1024 * (wave_u + j * NW)));
+        }
+#pragma unroll
+        for (int j = 0; j < LB; ++j) {
+            const bool ok = live && b_ok[j] && b_k[j] + dk < kend;
+            copy16_to_lds(ok ? b_src[j] + db : zero,
+                          (unsigned)(uintptr_t)(stage_base(stage) + A_BYTES + 1024 * (wave_u + j * NW)));
+        }
+    };
+
+    acc_t acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int r = 0; r < I::NR; ++r) acc[i][j][r] = 0.f;
+
+    // one slab: lane group g takes k in [8g, 8g + 8); every fragment read is
+    // issued before the first MFMA
+    auto compute = [&](int stage) {
+        lds_char *sa = stage_base(stage);
+        lds_char *sb = sa + A_BYTES;
+        f32x8 a[FM];
+        float b[8][FN];
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+            const int row = wm * WTM + 32 * i + li;
+            const int sw = (row >> 2) & 3;
+            const f32x4 lo = *(__attribute__((address_space(3))) f32x4 *)(sa + row * 64 + 16 * ((2 * lg) ^ sw));
+            const f32x4 hi = *(__attribute__((address_space(3))) f32x4 *)(sa + row * 64 + 16 * ((2 * lg + 1) ^ sw));
+            a[i] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        }
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            lds_char *brow = sb + (8 * lg + t) * B_ROW;
+#pragma unroll
+            for (int j = 0; j < FN; ++j) {
+                const int cc = wn * WTN + 32 * j + li;
+                b[t][j] = *(__attribute__((address_space(3))) float *)(brow + 16 * ((cc >> 2) ^ (lg << 3)) + 4 * (cc & 3));
+            }
+        }
+#pragma unroll
+        for (int t = 0; t < 8; ++t)
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j) acc[i][j] = I::mma(a[i][t], b[t][j], acc[i][j]);
+        __builtin_amdgcn_sched_group_barrier(0x100, FM * 2 + 8 * FN, 0);   // all LDS reads first
+        __builtin_amdgcn_sched_group_barrier(0x008, 8 * FM * FN, 0);       // then the MFMAs
+    };
+
+    // slab kk is copied into stage kk % ST while slab kk - ST + 1 is
+    // multiplied; one barrier per slab
+#pragma unroll
+    for (int u = 0; u < ST - 1; ++u) copy_slab(u, u);
+    for (int it0 = 0; it0 < nk; it0 += ST) {
+#pragma unroll
+        for (int u = 0; u < ST; ++u) {
+            const int it = it0 + u;
+            // this wave's copies of slab it are done once at most the copies
+            // of the ST - 2 later slabs are pending; the barrier then makes
+            // every wave's copies visible and frees the stage multiplied in
+            // the previous iteration
+            wait_vmcnt<(ST - 2) * LC>();
+            lds_barrier();
+            copy_slab((u + ST - 1) % ST, it + ST - 1);
+            if (it < nk) compute(u);
+        }
+    }
+    wait_vmcnt<0>();   // no copy may still target LDS when the workgroup ends
+
+    const int rbase = m0 + wm * WTM, cbase = n0 + wn * WTN + li;
+    float *out = C;
+    long long ldo = p.ldc;
+    if (p.S > 1) {
+        out = p.ws + ((long long)s * p.batch + z) * (long long)M * N;
+        ldo = N;
+    }
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int r = 0; r < I::NR; ++r) {
+                const int row = rbase + 32 * i + I::row_of(r, lg), col = cbase + 32 * j;
+                if (row < M && col < N) out[(long long)row * ldo + col] = acc[i][j][r];
+            }
+}
+
+template <int MT, int NT, int WM, int WN, int ST>
+static hipError_t launch_gemm_f32t(const void *params, dim3 grid, hipStream_t stream)
+{
+    hipLaunchKernelGGL((gemm_f32t_kernel<MT, NT, WM, WN, ST>), grid, dim3(WM * WN * 64), 0, stream,
+                       *(const GemmParams *)params);
+    return hipGetLastError();
+}
+
 constexpr int lds_f32(int mt, int nt, int kt, int st, int ks) {
     return (ks * st * (mt * (kt == 16 ? kt : kt + 4) + kt * (nt + 4)) > (ks - 1) * mt * nt
                 ? ks * st * (mt * (kt == 16 ? kt : kt + 4) + kt * (nt + 4))
@@ -643,6 +840,36 @@ NNJIT_F32W_LIST(NNJIT_F32W_INST)
     X(64, 64, 16, 2, 2, 32, 2, 1, 1, false) \
     X(32, 32, 16, 1, 1, 32, 2, 1, 1, false)
 
+// Shared-slab direct-copy variants: accumulators, one slab of fragments, the
+// per-lane copy geometry (2 registers per copy) and a fixed overhead.
+constexpr int est_regs_f32t(int mt, int nt, int wm, int wn) {
+    return (mt / wm) * (nt / wn) / 64 + 8 * ((mt / wm) / 32) + 8 * ((nt / wn) / 32) +
+           2 * ((mt * 64 + 64 * nt) / 1024 / (wm * wn)) + 32;
+}
+constexpr int lds_f32t(int mt, int nt, int st) { return st * (mt * 64 + 64 * nt); }
+#define NNJIT_F32T_VARIANT(MT, NT, WM, WN, ST)                                                                \
+    {"gemm_f32t_" #MT "x" #NT "x16_w" #WM "x" #WN "_s" #ST, FAM_GEMM_F32, 32, 2, MT, NT, 16, WM, WN, ST, ST - 1, \
+     1, 16, 0, 0, WM * WN * 64, lds_f32t(MT, NT, ST), est_regs_f32t(MT, NT, WM, WN),                          \
+     (const void *)&gemm_f32t_kernel<MT, NT, WM, WN, ST>, &launch_gemm_f32t<MT, NT, WM, WN, ST>, 1}
+
+// The compiled shared-slab direct-copy configurations (16-byte aligned
+// operands, Nt >= 64).
+#define NNJIT_F32T_LIST(X) \
+    X(256, 128, 4, 2, 3) \
+    X(256, 128, 4, 2, 4) \
+    X(128, 256, 2, 4, 4) \
+    X(256, 256, 2, 4, 3) \
+    X(256, 256, 4, 2, 3) \
+    X(128, 128, 2, 2, 3) \
+    X(128, 128, 2, 2, 4) \
+    X(128, 128, 2, 4, 4) \
+    X(128, 64, 2, 1, 4) \
+    X(64, 128, 1, 2, 4) \
+    X(64, 64, 2, 2, 4)
+
+#define NNJIT_F32T_INST(MT, NT, WM, WN, ST) template __global__ void gemm_f32t_kernel<MT, NT, WM, WN, ST>(GemmParams);
+NNJIT_F32T_LIST(NNJIT_F32T_INST)
+
 #define NNJIT_F32_INST(MT, NT, KT, WM, WN, MF, ST, PF, KS, VEC) \
     template __global__ void gemm_f32_kernel<MT, NT, KT, WM, WN, MF, ST, PF, KS, VEC>(GemmParams);
 NNJIT_F32_LIST(NNJIT_F32_INST)
@@ -650,7 +877,9 @@ NNJIT_F32_LIST(NNJIT_F32_INST)
 #if !defined(__HIP_DEVICE_COMPILE__)
 #define NNJIT_F32_ENTRY(...) NNJIT_F32_VARIANT(__VA_ARGS__),
 #define NNJIT_F32W_ENTRY(...) NNJIT_F32W_VARIANT(__VA_ARGS__),
-const Variant kGemmF32Variants[] = {NNJIT_F32_LIST(NNJIT_F32_ENTRY) NNJIT_F32W_LIST(NNJIT_F32W_ENTRY)};
+#define NNJIT_F32T_ENTRY(...) NNJIT_F32T_VARIANT(__VA_ARGS__),
+const Variant kGemmF32Variants[] = {NNJIT_F32_LIST(NNJIT_F32_ENTRY) NNJIT_F32W_LIST(NNJIT_F32W_ENTRY)
+                                        NNJIT_F32T_LIST(NNJIT_F32T_ENTRY)};
 const int kNumGemmF32Variants = sizeof(kGemmF32Variants) / sizeof(kGemmF32Variants[0]);
 #endif
 
