@@ -578,6 +578,7 @@ constexpr int lds_f16t(int mt, int nt, int kt, int st) { return st * (mt + nt) *
 // The compiled direct-copy configurations (16-byte aligned operands, Nt >= 128).
 #define NNJIT_F16T_LIST(X) \
     X(256, 256, 64, 4, 2, 32, 2) \
+    X(256, 128, 64, 4, 4, 32, 3) \
     X(256, 256, 64, 2, 4, 32, 2) \
     X(256, 256, 32, 2, 4, 32, 4) \
     X(256, 256, 32, 2, 4, 32, 5) \
