@@ -121,6 +121,9 @@ def test_resource_limits_follow_the_formula(lib):
         assert r["lds_limit"] == (min(163840 // r["lds_per_wg"], 1 << 20) if r["lds_per_wg"] > 0 else 1 << 20)
         assert r["wave_limit"] == 32 // r["waves_per_wg"]
         assert r["wg_per_cu"] == min(r["reg_limit"], r["lds_limit"], r["wave_limit"])
+        # every compiled configuration fits one CDNA4 CU: LDS and workgroup size limits
+        assert 0 <= r["lds_per_wg"] <= 163840, c["name"]
+        assert c["threads"] <= 1024, c["name"]
 
 
 def _kind(op):
