@@ -279,3 +279,24 @@ def test_transpose_identity(dt):
     R = oracle.matmul(A, B)
     assert accept.check(C, R, A, B, dt)["ok"]
     assert accept.check(Ct, R, A, B, dt)["ok"]
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16"])
+def test_batch_beyond_one_launch(all_configs, dt):
+    """70 001 batch slices: more than the 65 535 a launch's grid.z holds, so
+    the batch is cut into several launches (and, with split-K, several
+    reductions over the matching slices of the scratch).  Small integers:
+    bit-exact against the oracle, on the default configuration and on a
+    forced split-K configuration."""
+    import torch
+    batch, M, N, K = 70001, 3, 8, 40
+    A, B = workloads.small_int_operands(31337, batch, M, K, N, dt)
+    R = oracle.matmul(A, B)
+    dA, dB = dev(A), dev(B)
+    C = nj.batched_matmul(dA, dB)
+    assert np.array_equal(host(C), R)
+    fam = "gemm_f16" if dt == "f16" else "gemm_f32"
+    cfg = next(c for c in all_configs if c["family"] == fam and c["vec"] == 16 and c["split"] == 4 and c["Mt"] <= 64)
+    C2 = torch.full(R.shape, float("nan"), dtype=torch.float32, device="cuda:0")
+    nj.batched_matmul(dA, dB, C2, cfg=cfg["id"])
+    assert np.array_equal(host(C2), R), f"config {cfg['name']} split={cfg['split']}"
