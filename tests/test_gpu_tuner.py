@@ -264,3 +264,51 @@ def test_online_tuning_serves_every_call_and_converges():
     nj.matmul(dA, dB, C)
     assert np.array_equal(host(C), R)
     nj.nnjit_cache_clear()
+
+
+def test_concurrent_host_threads_on_own_streams():
+    """Four host threads, each on its own stream, alternate default-config
+    calls and a forced split-K configuration (each stream's own scratch in use
+    at once) while a fifth thread tunes another shape: every result is the
+    oracle's exact sum (small integers)."""
+    import threading
+    import torch
+    cfg = next(c for c in nj.configs()
+               if c["family"] == "gemm_f32" and c["vec"] == 16 and c["split"] == 4 and c["Mt"] <= 64)
+    shapes = [(96, 136, 264), (64, 200, 512), (130, 72, 320), (48, 256, 400)]
+    results, errors = {}, []
+
+    def worker(t):
+        try:
+            M, N, K = shapes[t]
+            A, B = workloads.small_int_operands(9100 + t, 1, M, K, N, "f32")
+            R = oracle.matmul(A, B)
+            s = torch.cuda.Stream()
+            with torch.cuda.stream(s):
+                dA = torch.from_numpy(A).to("cuda:0")
+                dB = torch.from_numpy(B).to("cuda:0")
+                ok = True
+                for it in range(16):
+                    C = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda:0")
+                    nj.matmul(dA, dB, C, stream=s, cfg=cfg["id"] if it % 2 else None)
+                    s.synchronize()
+                    ok = ok and np.array_equal(C.cpu().numpy().astype(np.float64), R)
+            results[t] = ok
+        except Exception as e:   # reported below
+            errors.append(repr(e))
+
+    def tuner():
+        try:
+            nj.check(nj.nnjit_tune(256, 512, 1024, nj.NNJIT_F32))
+        except Exception as e:
+            errors.append(repr(e))
+
+    nj.matmul(dev(np.ones((4, 8), np.float32)), dev(np.ones((8, 8), np.float32)))   # device state initialised
+    torch.cuda.synchronize()
+    threads = [threading.Thread(target=worker, args=(t,)) for t in range(4)] + [threading.Thread(target=tuner)]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join(timeout=120)
+    assert not errors, errors
+    assert results == {0: True, 1: True, 2: True, 3: True}
