@@ -300,3 +300,51 @@ def test_batch_beyond_one_launch(all_configs, dt):
     C2 = torch.full(R.shape, float("nan"), dtype=torch.float32, device="cuda:0")
     nj.batched_matmul(dA, dB, C2, cfg=cfg["id"])
     assert np.array_equal(host(C2), R), f"config {cfg['name']} split={cfg['split']}"
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16"])
+def test_gemv_split_k_back_to_back_and_replayed(all_configs, dt):
+    """Split-K GEMV: launches of different configurations, splits and column
+    segment counts back to back on one stream (no host synchronisation
+    between them, each reduction reading the scratch its own GEMV just
+    wrote), then a graph of three of them replayed four times: every result
+    is the oracle's exact sum (small integers)."""
+    import torch
+    fam = "gemv_" + dt
+    split = [c for c in all_configs if c["family"] == fam and c["vec"] == 16 and c["split"] > 1]
+    assert split
+    picks = split[:: max(1, len(split) // 8)][:8]
+    shapes = [(1, 2056, 4096), (1, 1032, 997), (1, 8192, 3000), (1, 264, 5000)]   # (M, N, K)
+    cases = []
+    for i, c in enumerate(picks):
+        M, N, K = shapes[i % len(shapes)]
+        A, B = workloads.small_int_operands(7300 + i, 1, M, K, N, dt)
+        cases.append((c, dev(A), dev(B), oracle.matmul(A, B)))
+    outs = [torch.full(R.shape, float("nan"), dtype=torch.float32, device="cuda:0") for _, _, _, R in cases]
+    for (c, dA, dB, _), C in zip(cases, outs):
+        nj.matmul(dA, dB, C, cfg=c["id"])
+    torch.cuda.synchronize()
+    for (c, _, _, R), C in zip(cases, outs):
+        assert np.array_equal(host(C), R), f"config {c['name']} split={c['split']}"
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    trio = cases[:3]
+
+    def step():
+        for (c, dA, dB, _), C in zip(trio, outs):
+            nj.matmul(dA, dB, C, stream=side, cfg=c["id"])
+    with torch.cuda.stream(side):
+        step()   # scratch and counters of the side stream allocated outside capture
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        step()
+    for rep in range(4):
+        for C in outs:
+            C.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for (c, _, _, R), C in zip(trio, outs):
+            assert np.array_equal(host(C), R), f"replay {rep}: config {c['name']} split={c['split']}"
