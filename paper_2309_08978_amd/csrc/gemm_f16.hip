@@ -407,6 +407,23 @@ gemm_f16t_kernel(GemmParams p)
                           (unsigned)(uintptr_t)(stage_base(stage) + A_BYTES + 1024 * (wave_u + j * NW)));
         }
     };
+    // the same copies for a slab that lies wholly inside [kbeg, kend): no
+    // checks (rows past M and columns past N were pointed at row / column 0
+    // above; what they bring reaches only outputs that are never stored)
+    auto copy_full = [&](int stage, int kk) {
+        const int dk = kk * KT;
+        const long long db = (long long)dk * ldb;
+#pragma unroll
+        for (int j = 0; j < LA; ++j) {
+            copy16_to_lds(a_src[j] + dk, (unsigned)(uintptr_t)(stage_base(stage) + 1024 * (wave_u + j * NW)));
+        }
+#pragma unroll
+        for (int j = 0; j < LB; ++j) {
+            copy16_to_lds(b_src[j] + db,
+                          (unsigned)(uintptr_t)(stage_base(stage) + A_BYTES + 1024 * (wave_u + j * NW)));
+        }
+    };
+    const int nfull = kend > kbeg ? (kend - kbeg) / KT : 0;   // whole slabs of the range
 
     acc_t acc[FM][FN];
 #pragma unroll
@@ -469,14 +486,29 @@ gemm_f16t_kernel(GemmParams p)
 
 #pragma unroll
     for (int u = 0; u < ST - 1; ++u) copy_slab(u, u);
-    for (int it0 = 0; it0 < nk; it0 += ST) {
+    // ST slabs at a time.  While every slab copied in a group is whole (and
+    // so is every slab multiplied), the group is one branch-free block with
+    // unchecked copies that the scheduler can place among the MFMAs; the
+    // rest runs with checked copies and a guard per slab.  Both issue the
+    // same copies per slab, so the counted waits are the same.
+    int it0 = 0;
+    for (; it0 + 2 * ST - 1 <= nfull; it0 += ST) {
 #pragma unroll
         for (int u = 0; u < ST; ++u) {
-            const int it = it0 + u;
-            // this wave's copies of slab `it` are done once at most the
+            // this wave's copies of slab it0 + u are done once at most the
             // copies of the ST - 2 later slabs are pending; the barrier
             // then makes every wave's copies visible and frees the stage
             // multiplied in the previous iteration
+            wait_vmcnt<(ST - 2) * (LA + LB)>();
+            lds_barrier();
+            copy_full((u + ST - 1) % ST, it0 + u + ST - 1);
+            compute(u);
+        }
+    }
+    for (; it0 < nk; it0 += ST) {
+#pragma unroll
+        for (int u = 0; u < ST; ++u) {
+            const int it = it0 + u;
             wait_vmcnt<(ST - 2) * (LA + LB)>();
             lds_barrier();
             copy_slab((u + ST - 1) % ST, it + ST - 1);

@@ -360,7 +360,7 @@ gemm_f32w_kernel(GemmParams p)
     const int kbeg = s * p.kchunk;
     const int kend = min(p.K, kbeg + p.kchunk);
     const int nk = kend > kbeg ? (kend - kbeg + KT - 1) / KT : 0;
-    const int nmine = nk > wave ? (nk - wave + KS - 1) / KS : 0;    // slabs of this wave
+    const int nmine = nk > wave_u ? (nk - wave_u + KS - 1) / KS : 0;    // slabs of this wave
 
     const float *A = (const float *)p.A + (long long)z * p.sA;
     const float *B = (const float *)p.B + (long long)z * p.sB;
@@ -397,7 +397,7 @@ gemm_f32w_kernel(GemmParams p)
     // copy this wave's kk-th slab into stage st (past the wave's last slab the
     // sources are the zero buffer, so every wave issues the same copies)
     auto copy_slab = [&](int st, int kk) {
-        const int sl = wave + kk * KS;
+        const int sl = wave_u + kk * KS;
         const bool live = sl < nk;
         const int dk = sl * KT;
         const long long db = (long long)dk * ldb;
@@ -413,6 +413,21 @@ gemm_f32w_kernel(GemmParams p)
             copy16_to_lds(ok ? b_src[c] + db : zero, (unsigned)(uintptr_t)(dst + A_BYTES + B_CHUNK * c));
         }
     };
+    // the same copies for a slab that lies wholly inside [kbeg, kend): no
+    // checks (rows past M and columns past N were pointed at row / column 0
+    // above; what they bring reaches only outputs that are never stored)
+    auto copy_full = [&](int st, int kk) {
+        const int dk = (wave_u + kk * KS) * KT;
+        const long long db = (long long)dk * ldb;
+        lds_char *dst = mine + st * STAGE;
+#pragma unroll
+        for (int c = 0; c < NA; ++c) copy16_to_lds(a_src[c] + dk, (unsigned)(uintptr_t)(dst + 1024 * c));
+#pragma unroll
+        for (int c = 0; c < NBC; ++c)
+            copy16_to_lds(b_src[c] + db, (unsigned)(uintptr_t)(dst + A_BYTES + B_CHUNK * c));
+    };
+    const int nfull = kend > kbeg ? (kend - kbeg) / KT : 0;                    // whole slabs of the range
+    const int nfull_mine = nfull > wave_u ? (nfull - wave_u + KS - 1) / KS : 0;  // ... of this wave
 
     acc_t acc[FM][FN];
 #pragma unroll
@@ -422,14 +437,10 @@ gemm_f32w_kernel(GemmParams p)
 #pragma unroll
             for (int r = 0; r < I::NR; ++r) acc[i][j][r] = 0.f;
 
-    // one slab: every fragment read is issued before the first MFMA (the
-    // reads return in order, so MFMA t waits only for the reads it uses and
-    // the LDS latency is paid once per slab rather than once per step)
-    auto compute = [&](int st) {
+    // fragments of one slab: FM A rows of 8 k, 8 k rows of FN B columns
+    auto read_frags = [&](int st, f32x8 (&a)[FM], float (&b)[8][FN]) {
         lds_char *sa = mine + st * STAGE;
         lds_char *sb = sa + A_BYTES;
-        f32x8 a[FM];
-        float b[8][FN];
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
             const int row = 32 * i + li;
@@ -445,25 +456,88 @@ gemm_f32w_kernel(GemmParams p)
 #pragma unroll
             for (int j = 0; j < FN; ++j) b[t][j] = *(__attribute__((address_space(3))) float *)(brow + 4 * (32 * j + li));
         }
+    };
+    auto mma_slab = [&](const f32x8 (&a)[FM], const float (&b)[8][FN]) {
 #pragma unroll
         for (int t = 0; t < 8; ++t)
 #pragma unroll
             for (int i = 0; i < FM; ++i)
 #pragma unroll
                 for (int j = 0; j < FN; ++j) acc[i][j] = I::mma(a[i][t], b[t][j], acc[i][j]);
+    };
+
+    // one slab: every fragment read is issued before the first MFMA (the
+    // reads return in order, so MFMA t waits only for the reads it uses and
+    // the LDS latency is paid once per slab rather than once per step)
+    auto compute = [&](int st) {
+        f32x8 a[FM];
+        float b[8][FN];
+        read_frags(st, a, b);
+        mma_slab(a, b);
         __builtin_amdgcn_sched_group_barrier(0x100, FM * 2 + 8 * FN, 0);   // all LDS reads first
         __builtin_amdgcn_sched_group_barrier(0x008, 8 * FM * FN, 0);       // then the MFMAs
     };
 
 #pragma unroll
     for (int u = 0; u < ST - 1; ++u) copy_slab(u, u);
-    for (int it0 = 0; it0 < nmine; it0 += ST) {
+    // ST iterations at a time.  While every slab copied in a group is whole
+    // (and so is every slab multiplied), the group is one branch-free block:
+    // unchecked copies that the scheduler can place among the MFMAs.  The
+    // rest runs with checked copies and a guard per slab.  Both issue NCOPY
+    // copies per iteration, so the counted waits are the same.
+    int it0 = 0;
+    if constexpr (ST >= 4 && FM * FN >= 2) {
+        static_assert(ST % 2 == 0, "the two register sets alternate within a group of ST slabs");
+        // with four or more stages and at least two accumulator tiles (a
+        // slab of >= 16 MFMAs, long enough to cover a copy with one fewer
+        // slab in flight) the group also reads slab it + 1 into a second
+        // register set while the MFMAs of slab it run (the reads interleaved
+        // with them), keeping ST - 3 slabs' copies in flight
+        if (2 * ST - 1 <= nfull_mine) {
+            f32x8 fa[2][FM];
+            float fb[2][8][FN];
+            wait_vmcnt<(ST - 2) * NCOPY>();   // slab 0
+            read_frags(0, fa[0], fb[0]);
+            for (; it0 + 2 * ST - 1 <= nfull_mine; it0 += ST) {
+#pragma unroll
+                for (int u = 0; u < ST; ++u) {
+                    // slab it0 + u + 1 has landed once at most the ST - 3
+                    // slabs after it are pending; this wave's reads of the
+                    // stage about to be refilled (slab it0 + u - 1) are done
+                    wait_vmcnt<(ST - 3) * NCOPY>();
+                    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+                    copy_full((u + ST - 1) % ST, it0 + u + ST - 1);
+                    read_frags((u + 1) % ST, fa[(u + 1) & 1], fb[(u + 1) & 1]);
+                    mma_slab(fa[u & 1], fb[u & 1]);
+#pragma unroll
+                    for (int q = 0; q < 8 * FM * FN; ++q) {
+                        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+                        if (q < FM * 2 + 8 * FN) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
+                    }
+                }
+            }
+            // the reads of slab it0 issued by the last group are not used: the
+            // loop below reads every slab it multiplies itself
+        }
+    } else {
+        for (; it0 + 2 * ST - 1 <= nfull_mine; it0 += ST) {
+#pragma unroll
+            for (int u = 0; u < ST; ++u) {
+                // slab it0 + u has landed once at most the ST - 2 later
+                // slabs' copies are pending; this wave's reads of the stage
+                // about to be refilled (multiplied in the previous iteration)
+                // are complete
+                wait_vmcnt<(ST - 2) * NCOPY>();
+                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+                copy_full((u + ST - 1) % ST, it0 + u + ST - 1);
+                compute(u);
+            }
+        }
+    }
+    for (; it0 < nmine; it0 += ST) {
 #pragma unroll
         for (int u = 0; u < ST; ++u) {
             const int it = it0 + u;
-            // slab it has landed once at most the ST - 2 later slabs' copies
-            // are pending; this wave's reads of the stage about to be
-            // refilled (multiplied in the previous iteration) are complete
             wait_vmcnt<(ST - 2) * NCOPY>();
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
             copy_slab((u + ST - 1) % ST, it + ST - 1);
@@ -618,6 +692,23 @@ gemm_f32t_kernel(GemmParams p)
                           (unsigned)(uintptr_t)(stage_base(stage) + A_BYTES + 1024 * (wave_u + j * NW)));
         }
     };
+    // the same copies for a slab that lies wholly inside [kbeg, kend): no
+    // checks (rows past M and columns past N were pointed at row / column 0
+    // above; what they bring reaches only outputs that are never stored)
+    auto copy_full = [&](int stage, int kk) {
+        const int dk = kk * KT;
+        const long long db = (long long)dk * ldb;
+#pragma unroll
+        for (int j = 0; j < LA; ++j) {
+            copy16_to_lds(a_src[j] + dk, (unsigned)(uintptr_t)(stage_base(stage) + 1024 * (wave_u + j * NW)));
+        }
+#pragma unroll
+        for (int j = 0; j < LB; ++j) {
+            copy16_to_lds(b_src[j] + db,
+                          (unsigned)(uintptr_t)(stage_base(stage) + A_BYTES + 1024 * (wave_u + j * NW)));
+        }
+    };
+    const int nfull = kend > kbeg ? (kend - kbeg) / KT : 0;   // whole slabs of the range
 
     acc_t acc[FM][FN];
 #pragma unroll
@@ -665,14 +756,29 @@ gemm_f32t_kernel(GemmParams p)
     // multiplied; one barrier per slab
 #pragma unroll
     for (int u = 0; u < ST - 1; ++u) copy_slab(u, u);
-    for (int it0 = 0; it0 < nk; it0 += ST) {
+    // ST slabs at a time.  While every slab copied in a group is whole (and
+    // so is every slab multiplied), the group is one branch-free block with
+    // unchecked copies that the scheduler can place among the MFMAs; the
+    // rest runs with checked copies and a guard per slab.  Both issue the
+    // same copies per slab, so the counted waits are the same.
+    int it0 = 0;
+    for (; it0 + 2 * ST - 1 <= nfull; it0 += ST) {
 #pragma unroll
         for (int u = 0; u < ST; ++u) {
-            const int it = it0 + u;
-            // this wave's copies of slab it are done once at most the copies
+            // this wave's copies of slab it0 + u are done once at most the copies
             // of the ST - 2 later slabs are pending; the barrier then makes
             // every wave's copies visible and frees the stage multiplied in
             // the previous iteration
+            wait_vmcnt<(ST - 2) * LC>();
+            lds_barrier();
+            copy_full((u + ST - 1) % ST, it0 + u + ST - 1);
+            compute(u);
+        }
+    }
+    for (; it0 < nk; it0 += ST) {
+#pragma unroll
+        for (int u = 0; u < ST; ++u) {
+            const int it = it0 + u;
             wait_vmcnt<(ST - 2) * LC>();
             lds_barrier();
             copy_slab((u + ST - 1) % ST, it + ST - 1);
@@ -751,6 +857,7 @@ constexpr int lds_f32w(int mt, int nt, int ks, int st) {
     X(32, 32, 8, 4) \
     X(32, 64, 4, 4) \
     X(64, 64, 4, 3) \
+    X(64, 64, 4, 4) \
     X(128, 32, 4, 3) \
     X(32, 128, 4, 3)
 
