@@ -80,6 +80,7 @@ struct Tuned {
     std::vector<std::pair<int, double>> ranked;   // up to kRanked (config, us): the registered one, then the fastest others
 };
 constexpr int kRanked = 5;
+constexpr int kRunoff = 4;   // candidates re-timed in the tuner's run-off
 std::map<ShapeKey, Tuned> g_tuned;
 std::map<ShapeKey, int> g_default;
 
@@ -717,8 +718,59 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
         best_first_us = std::min(best_first_us, first_us);
     }
     destroy();
-    t_stats.eval_ms = ms_since(te);
     if (best < 0) return fail(NNJIT_ENOCFG, "every candidate failed");
+
+    // Run-off: the candidates within 10% of the best (at most kRunoff) are
+    // timed again with bursts of >= ~150 us, taking turns over several
+    // rounds so that clock drift reaches them alike; each keeps the median
+    // of its rounds.  Short bursts of a few-microsecond kernel cannot tell
+    // such candidates apart.
+    if (env_int("NNJIT_TUNE_RUNOFF", 1) != 0 && ms_since(te) < budget_ms) {
+        std::vector<std::pair<double, int>> close;
+        for (const auto &kv : timed)
+            if (kv.second <= best_us * 1.10) close.emplace_back(kv.second, kv.first);
+        std::sort(close.begin(), close.end());
+        if ((int)close.size() > kRunoff) close.resize(kRunoff);
+        if (close.size() >= 2) {
+            const int rounds = 5;
+            const int burst2 = std::min(64, std::max(burst, (int)std::ceil(150.0 / std::max(best_us, 0.1))));
+            const int nc = (int)close.size();
+            std::vector<hipEvent_t> rev(2 * nc * rounds);
+            bool ok = true;
+            for (auto &x : rev)
+                if (hipEventCreate(&x) != hipSuccess) ok = false;
+            for (int r = 0; r < rounds && ok; ++r)
+                for (int j = 0; j < nc && ok; ++j) {
+                    const Config &cfg = configs()[close[j].second];
+                    (void)hipEventRecord(rev[2 * (r * nc + j)], c.stream);
+                    for (int b = 0; b < burst2 && ok; ++b) ok = launch_next(cfg) == NNJIT_OK;
+                    (void)hipEventRecord(rev[2 * (r * nc + j) + 1], c.stream);
+                }
+            if (ok && hipEventSynchronize(rev.back()) == hipSuccess) {
+                best_us = 1e300;
+                for (int j = 0; j < nc; ++j) {
+                    std::vector<float> ts(rounds);
+                    for (int r = 0; r < rounds; ++r)
+                        (void)hipEventElapsedTime(&ts[r], rev[2 * (r * nc + j)], rev[2 * (r * nc + j) + 1]);
+                    const double us = median(ts) * 1e3 / burst2;
+                    timed[close[j].second] = us;
+                    if (trace)
+                        fprintf(stderr, "[nnjit] tune run-off %d %s S=%d %.2f us (was %.2f)\n", close[j].second,
+                                configs()[close[j].second].v->name, configs()[close[j].second].split, us, close[j].first);
+                }
+                for (const auto &kv : timed)
+                    if (kv.second < best_us) {
+                        best_us = kv.second;
+                        best = kv.first;
+                    }
+            } else {
+                (void)hipGetLastError();
+                (void)hipStreamSynchronize(c.stream);
+            }
+            for (auto &x : rev) (void)hipEventDestroy(x);
+        }
+    }
+    t_stats.eval_ms = ms_since(te);
     // the registered kernel (cached, else the default) is replaced only by one
     // that is significantly (>= 3%) faster
     int incumbent = hit != g_tuned.end() ? hit->second.cfg : lr.ids[0];
