@@ -100,6 +100,32 @@ def test_direct_copy_configs_short_k(all_configs, K):
     assert n > 0
 
 
+
+@pytest.mark.parametrize("K", [1024, 1064])
+def test_direct_copy_configs_long_k(all_configs, K):
+    """Direct-copy configurations, every split, with K long enough that each
+    wave (or workgroup) runs the branch-free main loop over whole K slabs
+    with unchecked copies before the checked loop takes the rest: whole slabs
+    only (K = 1024) and a ragged last slab (K = 1064), with M and N ragged
+    against every tile (rows and columns past the edge are read from row /
+    column 0 in the main loop and never stored).  Small integers: the
+    oracle's exact sums."""
+    import torch
+    n = 0
+    for family in ("gemm_f32", "gemm_f16"):
+        A, B = workloads.small_int_operands(5150 + K, 1, 70, K, 136, FAMILY_DTYPE[family])
+        R = oracle.matmul(A, B)
+        dA, dB = dev(A), dev(B)
+        for c in all_configs:
+            if c["family"] != family or not c.get("direct"):
+                continue
+            C = torch.full(R.shape, float("nan"), dtype=torch.float32, device="cuda:0")
+            nj.matmul(dA, dB, C, cfg=c["id"])
+            assert np.array_equal(host(C), R), f"config {c['id']} {c['name']} split={c['split']} K={K}"
+            n += 1
+    assert n > 0
+    print(f"K={K}: {n} direct-copy configurations bit-exact", flush=True)
+
 def _sample_idx(rng, shape, n=1500):
     """Random output positions plus the corners and the ragged edges."""
     if len(shape) == 2:
