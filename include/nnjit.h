@@ -50,6 +50,22 @@
  *   - A launch is limited to 2^31 - 1 workgroups (tiles x split x batch slices
  *     of up to 65535): larger problems return NNJIT_EINVAL.
  *   - Errors: a negative return code; nnjit_last_error() gives a message.
+ *
+ * Environment variables (read at each call; none is needed)
+ *   NNJIT_TUNE_BUDGET_MS  wall-time budget of one shape's tuning (default 900)
+ *   NNJIT_TUNE_REPS       timed bursts per candidate (default 3)
+ *   NNJIT_TUNE_RUNOFF     0 skips the re-timing of the near-best candidates
+ *   NNJIT_RETUNE          non-zero: tune a shape again even if it is cached
+ *   NNJIT_FORCE_CONFIG    configuration id used for every call of its family
+ *                         (for experiments; results are the same, speed not)
+ *   NNJIT_GROUP_M         tile rows per group of a GEMM's tile order
+ *                         (default: chosen per launch; any value gives the
+ *                         same results)
+ *   NNJIT_LOG, NNJIT_TRACE  non-zero: print each tuned shape / each timed
+ *                         candidate to stderr
+ *   NNJIT_FAULT_CONFIG    configuration id whose launches fail with
+ *                         NNJIT_EHIP before any GPU work (tests of the
+ *                         tuner's failure handling)
  */
 #ifndef NNJIT_H
 #define NNJIT_H

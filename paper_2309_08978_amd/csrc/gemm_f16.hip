@@ -75,7 +75,8 @@ gemm_f16_kernel(GemmParams p)
     const int rest = logical - z * gx;
     const int s = rest / tiles;
     const int tile = rest - s * tiles;
-    const int tm = tile % p.tiles_m, tn = tile / p.tiles_m;
+    int tm, tn;
+    tile_of(tile, p.tiles_m, p.tiles_n, p.group_m, tm, tn);
     const int m0 = tm * MT, n0 = tn * NT;
     const int kbeg = s * p.kchunk;
     const int kend = min(p.K, kbeg + p.kchunk);
@@ -348,7 +349,8 @@ gemm_f16t_kernel(GemmParams p)
     const int rest = logical - z * gx;
     const int s = rest / tiles;
     const int tile = rest - s * tiles;
-    const int tm = tile % p.tiles_m, tn = tile / p.tiles_m;
+    int tm, tn;
+    tile_of(tile, p.tiles_m, p.tiles_n, p.group_m, tm, tn);
     const int m0 = tm * MT, n0 = tn * NT;
     const int kbeg = s * p.kchunk;
     const int kend = min(p.K, kbeg + p.kchunk);

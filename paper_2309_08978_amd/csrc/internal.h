@@ -23,6 +23,7 @@ struct GemmParams {
     int S;                 // split-K factor
     int kchunk;            // K range of one split, a multiple of the K-slab
     int tiles_m, tiles_n;
+    int group_m;           // tile rows per group of the tile order (1 .. tiles_m)
     float *ws;             // S > 1: partial products, row-major [S][batch][M][N]
     const void *zero;      // >= 64 bytes of zeros: the load address of out-of-range elements
 };

@@ -23,6 +23,22 @@ __device__ __forceinline__ int xcd_remap(int flat, int G) {
     return (xcd < r) ? xcd * (q + 1) + local : r * (q + 1) + (xcd - r) * q + local;
 }
 
+// Tile of a GEMM launch from its index in the (XCD-renumbered) order: tiles
+// run in groups of G tile rows, each group column by column (G rows of one
+// tile column, then the next column), so that the run of consecutive tiles an
+// XCD holds at once covers about G rows and (run / G) columns of tiles -- A
+// rows and B columns that the XCD's L2 shares -- instead of one whole column
+// of tiles, which makes every XCD read all of A.  G = tiles_m is the plain
+// column-major order.  A bijection of [0, tiles_m * tiles_n).
+__device__ __forceinline__ void tile_of(int tile, int tiles_m, int tiles_n, int G, int &tm, int &tn)
+{
+    const int span = G * tiles_n;
+    const int g = tile / span, local = tile - g * span;
+    const int rows = min(G, tiles_m - g * G);
+    tm = g * G + local % rows;
+    tn = local / rows;
+}
+
 // Wait until at most N vector memory operations of this wave are pending.
 template <int N>
 __device__ __forceinline__ void wait_vmcnt()

@@ -277,6 +277,19 @@ bool aligned_for(int kind, const Call &c) {
 
 // ------------------------------------------------------------------ launch
 
+// Tile rows per group of a GEMM's tile order (see tile_of in kcommon.h): the
+// ~tiles/8 consecutive tiles that one XCD holds form a block of G rows by
+// about tiles/(8 G) columns; G is the largest power of two with G^2 <= that
+// run, so the block is near square and its A rows plus B columns are fewest.
+int tile_group_rows(int tiles_m, int tiles_n) {
+    const int ov = env_int("NNJIT_GROUP_M", 0);
+    if (ov > 0) return std::min(ov, std::max(tiles_m, 1));
+    const int64_t run = ((int64_t)tiles_m * tiles_n + 7) / 8;
+    int G = 1;
+    while ((int64_t)(2 * G) * (2 * G) <= run) G *= 2;
+    return std::max(1, std::min(G, tiles_m));
+}
+
 int launch(Device &d, const Config &cfg, const Call &c) {
     if (env_flag("NNJIT_FAULT_CONFIG") && env_int("NNJIT_FAULT_CONFIG", -1) == cfg.id)
         return fail(NNJIT_EHIP, "config %d: launch failure injected by NNJIT_FAULT_CONFIG", cfg.id);
@@ -315,6 +328,7 @@ int launch(Device &d, const Config &cfg, const Call &c) {
         p.kchunk = g.kchunk;
         p.tiles_m = g.tiles_m;
         p.tiles_n = g.tiles_n;
+        p.group_m = tile_group_rows(g.tiles_m, g.tiles_n);
         p.ws = w ? w->ws : nullptr;
         p.zero = d.zero;
         const int64_t gx = (int64_t)g.tiles_m * g.tiles_n * cfg.split;
