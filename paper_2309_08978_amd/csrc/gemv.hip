@@ -292,9 +292,12 @@ hipError_t launch_splitk_reduce(const float *ws, int S, int batch, int M, int N,
     const int rows = batch * M;
     const long long total = (long long)rows * ((N + 3) / 4);
     if (total <= 0) return hipSuccess;
-    long long blocks = (total + 255) / 256;
+    // small outputs (a GEMV's single row) in 64-thread workgroups, so that
+    // their few thousand threads spread over as many CUs as possible
+    const int tpb = total < 64LL * 1024 ? 64 : 256;
+    long long blocks = (total + tpb - 1) / tpb;
     if (blocks > 8192) blocks = 8192;
-    hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, ws, S,
+    hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(tpb), 0, stream, ws, S,
                        (long long)rows * N, rows, M, N, C, ldc, sC);
     return hipGetLastError();
 }
