@@ -485,6 +485,28 @@ gemm_f16t_kernel(GemmParams p)
             if (st + 1 < NSTEP) interleave_mfma_ds<0, NMMA, NRD>();
         }
     };
+    // the same with the first step's fragments passed in (ca, cb); the last
+    // step reads the first step of the slab in stage `next` into them, so no
+    // slab starts with an LDS wait
+    auto compute_carry = [&](int stage, int next, f16x8 (&ca)[FM], f16x8 (&cb)[FN]) {
+        lds_char *sa = stage_base(stage);
+        f16x8 a[2][FM], b[2][FN];
+#pragma unroll
+        for (int i = 0; i < FM; ++i) a[0][i] = ca[i];
+#pragma unroll
+        for (int j = 0; j < FN; ++j) b[0][j] = cb[j];
+#pragma unroll
+        for (int st = 0; st < NSTEP; ++st) {
+            const int cur = st & 1;
+            if (st + 1 < NSTEP) read_frags(sa, st + 1, a[cur ^ 1], b[cur ^ 1]);
+            else read_frags(stage_base(next), 0, ca, cb);
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j) acc[i][j] = I::mma(a[cur][i], b[cur][j], acc[i][j]);
+            interleave_mfma_ds<0, NMMA, NRD>();
+        }
+    };
 
 #pragma unroll
     for (int u = 0; u < ST - 1; ++u) copy_slab(u, u);
@@ -494,17 +516,46 @@ gemm_f16t_kernel(GemmParams p)
     // rest runs with checked copies and a guard per slab.  Both issue the
     // same copies per slab, so the counted waits are the same.
     int it0 = 0;
-    for (; it0 + 2 * ST - 1 <= nfull; it0 += ST) {
-#pragma unroll
-        for (int u = 0; u < ST; ++u) {
-            // this wave's copies of slab it0 + u are done once at most the
-            // copies of the ST - 2 later slabs are pending; the barrier
-            // then makes every wave's copies visible and frees the stage
-            // multiplied in the previous iteration
-            wait_vmcnt<(ST - 2) * (LA + LB)>();
+    if constexpr (ST >= 4) {
+        // With four or more stages the main part runs one slab ahead: the
+        // wait and barrier at iteration it make slab it + 1 visible, so the
+        // last step of slab it can read slab it + 1's first fragments (one
+        // slab fewer of copies in flight, ST - 3)
+        if (2 * ST - 1 <= nfull) {
+            f16x8 ca[FM], cb[FN];
+            wait_vmcnt<(ST - 2) * (LA + LB)>();   // slab 0
             lds_barrier();
-            copy_full((u + ST - 1) % ST, it0 + u + ST - 1);
-            compute(u);
+            read_frags(stage_base(0), 0, ca, cb);
+            for (; it0 + 2 * ST - 1 <= nfull; it0 += ST) {
+#pragma unroll
+                for (int u = 0; u < ST; ++u) {
+                    // this wave's copies of slab it0 + u + 1 are done once
+                    // at most the copies of the ST - 3 slabs after it are
+                    // pending; the barrier makes every wave's copies visible
+                    // and frees the stage of slab it0 + u - 1, whose reads
+                    // were issued in the two previous iterations
+                    wait_vmcnt<(ST - 3) * (LA + LB)>();
+                    lds_barrier();
+                    copy_full((u + ST - 1) % ST, it0 + u + ST - 1);
+                    compute_carry(u, (u + 1) % ST, ca, cb);
+                }
+            }
+            // the first fragments of slab it0 read by the last iteration go
+            // unused: the loop below reads every slab it multiplies itself
+        }
+    } else {
+        for (; it0 + 2 * ST - 1 <= nfull; it0 += ST) {
+#pragma unroll
+            for (int u = 0; u < ST; ++u) {
+                // this wave's copies of slab it0 + u are done once at most
+                // the copies of the ST - 2 later slabs are pending; the
+                // barrier then makes every wave's copies visible and frees
+                // the stage multiplied in the previous iteration
+                wait_vmcnt<(ST - 2) * (LA + LB)>();
+                lds_barrier();
+                copy_full((u + ST - 1) % ST, it0 + u + ST - 1);
+                compute(u);
+            }
         }
     }
     for (; it0 < nk; it0 += ST) {
