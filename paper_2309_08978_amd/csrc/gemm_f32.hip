@@ -721,13 +721,10 @@ gemm_f32t_kernel(GemmParams p)
 #pragma unroll
             for (int r = 0; r < I::NR; ++r) acc[i][j][r] = 0.f;
 
-    // one slab: lane group g takes k in [8g, 8g + 8); every fragment read is
-    // issued before the first MFMA
-    auto compute = [&](int stage) {
+    // fragments of one slab: lane group g takes k in [8g, 8g + 8)
+    auto read_frags = [&](int stage, f32x8 (&a)[FM], float (&b)[8][FN]) {
         lds_char *sa = stage_base(stage);
         lds_char *sb = sa + A_BYTES;
-        f32x8 a[FM];
-        float b[8][FN];
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
             const int row = wm * WTM + 32 * i + li;
@@ -745,12 +742,22 @@ gemm_f32t_kernel(GemmParams p)
                 b[t][j] = *(__attribute__((address_space(3))) float *)(brow + 16 * ((cc >> 2) ^ (lg << 3)) + 4 * (cc & 3));
             }
         }
+    };
+    auto mma_slab = [&](const f32x8 (&a)[FM], const float (&b)[8][FN]) {
 #pragma unroll
         for (int t = 0; t < 8; ++t)
 #pragma unroll
             for (int i = 0; i < FM; ++i)
 #pragma unroll
                 for (int j = 0; j < FN; ++j) acc[i][j] = I::mma(a[i][t], b[t][j], acc[i][j]);
+    };
+
+    // one slab: every fragment read is issued before the first MFMA
+    auto compute = [&](int stage) {
+        f32x8 a[FM];
+        float b[8][FN];
+        read_frags(stage, a, b);
+        mma_slab(a, b);
         __builtin_amdgcn_sched_group_barrier(0x100, FM * 2 + 8 * FN, 0);   // all LDS reads first
         __builtin_amdgcn_sched_group_barrier(0x008, 8 * FM * FN, 0);       // then the MFMAs
     };
@@ -765,17 +772,53 @@ gemm_f32t_kernel(GemmParams p)
     // rest runs with checked copies and a guard per slab.  Both issue the
     // same copies per slab, so the counted waits are the same.
     int it0 = 0;
-    for (; it0 + 2 * ST - 1 <= nfull; it0 += ST) {
-#pragma unroll
-        for (int u = 0; u < ST; ++u) {
-            // this wave's copies of slab it0 + u are done once at most the copies
-            // of the ST - 2 later slabs are pending; the barrier then makes
-            // every wave's copies visible and frees the stage multiplied in
-            // the previous iteration
-            wait_vmcnt<(ST - 2) * LC>();
+    if constexpr (ST == 4) {
+        // four stages: the main part runs one slab ahead -- the wait and
+        // barrier at iteration it make slab it + 1 visible, and its fragments
+        // are read into the other register set while slab it's MFMAs run
+        // (one slab fewer of copies in flight)
+        if (2 * ST - 1 <= nfull) {
+            f32x8 fa[2][FM];
+            float fb[2][8][FN];
+            wait_vmcnt<(ST - 2) * LC>();   // slab 0
             lds_barrier();
-            copy_full((u + ST - 1) % ST, it0 + u + ST - 1);
-            compute(u);
+            read_frags(0, fa[0], fb[0]);
+            for (; it0 + 2 * ST - 1 <= nfull; it0 += ST) {
+#pragma unroll
+                for (int u = 0; u < ST; ++u) {
+                    // this wave's copies of slab it0 + u + 1 are done once at
+                    // most the copies of the ST - 3 slabs after it are
+                    // pending; the barrier makes every wave's copies visible
+                    // and frees the stage of slab it0 + u - 1, whose reads
+                    // were issued in the two previous iterations
+                    wait_vmcnt<(ST - 3) * LC>();
+                    lds_barrier();
+                    copy_full((u + ST - 1) % ST, it0 + u + ST - 1);
+                    read_frags((u + 1) % ST, fa[(u + 1) & 1], fb[(u + 1) & 1]);
+                    mma_slab(fa[u & 1], fb[u & 1]);
+#pragma unroll
+                    for (int q = 0; q < 8 * FM * FN; ++q) {
+                        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+                        if (q < FM * 2 + 8 * FN) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
+                    }
+                }
+            }
+            // the fragments of slab it0 read by the last iteration go unused:
+            // the loop below reads every slab it multiplies itself
+        }
+    } else {
+        for (; it0 + 2 * ST - 1 <= nfull; it0 += ST) {
+#pragma unroll
+            for (int u = 0; u < ST; ++u) {
+                // this wave's copies of slab it0 + u are done once at most the copies
+                // of the ST - 2 later slabs are pending; the barrier then makes
+                // every wave's copies visible and frees the stage multiplied in
+                // the previous iteration
+                wait_vmcnt<(ST - 2) * LC>();
+                lds_barrier();
+                copy_full((u + ST - 1) % ST, it0 + u + ST - 1);
+                compute(u);
+            }
         }
     }
     for (; it0 < nk; it0 += ST) {
