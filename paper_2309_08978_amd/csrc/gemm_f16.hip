@@ -677,6 +677,7 @@ constexpr int lds_f16t(int mt, int nt, int kt, int st) { return st * (mt + nt) *
     X(128, 256, 64, 2, 2, 32, 3) \
     X(128, 256, 64, 2, 4, 32, 2) \
     X(128, 256, 64, 2, 4, 32, 3) \
+    X(128, 256, 32, 2, 4, 32, 4) \
     X(128, 256, 32, 2, 4, 32, 5) \
     X(128, 128, 64, 2, 2, 32, 2) \
     X(128, 128, 64, 2, 2, 32, 3) \
