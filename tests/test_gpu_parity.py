@@ -374,3 +374,30 @@ def test_gemv_split_k_back_to_back_and_replayed(all_configs, dt):
         torch.cuda.synchronize()
         for (c, _, _, R), C in zip(trio, outs):
             assert np.array_equal(host(C), R), f"replay {rep}: config {c['name']} split={c['split']}"
+
+
+@pytest.mark.parametrize("family", ["gemm_f32", "gemm_f16"])
+def test_tile_order_groups_cover_every_tile(all_configs, family, monkeypatch):
+    """The tile order runs in groups of G tile rows (NNJIT_GROUP_M forces G):
+    for every G, including ones that do not divide the tile rows and the
+    plain column order, each tile is computed exactly once -- the output
+    (NaN-filled first) is the oracle's exact sum, with split-K and batch."""
+    import torch
+    batch, M, N, K = 2, 1000, 520, 96
+    A, B = workloads.small_int_operands(6061, batch, M, K, N, FAMILY_DTYPE[family])
+    R = oracle.matmul(A, B)
+    dA, dB = dev(A), dev(B)
+    # one 64-row configuration of each kernel of the family, unsplit and split 2
+    prefixes = (("gemm_f32_", "gemm_f32w_", "gemm_f32t_") if family == "gemm_f32" else ("gemm_f16_", "gemm_f16t_"))
+    picks = []
+    for pre in prefixes:
+        for split in (1, 2):
+            picks += [c for c in all_configs if c["family"] == family and c["vec"] == 16 and c["Mt"] == 64
+                      and c["name"].startswith(pre) and c["split"] == split][:1]
+    assert len(picks) == 2 * len(prefixes), [c["name"] for c in picks]
+    for G in ("1", "3", "4", "5", "16", "64"):
+        monkeypatch.setenv("NNJIT_GROUP_M", G)
+        for c in picks:
+            C = torch.full(R.shape, float("nan"), dtype=torch.float32, device="cuda:0")
+            nj.batched_matmul(dA, dB, C, cfg=c["id"])
+            assert np.array_equal(host(C), R), f"G={G} config {c['name']} split={c['split']}"
