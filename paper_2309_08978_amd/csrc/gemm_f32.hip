@@ -551,15 +551,6 @@ gemm_f32w_kernel(GemmParams p)
 
     // every wave's partial tile to LDS, then wave w adds register slots
     // [w NREG / KS, (w + 1) NREG / KS) of all KS partials in wave order
-    float *red = (float *)smem;
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-#pragma unroll
-            for (int r = 0; r < I::NR; ++r) red[((wave * NREG) + (i * FN + j) * I::NR + r) * 64 + lane] = acc[i][j][r];
-    __syncthreads();
-
     float *out = C;
     long long ldo = p.ldc;
     if (p.S > 1) {
@@ -567,15 +558,52 @@ gemm_f32w_kernel(GemmParams p)
         ldo = N;
     }
     constexpr int SHARE = NREG / KS;
-#pragma unroll
-    for (int q = 0; q < SHARE; ++q) {
-        const int e = wave * SHARE + q;              // register slot (i, j, r)
-        float v = red[e * 64 + lane];
-#pragma unroll
-        for (int w = 1; w < KS; ++w) v += red[(w * NREG + e) * 64 + lane];
+    auto store_slot = [&](int e, float v) {
         const int i = e / (FN * I::NR), j = (e / I::NR) % FN, r = e % I::NR;
         const int row = m0 + 32 * i + I::row_of(r, lg), col = n0 + 32 * j + li;
         if (row < M && col < N) out[(long long)row * ldo + col] = v;
+    };
+    if constexpr (SHARE % 4 == 0) {
+        // four consecutive slots per lane and 16-byte LDS accesses:
+        // quad q of wave w at red4[(w NREG / 4 + q) 64 + lane]
+        typedef __attribute__((address_space(3))) f32x4 lds_f32x4;
+        lds_f32x4 *red4 = (lds_f32x4 *)smem;
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int r4 = 0; r4 < I::NR / 4; ++r4) {
+                    const f32x4 v = {acc[i][j][4 * r4], acc[i][j][4 * r4 + 1], acc[i][j][4 * r4 + 2], acc[i][j][4 * r4 + 3]};
+                    red4[(wave * (NREG / 4) + (i * FN + j) * (I::NR / 4) + r4) * 64 + lane] = v;
+                }
+        __syncthreads();
+#pragma unroll
+        for (int qq = 0; qq < SHARE / 4; ++qq) {
+            const int e0 = wave * SHARE + 4 * qq;
+            f32x4 v = red4[(e0 / 4) * 64 + lane];
+#pragma unroll
+            for (int w = 1; w < KS; ++w) v += red4[(w * (NREG / 4) + e0 / 4) * 64 + lane];
+#pragma unroll
+            for (int c = 0; c < 4; ++c) store_slot(e0 + c, v[c]);
+        }
+    } else {
+        float *red = (float *)smem;
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int r = 0; r < I::NR; ++r) red[((wave * NREG) + (i * FN + j) * I::NR + r) * 64 + lane] = acc[i][j][r];
+        __syncthreads();
+#pragma unroll
+        for (int q = 0; q < SHARE; ++q) {
+            const int e = wave * SHARE + q;              // register slot (i, j, r)
+            float v = red[e * 64 + lane];
+#pragma unroll
+            for (int w = 1; w < KS; ++w) v += red[(w * NREG + e) * 64 + lane];
+            store_slot(e, v);
+        }
     }
 }
 
