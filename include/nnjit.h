@@ -55,6 +55,8 @@
  *   NNJIT_TUNE_BUDGET_MS  wall-time budget of one shape's tuning (default 900)
  *   NNJIT_TUNE_REPS       timed bursts per candidate (default 3)
  *   NNJIT_TUNE_RUNOFF     0 skips the re-timing of the near-best candidates
+ *   NNJIT_TUNE_GRAPH      0 times candidates with eager launches instead of
+ *                         captured graph bursts
  *   NNJIT_RETUNE          non-zero: tune a shape again even if it is cached
  *   NNJIT_FORCE_CONFIG    configuration id used for every call of its family
  *                         (for experiments; results are the same, speed not)

@@ -80,7 +80,7 @@ struct Tuned {
     std::vector<std::pair<int, double>> ranked;   // up to kRanked (config, us): the registered one, then the fastest others
 };
 constexpr int kRanked = 5;
-constexpr int kRunoff = 4;   // candidates re-timed in the tuner's run-off
+constexpr int kRunoff = 6;   // candidates re-timed in the tuner's run-off
 std::map<ShapeKey, Tuned> g_tuned;
 std::map<ShapeKey, int> g_default;
 
@@ -649,6 +649,33 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
         return launch(*d, cfg, c);
     };
 
+    // A burst of n launches captured as a graph on the tuner's stream, so that
+    // its replay measures device time per launch even when one launch takes
+    // less time on the device than on the host (a few-microsecond kernel
+    // launched eagerly measures the host's launch rate).  nullptr when the
+    // capture fails; the caller then launches eagerly.
+    const bool use_graphs = env_int("NNJIT_TUNE_GRAPH", 1) != 0;
+    auto capture_burst = [&](const Config &cfg, int n) -> hipGraphExec_t {
+        if (!use_graphs) return nullptr;
+        if (hipStreamBeginCapture(c.stream, hipStreamCaptureModeThreadLocal) != hipSuccess) {
+            (void)hipGetLastError();
+            return nullptr;
+        }
+        bool ok = true;
+        for (int b = 0; b < n && ok; ++b) ok = launch_next(cfg) == NNJIT_OK;
+        hipGraph_t g = nullptr;
+        const hipError_t ee = hipStreamEndCapture(c.stream, &g);
+        hipGraphExec_t x = nullptr;
+        if (!(ok && ee == hipSuccess && g && hipGraphInstantiate(&x, g, nullptr, nullptr, 0) == hipSuccess &&
+              hipGraphUpload(x, c.stream) == hipSuccess)) {
+            if (x) (void)hipGraphExecDestroy(x);
+            x = nullptr;
+            (void)hipGetLastError();
+        }
+        if (g) (void)hipGraphDestroy(g);
+        return x;
+    };
+
     const int reps = std::max(1, env_int("NNJIT_TUNE_REPS", 3));
     const double budget_ms = (double)env_int("NNJIT_TUNE_BUDGET_MS", 900);
     const bool trace = env_flag("NNJIT_TRACE");
@@ -694,29 +721,43 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
         float first_ms = 0.f;
         (void)hipEventElapsedTime(&first_ms, ev[0], ev[1]);
         const double first_us = first_ms * 1e3;
-        if (burst == 0) burst = first_us < 50.0 ? 8 : first_us < 400.0 ? 2 : 1;
+        if (burst == 0) burst = first_us < 10.0 ? 32 : first_us < 50.0 ? 8 : first_us < 400.0 ? 2 : 1;
         if (best >= 0 && first_us > 1.5 * best_first_us) {
             ++t_stats.n_aborted;
             t_trace.emplace_back(cfg.id, -1.0, ms_since(t0));
             if (trace) fprintf(stderr, "[nnjit] tune cand %d %s S=%d first %.1f us > 1.5x best, dropped\n", cfg.id, cfg.v->name, cfg.split, first_us);
             continue;
         }
+        // one graph per repetition, so each replays a fresh run of the
+        // rotating weight copies (cold, as eager launches would be)
+        std::vector<hipGraphExec_t> gx(reps, nullptr);
+        for (int r = 0; r < reps; ++r) gx[r] = capture_burst(cfg, burst);
+        const bool graphs = std::all_of(gx.begin(), gx.end(), [](hipGraphExec_t x) { return x != nullptr; });
+        auto drop_graphs = [&]() {
+            for (auto &x : gx)
+                if (x) (void)hipGraphExecDestroy(x);
+        };
         bool ok = true;
         for (int r = 0; r < reps && ok; ++r) {
             (void)hipEventRecord(ev[2 + 2 * r], c.stream);
-            for (int b = 0; b < burst && ok; ++b) ok = launch_next(cfg) == NNJIT_OK;
+            if (graphs) ok = hipGraphLaunch(gx[r], c.stream) == hipSuccess;
+            else
+                for (int b = 0; b < burst && ok; ++b) ok = launch_next(cfg) == NNJIT_OK;
             (void)hipEventRecord(ev[3 + 2 * r], c.stream);
         }
         if (!ok) {
             ++t_stats.n_failed;
             (void)hipGetLastError();
             (void)hipStreamSynchronize(c.stream);
+            drop_graphs();
             continue;
         }
         if ((e = hipEventSynchronize(ev[1 + 2 * reps])) != hipSuccess) {
+            drop_graphs();
             destroy();
             return hip_fail(e, "candidate timing");
         }
+        drop_graphs();
         std::vector<float> ts(reps);
         for (int r = 0; r < reps; ++r) (void)hipEventElapsedTime(&ts[r], ev[2 + 2 * r], ev[3 + 2 * r]);
         const double us = median(ts) * 1e3 / burst;
@@ -734,7 +775,7 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
     destroy();
     if (best < 0) return fail(NNJIT_ENOCFG, "every candidate failed");
 
-    // Run-off: the candidates within 10% of the best (at most kRunoff) are
+    // Run-off: the candidates within 15% of the best (at most kRunoff) are
     // timed again with bursts of >= ~150 us, taking turns over several
     // rounds so that clock drift reaches them alike; each keeps the median
     // of its rounds.  Short bursts of a few-microsecond kernel cannot tell
@@ -742,7 +783,7 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
     if (env_int("NNJIT_TUNE_RUNOFF", 1) != 0 && ms_since(te) < budget_ms) {
         std::vector<std::pair<double, int>> close;
         for (const auto &kv : timed)
-            if (kv.second <= best_us * 1.10) close.emplace_back(kv.second, kv.first);
+            if (kv.second <= best_us * 1.15) close.emplace_back(kv.second, kv.first);
         std::sort(close.begin(), close.end());
         if ((int)close.size() > kRunoff) close.resize(kRunoff);
         if (close.size() >= 2) {
@@ -753,11 +794,17 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
             bool ok = true;
             for (auto &x : rev)
                 if (hipEventCreate(&x) != hipSuccess) ok = false;
+            std::vector<hipGraphExec_t> rg(nc * rounds, nullptr);
+            for (int r = 0; r < rounds && ok; ++r)
+                for (int j = 0; j < nc; ++j) rg[r * nc + j] = capture_burst(configs()[close[j].second], burst2);
+            const bool graphs = std::all_of(rg.begin(), rg.end(), [](hipGraphExec_t x) { return x != nullptr; });
             for (int r = 0; r < rounds && ok; ++r)
                 for (int j = 0; j < nc && ok; ++j) {
                     const Config &cfg = configs()[close[j].second];
                     (void)hipEventRecord(rev[2 * (r * nc + j)], c.stream);
-                    for (int b = 0; b < burst2 && ok; ++b) ok = launch_next(cfg) == NNJIT_OK;
+                    if (graphs) ok = hipGraphLaunch(rg[r * nc + j], c.stream) == hipSuccess;
+                    else
+                        for (int b = 0; b < burst2 && ok; ++b) ok = launch_next(cfg) == NNJIT_OK;
                     (void)hipEventRecord(rev[2 * (r * nc + j) + 1], c.stream);
                 }
             if (ok && hipEventSynchronize(rev.back()) == hipSuccess) {
@@ -781,6 +828,8 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
                 (void)hipGetLastError();
                 (void)hipStreamSynchronize(c.stream);
             }
+            for (auto &x : rg)
+                if (x) (void)hipGraphExecDestroy(x);
             for (auto &x : rev) (void)hipEventDestroy(x);
         }
     }
