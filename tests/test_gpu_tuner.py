@@ -68,6 +68,32 @@ def test_failing_candidate_is_skipped(monkeypatch):
     nj.nnjit_cache_clear()
 
 
+
+@pytest.mark.parametrize("graph", ["1", "0"])
+def test_graph_and_eager_timing_both_tune(monkeypatch, graph):
+    """Candidates are timed as captured graph bursts (default) or, with
+    NNJIT_TUNE_GRAPH=0 (the fallback when capture is refused), as eager
+    bursts: either way a lite-space configuration is measured, registered,
+    and then computes the oracle's exact sums (small integers); a split-K
+    GEMV shape exercises the scratch allocated before capture."""
+    monkeypatch.setenv("NNJIT_TUNE_GRAPH", graph)
+    for name, index in (("bart_base_layer_seq128_f32", 4), ("llama2_7b_decode_f16", 1)):
+        op = workloads.workload(name)[index]
+        dt = dtype_code(op.dtype)
+        nj.nnjit_cache_clear()
+        cfg = nj.check(_tune(op))
+        st = nj.nnjit_last_tune_stats()
+        lite, _, _, _ = nj.nnjit_lite_space(kind_of(op.batch, op.M), dt, op.batch, op.M, op.N, op.K)
+        assert cfg in lite and st["n_timed"] >= 1 and st["n_failed"] == 0, st
+        A, B = workloads.small_int_operands(8080, op.batch, op.M, op.K, op.N, op.dtype)
+        R = oracle.matmul(A, B)
+        if op.batch == 1:
+            C = nj.matmul(dev(A[0] if A.ndim == 3 else A), dev(B[0] if B.ndim == 3 else B))
+        else:
+            C = nj.batched_matmul(dev(A), dev(B))
+        assert np.array_equal(host(C).reshape(R.shape), R), f"{op.name} graph={graph}"
+    nj.nnjit_cache_clear()
+
 def test_dispatch_uses_tuned_config_and_matches_oracle():
     name, i = "bart_base_layer_seq128_f32", 3
     op = workloads.workload(name)[i]
