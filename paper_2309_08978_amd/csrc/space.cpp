@@ -234,7 +234,10 @@ LiteResult lite_space(const Shape &s, const nnjit_device_limits &d, const std::v
                 // a workgroup with K groups needs half the split for the same waves
                 const int64_t lo = v.kslices > 1 ? std::max<int64_t>(1, sfill / 2) : sfill;
                 if (c.split < lo || c.split > 2 * sfill) continue;
-                if (tiles * c.split > 2 * slots) continue;  // over-split
+                // over-split: more than two waves of workgroups, unless they
+                // form whole waves (at most four)
+                const int64_t wgs = tiles * c.split;
+                if (wgs > 2 * slots && !(wgs % slots == 0 && wgs <= 4 * slots)) continue;
                 if (s.K < 2LL * c.split * v.kt) continue;    // at least two K slabs per split
             }
         } else {
