@@ -721,7 +721,9 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
         float first_ms = 0.f;
         (void)hipEventElapsedTime(&first_ms, ev[0], ev[1]);
         const double first_us = first_ms * 1e3;
-        if (burst == 0) burst = first_us < 10.0 ? 32 : first_us < 50.0 ? 8 : first_us < 400.0 ? 2 : 1;
+        // ~500 us of device work per burst (1 .. 64 launches), so that the
+        // fixed cost of launching the burst's graph is a small share of it
+        if (burst == 0) burst = std::min(64, std::max(1, (int)std::ceil(500.0 / std::max(first_us, 0.5))));
         if (best >= 0 && first_us > 1.5 * best_first_us) {
             ++t_stats.n_aborted;
             t_trace.emplace_back(cfg.id, -1.0, ms_since(t0));
@@ -776,7 +778,7 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
     if (best < 0) return fail(NNJIT_ENOCFG, "every candidate failed");
 
     // Run-off: the candidates within 15% of the best (at most kRunoff) are
-    // timed again with bursts of >= ~150 us, taking turns over several
+    // timed again with bursts of >= ~500 us, taking turns over several
     // rounds so that clock drift reaches them alike; each keeps the median
     // of its rounds.  Short bursts of a few-microsecond kernel cannot tell
     // such candidates apart.
@@ -788,7 +790,7 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
         if ((int)close.size() > kRunoff) close.resize(kRunoff);
         if (close.size() >= 2) {
             const int rounds = 5;
-            const int burst2 = std::min(64, std::max(burst, (int)std::ceil(150.0 / std::max(best_us, 0.1))));
+            const int burst2 = std::min(64, std::max(burst, (int)std::ceil(500.0 / std::max(best_us, 0.1))));
             const int nc = (int)close.size();
             std::vector<hipEvent_t> rev(2 * nc * rounds);
             bool ok = true;
