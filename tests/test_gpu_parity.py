@@ -401,3 +401,37 @@ def test_tile_order_groups_cover_every_tile(all_configs, family, monkeypatch):
             C = torch.full(R.shape, float("nan"), dtype=torch.float32, device="cuda:0")
             nj.batched_matmul(dA, dB, C, cfg=c["id"])
             assert np.array_equal(host(C), R), f"G={G} config {c['name']} split={c['split']}"
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16"])
+def test_random_shapes_bit_exact(all_configs, dt):
+    """Seeded random shapes (batch 1-3, M 1-300, N 8-520 in steps of 8 or any,
+    K 1-1500): the default configuration and two random configurations of the
+    family that accept the operands all give the oracle's exact sums (small
+    integers), covering slab, split and tile boundaries no fixed case hits."""
+    import torch
+    rng = np.random.default_rng(20240 + (dt == "f16"))
+    fam = "gemm_" + dt
+    n = 0
+    for t in range(24):
+        batch = int(rng.integers(1, 4))
+        M = int(rng.integers(1, 301))
+        vec = bool(rng.integers(0, 2))
+        N = int(rng.integers(1, 66)) * 8 if vec else int(rng.integers(1, 521))
+        K = int(rng.integers(1, 188)) * 8 if vec else int(rng.integers(1, 1501))
+        if M == 1:
+            M = 2   # M = 1 is the GEMV kind, covered elsewhere
+        A, B = workloads.small_int_operands(30000 + t, batch, M, K, N, dt)
+        R = oracle.matmul(A, B)
+        dA, dB = dev(A), dev(B)
+        mm = nj.matmul if A.ndim == 2 else nj.batched_matmul
+        C = mm(dA, dB)
+        assert np.array_equal(host(C), R), f"default: batch={batch} M={M} N={N} K={K}"
+        want16 = vec and (K * (2 if dt == "f16" else 4)) % 16 == 0 and (N * (2 if dt == "f16" else 4)) % 16 == 0
+        pool = [c for c in all_configs if c["family"] == fam and (c["vec"] == 16) == want16]
+        for c in rng.choice(pool, size=2, replace=False):
+            C = torch.full(R.shape, float("nan"), dtype=torch.float32, device="cuda:0")
+            mm(dA, dB, C, cfg=int(c["id"]))
+            assert np.array_equal(host(C), R), f"{c['name']} split={c['split']}: batch={batch} M={M} N={N} K={K}"
+            n += 1
+    print(f"{dt}: {n} forced random-shape runs bit-exact", flush=True)
