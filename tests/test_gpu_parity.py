@@ -435,3 +435,30 @@ def test_random_shapes_bit_exact(all_configs, dt):
             assert np.array_equal(host(C), R), f"{c['name']} split={c['split']}: batch={batch} M={M} N={N} K={K}"
             n += 1
     print(f"{dt}: {n} forced random-shape runs bit-exact", flush=True)
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16"])
+def test_random_gemv_shapes_bit_exact(all_configs, dt):
+    """Seeded random M = 1 shapes (N 1-9000, K 1-6000, aligned or not): the
+    default configuration and three random GEMV configurations that accept
+    the operands (any split) give the oracle's exact sums (small integers)."""
+    import torch
+    rng = np.random.default_rng(40960 + (dt == "f16"))
+    fam = "gemv_" + dt
+    n = 0
+    for t in range(20):
+        vec = bool(rng.integers(0, 2))
+        N = int(rng.integers(1, 1126)) * 8 if vec else int(rng.integers(1, 9001))
+        K = int(rng.integers(1, 6001))
+        A, B = workloads.small_int_operands(50000 + t, 1, 1, K, N, dt)
+        R = oracle.matmul(A, B)
+        dA, dB = dev(A), dev(B)
+        C = nj.matmul(dA, dB)
+        assert np.array_equal(host(C), R), f"default: N={N} K={K}"
+        pool = [c for c in all_configs if c["family"] == fam and (c["vec"] == 16) == vec]
+        for c in rng.choice(pool, size=3, replace=False):
+            C = torch.full(R.shape, float("nan"), dtype=torch.float32, device="cuda:0")
+            nj.matmul(dA, dB, C, cfg=int(c["id"]))
+            assert np.array_equal(host(C), R), f"{c['name']} split={c['split']}: N={N} K={K}"
+            n += 1
+    print(f"{dt}: {n} forced random GEMV runs bit-exact", flush=True)
