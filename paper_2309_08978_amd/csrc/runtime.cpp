@@ -787,7 +787,14 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
         for (const auto &kv : timed)
             if (kv.second <= best_us * 1.15) close.emplace_back(kv.second, kv.first);
         std::sort(close.begin(), close.end());
-        if ((int)close.size() > kRunoff) close.resize(kRunoff);
+        if ((int)close.size() > kRunoff) {
+            // the incumbent (cached, else the default) keeps its place, so the
+            // 3% rule below compares run-off times with run-off times
+            const int inc_id = hit != g_tuned.end() ? hit->second.cfg : lr.ids[0];
+            auto it = std::find_if(close.begin(), close.end(), [&](const std::pair<double, int> &x) { return x.second == inc_id; });
+            if (it != close.end() && it - close.begin() >= kRunoff) std::swap(*it, close[kRunoff - 1]);
+            close.resize(kRunoff);
+        }
         if (close.size() >= 2) {
             const int rounds = 5;
             const int burst2 = std::min(64, std::max(burst, (int)std::ceil(500.0 / std::max(best_us, 0.1))));
@@ -821,10 +828,13 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
                         fprintf(stderr, "[nnjit] tune run-off %d %s S=%d %.2f us (was %.2f)\n", close[j].second,
                                 configs()[close[j].second].v->name, configs()[close[j].second].split, us, close[j].first);
                 }
-                for (const auto &kv : timed)
-                    if (kv.second < best_us) {
-                        best_us = kv.second;
-                        best = kv.first;
+                // the best of the re-timed candidates: the others were timed
+                // only in the first pass, whose back-to-back bursts of one
+                // candidate read lower than the run-off's interleaved ones
+                for (const auto &cj : close)
+                    if (timed[cj.second] < best_us) {
+                        best_us = timed[cj.second];
+                        best = cj.second;
                     }
             } else {
                 (void)hipGetLastError();
