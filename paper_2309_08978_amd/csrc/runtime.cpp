@@ -831,11 +831,14 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
                 // the best of the re-timed candidates: the others were timed
                 // only in the first pass, whose back-to-back bursts of one
                 // candidate read lower than the run-off's interleaved ones
-                for (const auto &cj : close)
+                for (const auto &cj : close) {
                     if (timed[cj.second] < best_us) {
                         best_us = timed[cj.second];
                         best = cj.second;
                     }
+                    // the default's time is reported on the same measure as the pick
+                    if (cj.second == lr.ids[0]) t_stats.default_us = timed[cj.second];
+                }
             } else {
                 (void)hipGetLastError();
                 (void)hipStreamSynchronize(c.stream);
