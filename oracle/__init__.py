@@ -66,8 +66,6 @@ class Oracle:
         lib.oracle_matmul.restype = ctypes.c_int
         lib.oracle_matmul.argtypes = [i64, i64, i64, i64, vp, i64, i64, vp, i64, i64,
                                       vp, i64, i64, ctypes.c_int, ctypes.c_int]
-        lib.oracle_element.restype = ctypes.c_double
-        lib.oracle_element.argtypes = [i64, vp, i64, vp, i64, i64, ctypes.c_int]
         lib.oracle_f16_to_f64.restype = ctypes.c_double
         lib.oracle_f16_to_f64.argtypes = [ctypes.c_uint16]
         lib.oracle_max_threads.restype = ctypes.c_int
@@ -93,21 +91,6 @@ class Oracle:
         if rc != 0:
             raise RuntimeError(f"oracle_matmul returned {rc}")
         return R[0] if squeeze else R
-
-    def elements(self, A: np.ndarray, B: np.ndarray, idx) -> np.ndarray:
-        """R at the given (b, i, j) triples (or (i, j) pairs for 2-D operands),
-        each the same k-ascending fp64 sum ``matmul`` forms."""
-        A3 = np.ascontiguousarray(_as3(A))
-        B3 = np.ascontiguousarray(_as3(B))
-        _, M, K = A3.shape
-        N = B3.shape[2]
-        code = _dtype_code(A3)
-        out = np.empty(len(idx), dtype=np.float64)
-        for n, t in enumerate(idx):
-            b, i, j = (0, *t) if len(t) == 2 else t
-            out[n] = self.lib.oracle_element(K, A3.ctypes.data, b * M * K + i * K,
-                                             B3.ctypes.data, b * K * N + j, N, code)
-        return out
 
     def f16_to_f64(self, bits) -> np.ndarray:
         """Decode binary16 bit patterns (uint16) to fp64, one by one."""
@@ -149,10 +132,6 @@ def default() -> Oracle:
 
 def matmul(A: np.ndarray, B: np.ndarray, nthreads: int = 0) -> np.ndarray:
     return default().matmul(A, B, nthreads)
-
-
-def elements(A: np.ndarray, B: np.ndarray, idx) -> np.ndarray:
-    return default().elements(A, B, idx)
 
 
 def f16_to_f64(bits) -> np.ndarray:

@@ -48,8 +48,3 @@ def check(C, R, A, B, dtype: str, K: int | None = None) -> dict:
     return {"ok": bool(ok), "rel_fro": rel, "max_err": max_err, "elt_bound": elt_bound,
             "finite": finite, "K": K}
 
-
-def check_sampled(c_vals, r_vals, A, B, dtype: str, K: int) -> dict:
-    """The same bar on sampled elements: the per-element bound for fp32, and
-    the Frobenius ratio over the sample (an estimate of the full one)."""
-    return check(np.asarray(c_vals), np.asarray(r_vals), A, B, dtype, K=K)

@@ -22,12 +22,15 @@
  * Layout: row-major with leading dimensions (lda >= K, ldb >= N, ldr >= N) and
  * batch strides in elements.  R is fp64.
  *
- * Loop order: each output row i is accumulated in place, k outer, j inner.
- * For every single element this is the same k-ascending sum as the i-j-k
- * triple loop, so the result is bit-identical to it and does not depend on the
- * number of OpenMP threads (work is split over (b, i, column block) only).
+ * Loop order: the operands are converted to fp64 once per call (exactly; a
+ * plain loop over every element), then each output row i is accumulated in
+ * place, k outer, j inner.  For every single element this is the same
+ * k-ascending sum as the i-j-k triple loop, so the result is bit-identical to
+ * it and does not depend on the number of OpenMP threads (work is split over
+ * (b, i, column block) only).
  */
 #include <stdint.h>
+#include <stdlib.h>
 #include <string.h>
 
 #ifdef _OPENMP
@@ -64,14 +67,37 @@ double oracle_f16_to_f64(uint16_t h)
 enum { ORACLE_F32 = 0, ORACLE_F16 = 1 };
 enum { COLS_PER_TASK = 512 };
 
-static inline double load_elt(const void *p, int64_t idx, int dtype)
+/* Elements an operand occupies: slices at stride `stride`, `rows` rows of
+ * `ld` elements, `cols` used per row (0 when the operand is empty). */
+static int64_t span_of(int64_t batch, int64_t stride, int64_t rows, int64_t ld, int64_t cols)
 {
-    if (dtype == ORACLE_F32)
-        return (double)((const float *)p)[idx];
-    return oracle_f16_to_f64(((const uint16_t *)p)[idx]);
+    if (batch == 0 || rows == 0 || cols == 0)
+        return 0;
+    return (batch - 1) * stride + (rows - 1) * ld + cols;
 }
 
-/* Batched product in fp64; see the file comment for the definition. */
+/* Every element of an operand's span, converted exactly to fp64, once.  The
+ * span includes padding between rows and slices; those values are converted
+ * but never used. */
+static double *to_f64(const void *p, int64_t n, int dtype)
+{
+    double *out = (double *)malloc((size_t)(n > 0 ? n : 1) * sizeof(double));
+    if (!out)
+        return NULL;
+    if (dtype == ORACLE_F32) {
+        const float *f = (const float *)p;
+        for (int64_t t = 0; t < n; ++t)
+            out[t] = (double)f[t];
+    } else {
+        const uint16_t *h = (const uint16_t *)p;
+        for (int64_t t = 0; t < n; ++t)
+            out[t] = oracle_f16_to_f64(h[t]);
+    }
+    return out;
+}
+
+/* Batched product in fp64; see the file comment for the definition.  The
+ * operands are first converted to fp64 (exactly), then the sums run. */
 int oracle_matmul(int64_t batch, int64_t M, int64_t N, int64_t K,
                   const void *A, int64_t lda, int64_t strideA,
                   const void *B, int64_t ldb, int64_t strideB,
@@ -86,6 +112,14 @@ int oracle_matmul(int64_t batch, int64_t M, int64_t N, int64_t K,
         return 0;
     if (lda < K || ldb < N || ldr < N)
         return -1;
+
+    double *Ad = to_f64(A, span_of(batch, strideA, M, lda, K), dtype);
+    double *Bd = to_f64(B, span_of(batch, strideB, K, ldb, N), dtype);
+    if (!Ad || !Bd) {
+        free(Ad);
+        free(Bd);
+        return -3;
+    }
 
     const int64_t col_tasks = (N + COLS_PER_TASK - 1) / COLS_PER_TASK;
     const int64_t ntasks = batch * M * col_tasks;
@@ -103,25 +137,16 @@ int oracle_matmul(int64_t batch, int64_t M, int64_t N, int64_t K,
         for (int64_t j = j0; j < j1; ++j)
             r[j] = 0.0;
         for (int64_t k = 0; k < K; ++k) {
-            const double a = load_elt(A, b * strideA + i * lda + k, dtype);
-            const int64_t brow = b * strideB + k * ldb;
+            const double a = Ad[b * strideA + i * lda + k];
+            const double *brow = Bd + b * strideB + k * ldb;
             for (int64_t j = j0; j < j1; ++j)
-                r[j] += a * load_elt(B, brow + j, dtype);
+                r[j] += a * brow[j];
         }
     }
+    free(Ad);
+    free(Bd);
     (void)nthreads;
     return 0;
-}
-
-/* One output element R[b][i][j], k ascending: the same sum oracle_matmul
- * forms, for sampled checks at sizes where the full product is too slow. */
-double oracle_element(int64_t K, const void *A, int64_t a_off, const void *B,
-                      int64_t b_off, int64_t ldb, int dtype)
-{
-    double s = 0.0;
-    for (int64_t k = 0; k < K; ++k)
-        s += load_elt(A, a_off + k, dtype) * load_elt(B, b_off + k * ldb, dtype);
-    return s;
 }
 
 /* Weight-only 4-bit GEMV (the paper runs Llama-2 decode with 4-bit weights,
