@@ -41,17 +41,26 @@
  *   - Thread safety: all entry points may be called from several host
  *     threads.  Split-K scratch is kept per (device, stream), so concurrent
  *     calls on different streams do not share it; calls on one stream are
- *     ordered by the stream.
+ *     ordered by the stream.  A tune in progress on one thread does not hold
+ *     up calls on other threads (it times candidates on its own stream and
+ *     scratch).
  *   - Stream capture: a call may be recorded into a HIP graph.  A call whose
  *     configuration needs more split-K scratch than any earlier call on that
- *     stream grows it, which synchronises the stream and reallocates; during
- *     capture such a call enqueues nothing and returns NNJIT_EHIP.  Run each
- *     shape once on the stream before capturing it.
+ *     stream allocates a larger buffer; the outgrown one is retired, not
+ *     freed, so queued launches and graphs captured earlier on the stream stay
+ *     valid.  Retired buffers are released by nnjit_cache_clear() (after a
+ *     device synchronisation); graphs captured before that call must be
+ *     captured again.  During capture a call that would need to grow the
+ *     scratch enqueues nothing and returns NNJIT_EHIP: run each shape once on
+ *     the stream before capturing it.  Graphs captured on one stream share
+ *     that stream's scratch, so they must not be replayed concurrently (on
+ *     several streams at once).
  *   - A launch is limited to 2^31 - 1 workgroups (tiles x split x batch slices
  *     of up to 65535): larger problems return NNJIT_EINVAL.
  *   - Errors: a negative return code; nnjit_last_error() gives a message.
  *
- * Environment variables (read at each call; none is needed)
+ * Environment variables (none is needed; read when the library first
+ * initialises a device and again by nnjit_cache_clear(), never per call)
  *   NNJIT_TUNE_BUDGET_MS  wall-time budget of one shape's tuning (default 900)
  *   NNJIT_TUNE_REPS       timed bursts per candidate (default 3)
  *   NNJIT_TUNE_RUNOFF     0 skips the re-timing of the near-best candidates
@@ -116,7 +125,8 @@ int nnjit_batched_matmul(int64_t batch, int64_t M, int64_t N, int64_t K,
                          void *C, int64_t ldc, int64_t strideC,
                          int dtype, void *stream);
 
-/* Just-in-time tuning of one shape (Sec. 3 JIT phase, Sec. 5.2 lite space):
+/* Just-in-time tuning of one shape (Sec. 3 JIT phase, Sec. 5.2 lite space;
+ * the problem statement: one kernel per operator shape, Sec. 3):
  * builds the shape's lite space (enumerate the compiled configurations of
  * the kind and dtype, compute each one's Table 1 resource use on this
  * device, prune by the heuristics, order by workgroups per CU, most first),
@@ -240,7 +250,16 @@ int nnjit_lite_space(int kind, int dtype, int64_t batch, int64_t M, int64_t N, i
                      const nnjit_device_limits *dev, int *ids, int cap,
                      int *n_enumerated, int64_t *n_naive);
 
-/* Statistics of the last nnjit_tune / nnjit_tune_batched call on this thread. */
+/* Statistics of the last nnjit_tune / nnjit_tune_batched / nnjit_tune_gemv_q4
+ * call on this thread (the paper reports tuning time per shape and the size
+ * of the space searched, Sec. 7.3 and Table 6): *wall_ms = wall time of the
+ * whole call (scratch set-up, evaluation, syncs; 0 on a cache hit beyond the
+ * lookup), *n_enum = compiled configurations of the kind and dtype that were
+ * considered, *n_pruned = the size of the pruned (lite) space, *n_timed =
+ * candidates fully timed.  Any pointer may be NULL.  Returns NNJIT_OK. */
+int nnjit_last_tune_stats(double *wall_ms, int *n_enum, int *n_pruned, int *n_timed);
+
+/* The same statistics in full. */
 typedef struct nnjit_tune_stats {
     double wall_ms;       /* whole call, including scratch set-up and syncs       */
     double eval_ms;       /* the candidate evaluation loop only                   */
@@ -255,7 +274,9 @@ typedef struct nnjit_tune_stats {
     int cache_hit;        /* 1 if the shape was already tuned (nothing timed)     */
 } nnjit_tune_stats;
 
-int nnjit_last_tune_stats(nnjit_tune_stats *out);
+/* Copies the full statistics of the last tune on this thread into *out.
+ * Returns NNJIT_OK, or NNJIT_EINVAL if out is NULL. */
+int nnjit_last_tune_stats_ex(nnjit_tune_stats *out);
 
 /* Best-so-far curve of the last tune on this thread: for the i-th evaluated
  * candidate, its id, its per-launch time in us (or -1 if aborted/failed) and the
@@ -320,6 +341,17 @@ int nnjit_cache_save(const char *path);
  * identical devices can be loaded one after another.  Returns the number of
  * valid entries read (>= 0), or NNJIT_EINVAL (unreadable file) / NNJIT_EHIP. */
 int nnjit_cache_load(const char *path);
+
+/* Measurement helper: reads `bytes` of device memory at `src` once, with
+ * 16-byte loads from `workgroups` workgroups of 256 threads, and writes
+ * (practically) nothing -- at most one word per workgroup into `sink`
+ * (device memory of `workgroups` 32-bit words).  Timed around it, this is
+ * what one launch can stream from HBM, the reference against which the
+ * bandwidth-bound GEMV launches are set.  Preconditions: bytes >= 0 and a
+ * multiple of 16; src 16-byte aligned (NULL only when bytes == 0);
+ * 1 <= workgroups <= 2^20.  Asynchronous on stream.  Returns NNJIT_OK,
+ * NNJIT_EINVAL or NNJIT_EHIP. */
+int nnjit_stream_read(const void *src, int64_t bytes, void *sink, int workgroups, void *stream);
 
 /* Message for the last error on this thread ("" if none).  The pointer stays
  * valid until the next nnjit_* call on the same thread. */

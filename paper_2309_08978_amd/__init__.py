@@ -29,9 +29,9 @@ ERROR_NAMES = {-1: "NNJIT_EINVAL", -2: "NNJIT_EDTYPE", -3: "NNJIT_ENOCFG", -4: "
 EXPORTED = ["nnjit_matmul", "nnjit_batched_matmul", "nnjit_tune", "nnjit_tune_batched", "nnjit_matmul_config",
             "nnjit_gemv_q4", "nnjit_tune_gemv_q4", "nnjit_gemv_q4_config",
             "nnjit_num_configs", "nnjit_config_info", "nnjit_config_resources", "nnjit_lite_space",
-            "nnjit_last_tune_stats", "nnjit_last_tune_trace", "nnjit_cached_config", "nnjit_cached_ranked",
+            "nnjit_last_tune_stats", "nnjit_last_tune_stats_ex", "nnjit_last_tune_trace", "nnjit_cached_config", "nnjit_cached_ranked",
             "nnjit_set_online", "nnjit_online_status", "nnjit_cache_clear",
-            "nnjit_cache_save", "nnjit_cache_load", "nnjit_last_error", "nnjit_version"]
+            "nnjit_cache_save", "nnjit_cache_load", "nnjit_stream_read", "nnjit_last_error", "nnjit_version"]
 
 
 class NnjitError(RuntimeError):
@@ -95,7 +95,9 @@ def load(build_if_missing: bool = False) -> ctypes.CDLL:
             "nnjit_config_resources": [ci, ctypes.POINTER(DeviceLimits), ctypes.POINTER(Resources)],
             "nnjit_lite_space": [ci, ci, i64, i64, i64, i64, ctypes.POINTER(DeviceLimits),
                                  ctypes.POINTER(ci), ci, ctypes.POINTER(ci), ctypes.POINTER(i64)],
-            "nnjit_last_tune_stats": [ctypes.POINTER(TuneStats)],
+            "nnjit_last_tune_stats": [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ci), ctypes.POINTER(ci),
+                                      ctypes.POINTER(ci)],
+            "nnjit_last_tune_stats_ex": [ctypes.POINTER(TuneStats)],
             "nnjit_last_tune_trace": [ctypes.POINTER(ci), ctypes.POINTER(ctypes.c_double),
                                       ctypes.POINTER(ctypes.c_double), ci],
             "nnjit_cached_config": [ci, ci, i64, i64, i64, i64],
@@ -106,6 +108,7 @@ def load(build_if_missing: bool = False) -> ctypes.CDLL:
             "nnjit_cache_clear": [],
             "nnjit_cache_save": [ctypes.c_char_p],
             "nnjit_cache_load": [ctypes.c_char_p],
+            "nnjit_stream_read": [vp, i64, vp, ci, vp],
             "nnjit_last_error": [],
             "nnjit_version": [],
         }
@@ -205,8 +208,17 @@ def nnjit_lite_space(kind, dtype, batch, M, N, K, dev: Optional[DeviceLimits] = 
 
 
 def nnjit_last_tune_stats() -> dict:
+    """-> {'wall_ms', 'n_enum', 'n_pruned', 'n_timed'} of the last tune on this thread."""
+    w = ctypes.c_double(0.0)
+    e, p, t = ctypes.c_int(0), ctypes.c_int(0), ctypes.c_int(0)
+    check(load().nnjit_last_tune_stats(ctypes.byref(w), ctypes.byref(e), ctypes.byref(p), ctypes.byref(t)))
+    return {"wall_ms": w.value, "n_enum": e.value, "n_pruned": p.value, "n_timed": t.value}
+
+
+def nnjit_last_tune_stats_ex() -> dict:
+    """-> every field of nnjit_tune_stats for the last tune on this thread."""
     st = TuneStats()
-    load().nnjit_last_tune_stats(ctypes.byref(st))
+    check(load().nnjit_last_tune_stats_ex(ctypes.byref(st)))
     return {f: getattr(st, f) for f, _ in TuneStats._fields_}
 
 
@@ -259,6 +271,10 @@ def nnjit_cache_load(path) -> int:
     return load().nnjit_cache_load(os.fsencode(path))
 
 
+def nnjit_stream_read(src, nbytes, sink, workgroups, stream=None) -> int:
+    return load().nnjit_stream_read(_ptr(src), nbytes, _ptr(sink), workgroups, _stream(stream))
+
+
 def nnjit_last_error() -> str:
     r = load().nnjit_last_error()
     return r.decode() if r else ""
@@ -298,44 +314,89 @@ def check(rc: int) -> int:
 
 
 def _ld(t) -> int:
-    # leading dimension of a row-major 2-D view (unit column stride required)
-    if t.stride(-1) != 1 and t.shape[-1] > 1:
+    """Leading dimension of the row-major matrices of t (last two dims):
+    unit column stride, and a row stride that separates the rows."""
+    rows, cols = int(t.shape[-2]), int(t.shape[-1])
+    if t.stride(-1) != 1 and cols > 1:
         raise ValueError("operands must have unit stride along the last dimension")
-    return max(int(t.stride(-2)), int(t.shape[-1]), 1)
+    if rows > 1 and int(t.stride(-2)) < cols:
+        raise ValueError(f"row stride {t.stride(-2)} < {cols} columns: rows overlap (an expanded or "
+                         "transposed view); pass a contiguous copy")
+    return max(int(t.stride(-2)), cols, 1)
+
+
+def _check_operands(A, B, C, batched: bool):
+    """Reject, before any library call, operands the C entry points would
+    read or write out of bounds: mismatched dtypes or shapes, an output that
+    is not fp32, overlapping rows or output slices, tensors not on one GPU."""
+    import torch
+    nd = 3 if batched else 2
+    for name, t in (("A", A), ("B", B), ("C", C)):
+        if t.dim() != nd:
+            raise ValueError(f"{name} must be {nd}-D, got shape {tuple(t.shape)}")
+    if A.dtype not in (torch.float32, torch.float16):
+        raise TypeError(f"unsupported dtype {A.dtype}")
+    if B.dtype != A.dtype:
+        raise TypeError(f"A is {A.dtype} but B is {B.dtype}")
+    if C.dtype != torch.float32:
+        raise TypeError(f"C must be float32, got {C.dtype}")
+    M, K = A.shape[-2:]
+    K2, N = B.shape[-2:]
+    if K2 != K:
+        raise ValueError(f"inner dimensions differ: {tuple(A.shape)} . {tuple(B.shape)}")
+    want = ((A.shape[0],) if batched else ()) + (M, N)
+    if batched and B.shape[0] != A.shape[0]:
+        raise ValueError(f"batch sizes differ: {tuple(A.shape)} . {tuple(B.shape)}")
+    if tuple(C.shape) != want:
+        raise ValueError(f"C has shape {tuple(C.shape)}, expected {want}")
+    lds = [_ld(t) for t in (A, B, C)]
+    if batched:
+        for name, t in (("A", A), ("B", B), ("C", C)):
+            if t.stride(0) < 0:
+                raise ValueError(f"negative batch stride of {name}")
+        span = (M - 1) * lds[2] + N if M > 0 and N > 0 else 0
+        if C.shape[0] > 1 and span > 0 and C.stride(0) < span:
+            raise ValueError(f"batch stride {C.stride(0)} of C < {span}: output slices overlap")
+    devs = {t.device for t in (A, B, C)}
+    if len(devs) != 1 or next(iter(devs)).type != "cuda":
+        raise ValueError(f"A, B and C must be on one GPU, got {sorted(str(d) for d in devs)}")
+    return lds
 
 
 def matmul(A, B, C=None, stream=None, cfg: Optional[int] = None):
     """C = A . B for 2-D fp32/fp16 CUDA tensors (C fp32, allocated if None)."""
     import torch
+    if A.dim() != 2 or B.dim() != 2:
+        raise ValueError(f"matmul takes 2-D operands, got {tuple(A.shape)} . {tuple(B.shape)}")
     M, K = A.shape
-    K2, N = B.shape
-    if K2 != K:
-        raise ValueError(f"inner dimensions differ: {tuple(A.shape)} . {tuple(B.shape)}")
+    N = B.shape[1]
     if C is None:
         C = torch.empty((M, N), dtype=torch.float32, device=A.device)
+    lda, ldb, ldc = _check_operands(A, B, C, batched=False)
     dt = dtype_code(A)
     if cfg is None:
-        check(nnjit_matmul(M, N, K, A, _ld(A), B, _ld(B), C, _ld(C), dt, stream))
+        check(nnjit_matmul(M, N, K, A, lda, B, ldb, C, ldc, dt, stream))
     else:
-        check(nnjit_matmul_config(cfg, 1, M, N, K, A, _ld(A), 0, B, _ld(B), 0, C, _ld(C), 0, dt, stream))
+        check(nnjit_matmul_config(cfg, 1, M, N, K, A, lda, 0, B, ldb, 0, C, ldc, 0, dt, stream))
     return C
 
 
 def batched_matmul(A, B, C=None, stream=None, cfg: Optional[int] = None):
     """C[b] = A[b] . B[b] for 3-D fp32/fp16 CUDA tensors (C fp32)."""
     import torch
+    if A.dim() != 3 or B.dim() != 3:
+        raise ValueError(f"batched_matmul takes 3-D operands, got {tuple(A.shape)} . {tuple(B.shape)}")
     batch, M, K = A.shape
-    _, K2, N = B.shape
-    if K2 != K or B.shape[0] != batch:
-        raise ValueError(f"shape mismatch {tuple(A.shape)} . {tuple(B.shape)}")
+    N = B.shape[2]
     if C is None:
         C = torch.empty((batch, M, N), dtype=torch.float32, device=A.device)
+    lda, ldb, ldc = _check_operands(A, B, C, batched=True)
     dt = dtype_code(A)
     sA, sB, sC = (int(t.stride(0)) for t in (A, B, C))
     if cfg is None:
-        check(nnjit_batched_matmul(batch, M, N, K, A, _ld(A), sA, B, _ld(B), sB, C, _ld(C), sC, dt, stream))
+        check(nnjit_batched_matmul(batch, M, N, K, A, lda, sA, B, ldb, sB, C, ldc, sC, dt, stream))
     else:
-        check(nnjit_matmul_config(cfg, batch, M, N, K, A, _ld(A), sA, B, _ld(B), sB, C, _ld(C), sC, dt, stream))
+        check(nnjit_matmul_config(cfg, batch, M, N, K, A, lda, sA, B, ldb, sB, C, ldc, sC, dt, stream))
     return C
 
 
@@ -344,13 +405,24 @@ def gemv_q4(x, Wq, scales, group: int, N: int, y=None, stream=None, cfg: Optiona
     x fp16 [K], Wq int32 [N, ldq] (uint32 code words, reinterpreted), scales
     fp16 [N, lds]; y fp32 [N] (allocated if None)."""
     import torch
+    if x.dim() != 1 or (x.shape[0] > 1 and x.stride(0) != 1):
+        raise ValueError(f"x must be a contiguous vector, got shape {tuple(x.shape)}")
     K = int(x.shape[0])
+    if group < 1:
+        raise ValueError(f"group must be >= 1, got {group}")
     if Wq.dim() != 2 or scales.dim() != 2 or Wq.shape[0] < N or scales.shape[0] < N:
         raise ValueError(f"shape mismatch x {tuple(x.shape)}, Wq {tuple(Wq.shape)}, scales {tuple(scales.shape)}")
+    if Wq.shape[1] < -(-K // 8) or scales.shape[1] < -(-K // group):
+        raise ValueError(f"rows too short for K={K}: Wq {tuple(Wq.shape)}, scales {tuple(scales.shape)}")
     if x.dtype != torch.float16 or scales.dtype != torch.float16 or Wq.element_size() != 4:
         raise TypeError("x and scales must be float16, Wq 32-bit words")
     if y is None:
         y = torch.empty((N,), dtype=torch.float32, device=x.device)
+    if y.dtype != torch.float32 or tuple(y.shape) != (N,) or (N > 1 and y.stride(0) != 1):
+        raise ValueError(f"y must be a contiguous float32 vector of {N}, got {y.dtype} {tuple(y.shape)}")
+    devs = {t.device for t in (x, Wq, scales, y)}
+    if len(devs) != 1 or next(iter(devs)).type != "cuda":
+        raise ValueError(f"x, Wq, scales and y must be on one GPU, got {sorted(str(d) for d in devs)}")
     ldq, lds = _ld(Wq), _ld(scales)
     if cfg is None:
         check(nnjit_gemv_q4(N, K, group, x, Wq, ldq, scales, lds, y, stream))

@@ -303,31 +303,73 @@ hipError_t launch_splitk_reduce(const float *ws, int S, int batch, int M, int N,
 }
 
 // ------------------------------------------------------------------------
-// Scratch fill for the tuner: a counter-based hash of (seed, index) mapped
-// to [-1, 1), written as fp32 or fp16.  Timing candidates does not depend on
-// the values; this only keeps the scratch finite and non-trivial.
+// Streaming-read reference: every 16-byte chunk of src read once (four loads
+// in flight per lane, consecutive lanes on consecutive chunks), combined by
+// XOR so the loads cannot be dropped; a workgroup stores only if its value
+// hits one constant, so the kernel writes (practically) nothing.  It is the
+// measure of what one launch can stream from HBM, set beside the GEMVs.
+__global__ void __launch_bounds__(256)
+stream_read_kernel(const u32x4 *__restrict__ src, long long n16, unsigned *sink)
+{
+    const long long stride = (long long)gridDim.x * 256;
+    long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+    unsigned acc = 0;
+    for (; i + 3 * stride < n16; i += 4 * stride) {
+        const u32x4 a = src[i], b = src[i + stride], c = src[i + 2 * stride], d = src[i + 3 * stride];
+        acc ^= (a.x ^ a.y ^ a.z ^ a.w) ^ (b.x ^ b.y ^ b.z ^ b.w) ^ (c.x ^ c.y ^ c.z ^ c.w) ^ (d.x ^ d.y ^ d.z ^ d.w);
+    }
+    for (; i < n16; i += stride) {
+        const u32x4 a = src[i];
+        acc ^= a.x ^ a.y ^ a.z ^ a.w;
+    }
+    if (acc == 0x9e3779b9u) sink[blockIdx.x] = acc;
+}
+
+hipError_t launch_stream_read(const void *src, long long bytes, unsigned *sink, int workgroups, hipStream_t stream)
+{
+    if (bytes <= 0) return hipSuccess;
+    hipLaunchKernelGGL(stream_read_kernel, dim3((unsigned)workgroups), dim3(256), 0, stream, (const u32x4 *)src,
+                       bytes / 16, sink);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------
+// Scratch fill for the tuner: a counter-based hash of (seed, index) gives
+// four uniforms in [-1, 1) per value; their sum, scaled to unit variance
+// (times `scale`), is close to normal -- the tuner times candidates on values
+// shaped like the workloads' activations and weights, since the matrix cores'
+// speed depends somewhat on the data.  FILL_WORDS writes the raw hash.
 __device__ __forceinline__ unsigned mix32(unsigned x) {
     x ^= x >> 16; x *= 0x7feb352du; x ^= x >> 15; x *= 0x846ca68bu; x ^= x >> 16;
     return x;
 }
 
-__global__ void fill_uniform_kernel(void *dst, long long n, int f16, unsigned seed)
+__global__ void fill_kernel(void *dst, long long n, int kind, float scale, unsigned seed)
 {
     const long long stride = (long long)gridDim.x * blockDim.x;
     for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
-        const unsigned h = mix32((unsigned)i * 0x9e3779b9u ^ mix32(seed + (unsigned)(i >> 32)));
-        const float v = (float)(h >> 8) * (1.0f / 8388608.0f) - 1.0f;
-        if (f16) ((_Float16 *)dst)[i] = (_Float16)v;
+        unsigned h = mix32((unsigned)i * 0x9e3779b9u ^ mix32(seed + (unsigned)(i >> 32)));
+        if (kind == FILL_WORDS) {
+            ((unsigned *)dst)[i] = h;
+            continue;
+        }
+        float sum = 0.f;
+        for (int u = 0; u < 4; ++u) {
+            sum += (float)(h >> 8) * (1.0f / 8388608.0f) - 1.0f;
+            h = mix32(h + 0x632be5abu);
+        }
+        const float v = sum * (0.8660254f * scale);   // sqrt(3)/2: four U[-1,1) have variance 4/3
+        if (kind == FILL_F16) ((_Float16 *)dst)[i] = (_Float16)v;
         else ((float *)dst)[i] = v;
     }
 }
 
-hipError_t launch_fill_uniform(void *dst, long long n, int dtype, unsigned seed, hipStream_t stream)
+hipError_t launch_fill(void *dst, long long n, int kind, float scale, unsigned seed, hipStream_t stream)
 {
     if (n <= 0) return hipSuccess;
     long long blocks = (n + 255) / 256;
     if (blocks > 4096) blocks = 4096;
-    hipLaunchKernelGGL(fill_uniform_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, dst, n, dtype, seed);
+    hipLaunchKernelGGL(fill_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, dst, n, kind, scale, seed);
     return hipGetLastError();
 }
 

@@ -90,9 +90,14 @@ extern const int kNumGemvQ4Variants;
 // Device helper kernels: the fixed-order split-K reduction
 //   C[z][i][j] = ws[0][z][i][j] + ws[1][z][i][j] + ... + ws[S-1][z][i][j]
 // (ws row-major [S][batch][M][N], C with leading dim ldc and batch stride sC),
-// and the scratch fill of the tuner.
+// and the scratch fill of the tuner: n values of about N(0, scale^2) as fp32
+// or fp16, or n random 32-bit words.
 hipError_t launch_splitk_reduce(const float *ws, int S, int batch, int M, int N, float *C, long long ldc,
                                 long long sC, hipStream_t stream);
-hipError_t launch_fill_uniform(void *dst, long long n, int dtype, unsigned seed, hipStream_t stream);
+enum FillKind { FILL_F32 = 0, FILL_F16 = 1, FILL_WORDS = 2 };
+// Streaming-read reference kernel (bytes % 16 == 0, src 16-byte aligned,
+// sink: `workgroups` words).
+hipError_t launch_stream_read(const void *src, long long bytes, unsigned *sink, int workgroups, hipStream_t stream);
+hipError_t launch_fill(void *dst, long long n, int kind, float scale, unsigned seed, hipStream_t stream);
 
 }  // namespace nnjit

@@ -49,8 +49,42 @@ int env_int(const char *name, int dflt) {
     return (v && *v) ? atoi(v) : dflt;
 }
 
+// Environment overrides, read once when the library first initialises a
+// device and again by nnjit_cache_clear(), never on the dispatch path.
+struct Settings {
+    int tune_budget_ms = 900;
+    int tune_reps = 3;
+    bool tune_runoff = true;
+    bool tune_graph = true;
+    bool retune = false;
+    bool log = false;
+    bool trace = false;
+    int force_config = -1;
+    int fault_config = -1;
+    int group_m = 0;
+};
+
+Settings read_settings() {
+    Settings s;
+    s.tune_budget_ms = env_int("NNJIT_TUNE_BUDGET_MS", 900);
+    s.tune_reps = std::max(1, env_int("NNJIT_TUNE_REPS", 3));
+    s.tune_runoff = env_int("NNJIT_TUNE_RUNOFF", 1) != 0;
+    s.tune_graph = env_int("NNJIT_TUNE_GRAPH", 1) != 0;
+    s.retune = env_flag("NNJIT_RETUNE");
+    s.log = env_flag("NNJIT_LOG");
+    s.trace = env_flag("NNJIT_TRACE");
+    s.force_config = env_int("NNJIT_FORCE_CONFIG", -1);
+    s.fault_config = env_flag("NNJIT_FAULT_CONFIG") ? env_int("NNJIT_FAULT_CONFIG", -1) : -1;
+    s.group_m = env_int("NNJIT_GROUP_M", 0);
+    return s;
+}
+
 // ------------------------------------------------------------ device state
 
+// Split-K partials of the calls on one (device, stream).  A buffer that is
+// outgrown is retired, not freed: a HIP graph captured earlier on the stream
+// keeps its address and may still be replayed.  Retired buffers are released
+// by nnjit_cache_clear() (after a device synchronisation) or at exit.
 struct Workspace {
     float *ws = nullptr;
     int64_t ws_floats = 0;
@@ -63,14 +97,14 @@ struct Device {
     std::string arch;
     std::vector<int> regs;    // measured VGPR+AGPR per lane, per variant
     std::vector<int> spills;  // private segment (scratch) > 0, per variant
-    hipStream_t tune_stream = nullptr;
     void *zero = nullptr;     // 256 zero bytes: load address of out-of-range GEMM elements
-    void *scratch = nullptr;  // tuner operands
-    size_t scratch_bytes = 0;
     std::map<hipStream_t, Workspace> workspaces;
+    std::vector<float *> retired;   // outgrown split-K buffers (see Workspace)
 };
 
 std::mutex g_mu;                  // guards everything below
+Settings g_set;                   // valid once any device is ready
+bool g_set_loaded = false;
 std::map<int, Device> g_devices;
 // tuned and default configurations: key (device, kind, dtype, batch, M, N, K)
 typedef std::tuple<int, int, int, int64_t, int64_t, int64_t, int64_t> ShapeKey;
@@ -123,6 +157,10 @@ int device_ready(Device **out) {
     int ord = -1;
     int rc = current_device(&ord);
     if (rc != NNJIT_OK) return rc;
+    if (!g_set_loaded) {
+        g_set = read_settings();
+        g_set_loaded = true;
+    }
     Device &d = g_devices[ord];
     if (!d.ready) {
         hipDeviceProp_t prop;
@@ -151,8 +189,6 @@ int device_ready(Device **out) {
             d.regs[gi] = attr.numRegs;
             d.spills[gi] = attr.localSizeBytes > 0 ? 1 : 0;
         }
-        e = hipStreamCreateWithFlags(&d.tune_stream, hipStreamNonBlocking);
-        if (e != hipSuccess) return hip_fail(e, "hipStreamCreate");
         e = hipMalloc(&d.zero, 256);
         if (e != hipSuccess) return hip_fail(e, "hipMalloc");
         e = hipMemset(d.zero, 0, 256);
@@ -163,31 +199,31 @@ int device_ready(Device **out) {
     return NNJIT_OK;
 }
 
-// Split-K scratch for (device, stream); grown on demand (under g_mu).
-int workspace_for(Device &d, hipStream_t stream, int64_t ws_floats, Workspace **out) {
+// Split-K scratch for (device, stream); grown on demand (under g_mu).  The
+// outgrown buffer is retired, not freed: launches still queued on the stream
+// and graphs captured on it keep using it, so growing needs no wait.
+int workspace_for(Device &d, hipStream_t stream, int64_t ws_floats, float **out) {
     Workspace &w = d.workspaces[stream];
     if (w.ws_floats < ws_floats) {
-        // growing means waiting for the stream and reallocating, neither of
-        // which a stream under capture allows: refuse instead of breaking it
+        // allocating is not allowed while the stream is being captured:
+        // refuse instead of breaking the capture
         hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
         if (hipStreamIsCapturing(stream, &cap) != hipSuccess) (void)hipGetLastError();
         if (cap != hipStreamCaptureStatusNone)
             return fail(NNJIT_EHIP, "split-K scratch of %lld floats needed while the stream is being captured; "
                                     "run this shape once on the stream outside capture first", (long long)ws_floats);
-        hipError_t e = hipStreamSynchronize(stream);  // earlier launches may still use the old buffer
-        if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
         const int64_t nf = std::max(w.ws_floats, ws_floats + ws_floats / 4);
-        if (w.ws) (void)hipFree(w.ws);
-        w.ws = nullptr;
-        w.ws_floats = 0;
-        e = hipMalloc((void **)&w.ws, (size_t)std::max<int64_t>(nf, 1) * sizeof(float));
+        float *fresh = nullptr;
+        hipError_t e = hipMalloc((void **)&fresh, (size_t)std::max<int64_t>(nf, 1) * sizeof(float));
         if (e != hipSuccess) {
             (void)hipGetLastError();
             return fail(NNJIT_ENOMEM, "split-K scratch of %lld floats", (long long)nf);
         }
+        if (w.ws) d.retired.push_back(w.ws);
+        w.ws = fresh;
         w.ws_floats = nf;
     }
-    *out = &w;
+    *out = w.ws;
     return NNJIT_OK;
 }
 
@@ -281,8 +317,8 @@ bool aligned_for(int kind, const Call &c) {
 // ~tiles/8 consecutive tiles that one XCD holds form a block of G rows by
 // about tiles/(8 G) columns; G is the largest power of two with G^2 <= that
 // run, so the block is near square and its A rows plus B columns are fewest.
-int tile_group_rows(int tiles_m, int tiles_n) {
-    const int ov = env_int("NNJIT_GROUP_M", 0);
+int tile_group_rows(int tiles_m, int tiles_n, int override_rows) {
+    const int ov = override_rows;
     if (ov > 0) return std::min(ov, std::max(tiles_m, 1));
     const int64_t run = ((int64_t)tiles_m * tiles_n + 7) / 8;
     int G = 1;
@@ -290,16 +326,15 @@ int tile_group_rows(int tiles_m, int tiles_n) {
     return std::max(1, std::min(G, tiles_m));
 }
 
-int launch(Device &d, const Config &cfg, const Call &c) {
-    if (env_flag("NNJIT_FAULT_CONFIG") && env_int("NNJIT_FAULT_CONFIG", -1) == cfg.id)
+// Launch one configuration on c.stream.  ws: split-K partial storage of at
+// least the geometry's ws_floats floats (unused when the split is 1).  Needs
+// no lock: it reads only the device's constant zero buffer.
+int launch(const Device &d, const Config &cfg, const Call &c, float *ws, const Settings &s) {
+    if (s.fault_config >= 0 && s.fault_config == cfg.id)
         return fail(NNJIT_EHIP, "config %d: launch failure injected by NNJIT_FAULT_CONFIG", cfg.id);
     const Variant &v = *cfg.v;
     const Geometry g = geometry_of(cfg, c.batch, c.M, c.N, c.K);
-    Workspace *w = nullptr;
-    if (g.ws_floats > 0) {
-        int rc = workspace_for(d, c.stream, g.ws_floats, &w);
-        if (rc != NNJIT_OK) return rc;
-    }
+    if (g.ws_floats > 0 && !ws) return fail(NNJIT_EINVAL, "config %d needs split-K scratch", cfg.id);
     hipError_t e = hipSuccess;
     if (family_is_q4(v.family)) {
         GemvQ4Params p{};
@@ -328,8 +363,8 @@ int launch(Device &d, const Config &cfg, const Call &c) {
         p.kchunk = g.kchunk;
         p.tiles_m = g.tiles_m;
         p.tiles_n = g.tiles_n;
-        p.group_m = tile_group_rows(g.tiles_m, g.tiles_n);
-        p.ws = w ? w->ws : nullptr;
+        p.group_m = tile_group_rows(g.tiles_m, g.tiles_n, s.group_m);
+        p.ws = ws;
         p.zero = d.zero;
         const int64_t gx = (int64_t)g.tiles_m * g.tiles_n * cfg.split;
         // the kernels number workgroups (x + gx * z) in 32-bit integers
@@ -358,12 +393,23 @@ int launch(Device &d, const Config &cfg, const Call &c) {
         p.S = cfg.split;
         p.kchunk = g.kchunk;
         p.segs = g.tiles_n;
-        p.ws = w ? w->ws : nullptr;
+        p.ws = ws;
         e = v.launch(&p, dim3((unsigned)g.wgs), c.stream);
         if (e == hipSuccess && cfg.split > 1) e = launch_splitk_reduce(p.ws, cfg.split, 1, 1, p.N, p.y, p.N, 0, c.stream);
     }
     if (e != hipSuccess) return hip_fail(e, v.name);
     return NNJIT_OK;
+}
+
+// Launch on the caller's stream with that stream's split-K scratch (under g_mu).
+int launch_on_stream(Device &d, const Config &cfg, const Call &c) {
+    const Geometry g = geometry_of(cfg, c.batch, c.M, c.N, c.K);
+    float *ws = nullptr;
+    if (g.ws_floats > 0) {
+        const int rc = workspace_for(d, c.stream, g.ws_floats, &ws);
+        if (rc != NNJIT_OK) return rc;
+    }
+    return launch(d, cfg, c, ws, g_set);
 }
 
 // First non-vector configuration of a family with split 1 (GEMM) or the split
@@ -446,7 +492,7 @@ int online_call(Device &d, int kind, const ShapeKey &key, const Call &c) {
         Tuned tu{o.registered, o.registered_us, {{o.registered, o.registered_us}}};
         std::vector<std::pair<double, int>> by_time;
         for (const auto &t : o.times)
-            if (t.first != o.registered) by_time.emplace_back(t.second, t.first);
+            if (t.first != o.registered && t.second < 1e299) by_time.emplace_back(t.second, t.first);
         std::sort(by_time.begin(), by_time.end());
         for (const auto &bt : by_time)
             if ((int)tu.ranked.size() < kRanked) tu.ranked.emplace_back(bt.second, bt.first);
@@ -458,9 +504,9 @@ int online_call(Device &d, int kind, const ShapeKey &key, const Call &c) {
         if (cfg.v->vec_bytes == 16 && !aligned_for(kind, c)) {
             const Config *fb = fallback_config(family_of(kind, c.dtype), c, d);
             if (!fb) return fail(NNJIT_ENOCFG, "no element-load fallback configuration");
-            return launch(d, *fb, c);
+            return launch_on_stream(d, *fb, c);
         }
-        return launch(d, cfg, c);
+        return launch_on_stream(d, cfg, c);
     }
     // measure the next candidate on this call, unless measuring is off, one is
     // still in flight, the stream is being captured or the operands need the
@@ -475,18 +521,25 @@ int online_call(Device &d, int kind, const ShapeKey &key, const Call &c) {
         }
         const int cand = o.ids[o.next++];
         (void)hipEventRecord(o.ev[0], c.stream);
-        const int rc = launch(d, configs()[cand], c);
-        if (rc != NNJIT_OK) return rc;   // a failing candidate is not retried
-        (void)hipEventRecord(o.ev[1], c.stream);
-        o.pending = cand;
-        return NNJIT_OK;
+        const int rc = launch_on_stream(d, configs()[cand], c);
+        if (rc == NNJIT_OK) {
+            (void)hipEventRecord(o.ev[1], c.stream);
+            o.pending = cand;
+            return NNJIT_OK;
+        }
+        // a candidate that cannot launch is recorded as failed (never timed,
+        // never registered) and this call's product is computed by the
+        // registered configuration below
+        (void)hipGetLastError();
+        o.times.emplace_back(cand, 1e300);
     }
     const Config *cfg = &configs()[o.registered];
     if (cfg->v->vec_bytes == 16 && !aligned) {
         cfg = fallback_config(family_of(kind, c.dtype), c, d);
         if (!cfg) return fail(NNJIT_ENOCFG, "no element-load fallback configuration");
     }
-    return launch(d, *cfg, c);
+    t_err.clear();
+    return launch_on_stream(d, *cfg, c);
 }
 
 int run(const Call &c, int forced) {
@@ -517,7 +570,7 @@ int run(const Call &c, int forced) {
     } else {
         const int kind = kind_of(c);
         int id = -1;
-        const int env_force = env_int("NNJIT_FORCE_CONFIG", -1);
+        const int env_force = g_set.force_config;
         if (env_force >= 0 && env_force < (int)configs().size() &&
             configs()[env_force].v->family == family_of(kind, c.dtype))
             id = env_force;
@@ -539,7 +592,7 @@ int run(const Call &c, int forced) {
             if (!cfg) return fail(NNJIT_ENOCFG, "no element-load fallback configuration");
         }
     }
-    return launch(*d, *cfg, c);
+    return launch_on_stream(*d, *cfg, c);
 }
 
 // -------------------------------------------------------------------- tuner
@@ -549,6 +602,33 @@ double median(std::vector<float> v) {
     const size_t n = v.size();
     return n % 2 ? v[n / 2] : 0.5 * (v[n / 2 - 1] + v[n / 2]);
 }
+
+// Device resources that one tune call owns -- its stream, the operand scratch
+// of the tuned shape and the split-K scratch of its candidates -- released
+// before the call returns.
+struct TuneResources {
+    hipStream_t stream = nullptr;
+    void *scratch = nullptr;
+    float *ws = nullptr;
+    std::vector<hipEvent_t> events;
+    ~TuneResources() {
+        if (stream) (void)hipStreamSynchronize(stream);
+        for (hipEvent_t e : events) (void)hipEventDestroy(e);
+        if (scratch) (void)hipFree(scratch);
+        if (ws) (void)hipFree(ws);
+        if (stream) (void)hipStreamDestroy(stream);
+        (void)hipGetLastError();
+    }
+    hipError_t event(hipEvent_t *out) {
+        hipError_t e = hipEventCreate(out);
+        if (e == hipSuccess) events.push_back(*out);
+        return e;
+    }
+};
+
+// The tuner's operand values follow the workloads' recipe (activations
+// N(0, 1), weights N(0, 0.02)): matrix-core time depends somewhat on the data.
+constexpr float kActScale = 1.0f, kWeightScale = 0.02f;
 
 int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
     using clock = std::chrono::steady_clock;
@@ -574,25 +654,40 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
     if (M > INT32_MAX || N > INT32_MAX || K > INT32_MAX || batch > INT32_MAX)
         return fail(NNJIT_EINVAL, "dimension above 2^31-1");
 
-    std::lock_guard<std::mutex> lk(g_mu);
+    // Under the lock: the device, the settings, the cache lookup and the lite
+    // space.  Candidates are then timed without it (on this call's own stream
+    // and scratch), so calls on other threads and streams are not held up;
+    // the lock is taken again only to register the result.
     Device *d = nullptr;
-    int rc = device_ready(&d);
-    if (rc != NNJIT_OK) return rc;
-    const auto t0 = clock::now();  // one-time library initialisation is not tune time
-    const ShapeKey key = key_of(d->ordinal, kind, c);
-    auto hit = g_tuned.find(key);
-    if (hit != g_tuned.end() && !env_flag("NNJIT_RETUNE")) {
-        t_stats.cache_hit = 1;
-        t_stats.chosen = hit->second.cfg;
-        t_stats.best_us = hit->second.us;
-        t_stats.wall_ms = ms_since(t0);
-        return hit->second.cfg;
+    Settings set;
+    clock::time_point t0;
+    ShapeKey key;
+    LiteResult lr;
+    int cached = -1;
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        int rc = device_ready(&d);
+        if (rc != NNJIT_OK) return rc;
+        set = g_set;
+        t0 = clock::now();  // one-time library initialisation is not tune time
+        key = key_of(d->ordinal, kind, c);
+        auto hit = g_tuned.find(key);
+        if (hit != g_tuned.end() && !set.retune) {
+            t_stats.cache_hit = 1;
+            t_stats.chosen = hit->second.cfg;
+            t_stats.best_us = hit->second.us;
+            t_stats.wall_ms = ms_since(t0);
+            return hit->second.cfg;
+        }
+        if (hit != g_tuned.end()) cached = hit->second.cfg;
+        lr = lite_space(shape_of(kind, c), d->limits, &d->regs, &d->spills);
     }
-
-    LiteResult lr = lite_space(shape_of(kind, c), d->limits, &d->regs, &d->spills);
     t_stats.n_enumerated = lr.n_enumerated;
     t_stats.n_lite = (int)lr.ids.size();
     if (lr.ids.empty()) return fail(NNJIT_ENOCFG, "no configuration fits this shape");
+    const int limit = std::min<int>((int)lr.ids.size(), kMaxTimed);
+    // the registered kernel this tune competes with: the cached one, else the default
+    const int incumbent = cached >= 0 ? cached : lr.ids[0];
 
     // scratch operands of this exact shape, filled on the device.  A GEMV is
     // bandwidth bound and runs on weights streamed from HBM, so it is timed
@@ -611,34 +706,38 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
                              ? (int)std::min<size_t>(16, std::max<size_t>(1, (kColdBytes + up(b_bytes) - 1) / up(b_bytes)))
                              : 1;
     const size_t need = up(a_bytes) + (size_t)b_copies * up(b_bytes) + up(c_bytes);
-    hipError_t e;
-    if (d->scratch_bytes < need) {
-        if (d->scratch) (void)hipFree(d->scratch);
-        d->scratch = nullptr;
-        d->scratch_bytes = 0;
-        e = hipMalloc(&d->scratch, need);
-        if (e != hipSuccess) {
-            (void)hipGetLastError();
-            return fail(NNJIT_ENOMEM, "tuner scratch of %zu bytes", need);
-        }
-        d->scratch_bytes = need;
+    int64_t ws_floats = 0;
+    for (int i = 0; i < limit; ++i)
+        ws_floats = std::max(ws_floats, geometry_of(configs()[lr.ids[i]], batch, M, N, K).ws_floats);
+
+    TuneResources res;
+    hipError_t e = hipStreamCreateWithFlags(&res.stream, hipStreamNonBlocking);
+    if (e != hipSuccess) return hip_fail(e, "hipStreamCreate");
+    if ((e = hipMalloc(&res.scratch, need)) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(NNJIT_ENOMEM, "tuner scratch of %zu bytes", need);
     }
-    char *base = (char *)d->scratch;
+    if (ws_floats > 0 && (e = hipMalloc((void **)&res.ws, (size_t)ws_floats * sizeof(float))) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(NNJIT_ENOMEM, "tuner split-K scratch of %lld floats", (long long)ws_floats);
+    }
+    char *base = (char *)res.scratch;
     char *b0 = base + up(a_bytes);
     c.A = base;
     c.B = b0;
     c.C = b0 + (size_t)b_copies * up(b_bytes);
-    c.stream = d->tune_stream;
-    if ((e = launch_fill_uniform((void *)c.A, q4 ? K : batch * M * K, dtype, 1234u, c.stream)) != hipSuccess)
+    c.stream = res.stream;
+    if ((e = launch_fill((void *)c.A, q4 ? K : batch * M * K, dtype == NNJIT_F16 ? FILL_F16 : FILL_F32, kActScale,
+                         1234u, c.stream)) != hipSuccess)
         return hip_fail(e, "scratch fill");
     for (int i = 0; i < b_copies; ++i) {
         char *dst = b0 + (size_t)i * up(b_bytes);
-        // 4-bit codes: any bit pattern is a valid code word, so the words are
-        // filled as fp32 values; the scales follow as fp16
-        e = q4 ? launch_fill_uniform(dst, N * c.ldb, NNJIT_F32, 5678u + i, c.stream)
-               : launch_fill_uniform(dst, batch * K * N, dtype, 5678u + i, c.stream);
-        if (e == hipSuccess && q4)
-            e = launch_fill_uniform(dst + up(q4_codes), N * c.lds, NNJIT_F16, 9012u + i, c.stream);
+        // 4-bit codes: any word is valid, so they are random words; the
+        // scales follow as fp16 (their sign does not matter to the timing)
+        e = q4 ? launch_fill(dst, N * c.ldb, FILL_WORDS, 0.f, 5678u + i, c.stream)
+               : launch_fill(dst, batch * K * N, dtype == NNJIT_F16 ? FILL_F16 : FILL_F32, kWeightScale, 5678u + i,
+                             c.stream);
+        if (e == hipSuccess && q4) e = launch_fill(dst + up(q4_codes), N * c.lds, FILL_F16, 0.006f, 9012u + i, c.stream);
         if (e != hipSuccess) return hip_fail(e, "scratch fill");
     }
     int rot = 0;
@@ -646,7 +745,7 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
         c.B = b0 + (size_t)(rot % b_copies) * up(b_bytes);
         if (q4) c.Sc = (const char *)c.B + up(q4_codes);
         ++rot;
-        return launch(*d, cfg, c);
+        return launch(*d, cfg, c, res.ws, set);
     };
 
     // A burst of n launches captured as a graph on the tuner's stream, so that
@@ -654,9 +753,8 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
     // less time on the device than on the host (a few-microsecond kernel
     // launched eagerly measures the host's launch rate).  nullptr when the
     // capture fails; the caller then launches eagerly.
-    const bool use_graphs = env_int("NNJIT_TUNE_GRAPH", 1) != 0;
     auto capture_burst = [&](const Config &cfg, int n) -> hipGraphExec_t {
-        if (!use_graphs) return nullptr;
+        if (!set.tune_graph) return nullptr;
         if (hipStreamBeginCapture(c.stream, hipStreamCaptureModeThreadLocal) != hipSuccess) {
             (void)hipGetLastError();
             return nullptr;
@@ -676,15 +774,12 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
         return x;
     };
 
-    const int reps = std::max(1, env_int("NNJIT_TUNE_REPS", 3));
-    const double budget_ms = (double)env_int("NNJIT_TUNE_BUDGET_MS", 900);
-    const bool trace = env_flag("NNJIT_TRACE");
+    const int reps = set.tune_reps;
+    const double budget_ms = (double)set.tune_budget_ms;
+    const bool trace = set.trace;
     std::vector<hipEvent_t> ev(2 * (reps + 1));
     for (auto &x : ev)
-        if ((e = hipEventCreate(&x)) != hipSuccess) return hip_fail(e, "hipEventCreate");
-    auto destroy = [&]() {
-        for (auto &x : ev) (void)hipEventDestroy(x);
-    };
+        if ((e = res.event(&x)) != hipSuccess) return hip_fail(e, "hipEventCreate");
 
     // A candidate's cost is the device time per launch of a burst of
     // back-to-back launches (what a stream or a graph of dependent products
@@ -696,13 +791,12 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
     int best = -1;
     double best_us = 1e300, best_first_us = 1e300;
     std::map<int, double> timed;
-    const int limit = std::min<int>((int)lr.ids.size(), kMaxTimed);
     for (int i = 0; i < limit; ++i) {
         if (ms_since(te) > budget_ms) break;
         const Config &cfg = configs()[lr.ids[i]];
         // warm-up launch (untimed: the first launch of a kernel pays one-time
         // costs), then one single timed launch that decides the early abort
-        rc = launch_next(cfg);
+        int rc = launch_next(cfg);
         if (rc == NNJIT_OK) {
             (void)hipEventRecord(ev[0], c.stream);
             rc = launch_next(cfg);
@@ -714,10 +808,7 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
             (void)hipGetLastError();
             continue;
         }
-        if ((e = hipEventSynchronize(ev[1])) != hipSuccess) {
-            destroy();
-            return hip_fail(e, "candidate warm-up");
-        }
+        if ((e = hipEventSynchronize(ev[1])) != hipSuccess) return hip_fail(e, "candidate warm-up");
         float first_ms = 0.f;
         (void)hipEventElapsedTime(&first_ms, ev[0], ev[1]);
         const double first_us = first_ms * 1e3;
@@ -756,7 +847,6 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
         }
         if ((e = hipEventSynchronize(ev[1 + 2 * reps])) != hipSuccess) {
             drop_graphs();
-            destroy();
             return hip_fail(e, "candidate timing");
         }
         drop_graphs();
@@ -774,7 +864,6 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
         }
         best_first_us = std::min(best_first_us, first_us);
     }
-    destroy();
     if (best < 0) return fail(NNJIT_ENOCFG, "every candidate failed");
 
     // Run-off: the candidates within 15% of the best (at most kRunoff) are
@@ -782,16 +871,16 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
     // rounds so that clock drift reaches them alike; each keeps the median
     // of its rounds.  Short bursts of a few-microsecond kernel cannot tell
     // such candidates apart.
-    if (env_int("NNJIT_TUNE_RUNOFF", 1) != 0 && ms_since(te) < budget_ms) {
+    if (set.tune_runoff && ms_since(te) < budget_ms) {
         std::vector<std::pair<double, int>> close;
         for (const auto &kv : timed)
             if (kv.second <= best_us * 1.15) close.emplace_back(kv.second, kv.first);
         std::sort(close.begin(), close.end());
         if ((int)close.size() > kRunoff) {
-            // the incumbent (cached, else the default) keeps its place, so the
-            // 3% rule below compares run-off times with run-off times
-            const int inc_id = hit != g_tuned.end() ? hit->second.cfg : lr.ids[0];
-            auto it = std::find_if(close.begin(), close.end(), [&](const std::pair<double, int> &x) { return x.second == inc_id; });
+            // the incumbent keeps its place, so the 3% rule below compares
+            // run-off times with run-off times
+            auto it = std::find_if(close.begin(), close.end(),
+                                   [&](const std::pair<double, int> &x) { return x.second == incumbent; });
             if (it != close.end() && it - close.begin() >= kRunoff) std::swap(*it, close[kRunoff - 1]);
             close.resize(kRunoff);
         }
@@ -802,7 +891,7 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
             std::vector<hipEvent_t> rev(2 * nc * rounds);
             bool ok = true;
             for (auto &x : rev)
-                if (hipEventCreate(&x) != hipSuccess) ok = false;
+                if (res.event(&x) != hipSuccess) ok = false;
             std::vector<hipGraphExec_t> rg(nc * rounds, nullptr);
             for (int r = 0; r < rounds && ok; ++r)
                 for (int j = 0; j < nc; ++j) rg[r * nc + j] = capture_burst(configs()[close[j].second], burst2);
@@ -845,13 +934,11 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
             }
             for (auto &x : rg)
                 if (x) (void)hipGraphExecDestroy(x);
-            for (auto &x : rev) (void)hipEventDestroy(x);
         }
     }
     t_stats.eval_ms = ms_since(te);
     // the registered kernel (cached, else the default) is replaced only by one
     // that is significantly (>= 3%) faster
-    int incumbent = hit != g_tuned.end() ? hit->second.cfg : lr.ids[0];
     auto inc = timed.find(incumbent);
     if (inc != timed.end() && best != incumbent && best_us > inc->second / 1.03) {
         best = incumbent;
@@ -869,11 +956,22 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
             tu.ranked.emplace_back(bt.second, bt.first);
         }
     }
-    g_tuned[key] = tu;
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        // another thread may have registered this shape meanwhile: its entry
+        // stays unless this result is significantly faster
+        auto now = g_tuned.find(key);
+        if (now != g_tuned.end() && now->second.cfg != cached && !(best_us < now->second.us / 1.03)) {
+            best = now->second.cfg;
+            best_us = now->second.us;
+        } else {
+            g_tuned[key] = tu;
+        }
+    }
     t_stats.chosen = best;
     t_stats.best_us = best_us;
     t_stats.wall_ms = ms_since(t0);
-    if (env_flag("NNJIT_LOG"))
+    if (set.log)
         fprintf(stderr, "[nnjit] tuned kind=%d dtype=%d batch=%lld M=%lld N=%lld K=%lld -> %d (%s S=%d) %.2f us, lite %d, timed %d, %.1f ms\n",
                 kind, dtype, (long long)batch, (long long)M, (long long)N, (long long)K, best,
                 configs()[best].v->name, configs()[best].split, best_us, t_stats.n_lite, t_stats.n_timed, t_stats.wall_ms);
@@ -1021,7 +1119,15 @@ int nnjit_lite_space(int kind, int dtype, int64_t batch, int64_t M, int64_t N, i
     return (int)lr.ids.size();
 }
 
-int nnjit_last_tune_stats(nnjit_tune_stats *out) {
+int nnjit_last_tune_stats(double *wall_ms, int *n_enum, int *n_pruned, int *n_timed) {
+    if (wall_ms) *wall_ms = t_stats.wall_ms;
+    if (n_enum) *n_enum = t_stats.n_enumerated;
+    if (n_pruned) *n_pruned = t_stats.n_lite;
+    if (n_timed) *n_timed = t_stats.n_timed;
+    return NNJIT_OK;
+}
+
+int nnjit_last_tune_stats_ex(nnjit_tune_stats *out) {
     if (!out) return fail(NNJIT_EINVAL, "NULL output");
     *out = t_stats;
     return NNJIT_OK;
@@ -1100,18 +1206,21 @@ int nnjit_cache_clear(void) {
     g_online.clear();
     g_tuned.clear();
     g_default.clear();
+    // outgrown split-K buffers: no launch may still be using them once the
+    // device is idle
+    int cur = -1;
+    (void)hipGetDevice(&cur);
     for (auto &kv : g_devices) {
-        if (kv.second.scratch) {
-            int cur = -1;
-            (void)hipGetDevice(&cur);
-            (void)hipSetDevice(kv.first);
-            (void)hipDeviceSynchronize();
-            (void)hipFree(kv.second.scratch);
-            if (cur >= 0) (void)hipSetDevice(cur);
-        }
-        kv.second.scratch = nullptr;
-        kv.second.scratch_bytes = 0;
+        if (kv.second.retired.empty()) continue;
+        (void)hipSetDevice(kv.first);
+        (void)hipDeviceSynchronize();
+        for (float *p : kv.second.retired) (void)hipFree(p);
+        kv.second.retired.clear();
     }
+    if (cur >= 0) (void)hipSetDevice(cur);
+    (void)hipGetLastError();
+    g_set = read_settings();
+    g_set_loaded = true;
     return NNJIT_OK;
 }
 
@@ -1192,8 +1301,25 @@ int nnjit_cache_load(const char *path) {
     return n;
 }
 
+int nnjit_stream_read(const void *src, int64_t bytes, void *sink, int workgroups, void *stream) {
+    t_err.clear();
+    if (bytes < 0 || bytes % 16) return fail(NNJIT_EINVAL, "bytes=%lld must be a non-negative multiple of 16", (long long)bytes);
+    if (workgroups < 1 || workgroups > (1 << 20)) return fail(NNJIT_EINVAL, "workgroups=%d out of [1, 2^20]", workgroups);
+    if (bytes > 0 && (!src || ((uintptr_t)src & 15u))) return fail(NNJIT_EINVAL, "src is NULL or not 16-byte aligned");
+    if (!sink) return fail(NNJIT_EINVAL, "sink is NULL");
+    if (bytes == 0) return NNJIT_OK;
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        Device *d = nullptr;
+        const int rc = device_ready(&d);
+        if (rc != NNJIT_OK) return rc;
+    }
+    const hipError_t e = launch_stream_read(src, bytes, (unsigned *)sink, workgroups, (hipStream_t)stream);
+    return e == hipSuccess ? NNJIT_OK : hip_fail(e, "stream_read");
+}
+
 const char *nnjit_last_error(void) { return t_err.c_str(); }
 
-int nnjit_version(void) { return (0 << 16) | 1; }
+int nnjit_version(void) { return (0 << 16) | 2; }
 
 }  // extern "C"

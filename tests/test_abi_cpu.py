@@ -67,6 +67,60 @@ def test_validation_without_gpu(lib):
     assert nj.nnjit_gemv_q4_config(f16, 64, 64, 32, 1, 2, 8, 3, 2, 4, None) == nj.NNJIT_EINVAL
 
 
+def test_tune_stats_forms(lib):
+    """The four-pointer statistics call and the full struct agree, and NULL
+    outputs are allowed (nothing tuned yet on this thread: zeros)."""
+    import ctypes
+    assert lib.nnjit_last_tune_stats(None, None, None, None) == nj.NNJIT_OK
+    short = nj.nnjit_last_tune_stats()
+    full = nj.nnjit_last_tune_stats_ex()
+    assert short == {"wall_ms": full["wall_ms"], "n_enum": full["n_enumerated"], "n_pruned": full["n_lite"],
+                     "n_timed": full["n_timed"]}
+    assert lib.nnjit_last_tune_stats_ex(ctypes.cast(None, ctypes.POINTER(nj.TuneStats))) == nj.NNJIT_EINVAL
+
+
+def test_binding_rejects_bad_operands(lib):
+    """The tensor conveniences refuse, before any library call, operands that
+    the entry points would read or write out of bounds."""
+    import torch
+    f32, f16 = torch.float32, torch.float16
+    A = torch.zeros(4, 8)
+    B = torch.zeros(8, 6)
+    with pytest.raises(TypeError, match="B is"):
+        nj.matmul(A, B.to(f16))
+    with pytest.raises(TypeError, match="C must be float32"):
+        nj.matmul(A, B, torch.zeros(4, 6, dtype=f16))
+    with pytest.raises(ValueError, match="C has shape"):
+        nj.matmul(A, B, torch.zeros(4, 5))
+    with pytest.raises(ValueError, match="inner dimensions"):
+        nj.matmul(A, torch.zeros(7, 6))
+    with pytest.raises(ValueError, match="rows overlap"):
+        nj.matmul(A, torch.zeros(1, 6).expand(8, 6))      # expanded view: row stride 0
+    with pytest.raises(ValueError, match="unit stride"):
+        nj.matmul(A, torch.zeros(6, 8).t())               # transposed view
+    with pytest.raises(ValueError, match="one GPU"):
+        nj.matmul(A, B)                                   # host tensors
+    Ab, Bb = torch.zeros(3, 4, 8), torch.zeros(3, 8, 6)
+    with pytest.raises(ValueError, match="output slices overlap"):
+        nj.batched_matmul(Ab, Bb, torch.zeros(4, 6).expand(3, 4, 6))
+    with pytest.raises(ValueError, match="batch sizes"):
+        nj.batched_matmul(Ab, torch.zeros(2, 8, 6))
+    with pytest.raises(ValueError, match="C has shape"):
+        nj.batched_matmul(Ab, Bb, torch.zeros(3, 4, 7))
+    with pytest.raises(ValueError, match="one GPU"):
+        nj.batched_matmul(Ab, Bb)
+    # 4-bit GEMV
+    x = torch.zeros(64, dtype=f16)
+    Wq = torch.zeros(16, 8, dtype=torch.int32)
+    S = torch.zeros(16, 2, dtype=f16)
+    with pytest.raises(ValueError, match="rows too short"):
+        nj.gemv_q4(x, Wq[:, :7], S, 32, 16)
+    with pytest.raises(ValueError, match="y must be"):
+        nj.gemv_q4(x, Wq, S, 32, 16, y=torch.zeros(15))
+    with pytest.raises(ValueError, match="one GPU"):
+        nj.gemv_q4(x, Wq, S, 32, 16)
+
+
 def test_no_gpu_is_ehip_not_abort(lib):
     try:
         import torch

@@ -129,7 +129,7 @@ def test_llama_decode_q4_parity(index):
     op = workloads.workload(name)[index]
     x, Wq, S = workloads.op_inputs(name, index)
     cfg = nj.check(nj.nnjit_tune_gemv_q4(op.N, op.K, op.group))
-    st = nj.nnjit_last_tune_stats()
+    st = nj.nnjit_last_tune_stats_ex()
     print(f"{op.name}: tuned -> {nj.nnjit_config_info(cfg)} | {st['best_us']:.2f} us, lite {st['n_lite']}, "
           f"timed {st['n_timed']}, tune {st['wall_ms']:.0f} ms", flush=True)
     lite, _, _, _ = nj.nnjit_lite_space(nj.NNJIT_KIND_GEMV_Q4, nj.NNJIT_F16, op.group, 1, op.N, op.K)

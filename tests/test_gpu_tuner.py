@@ -33,7 +33,7 @@ def test_tune_returns_measured_lite_config_within_budget(name, index):
     dt = dtype_code(op.dtype)
     nj.nnjit_cache_clear()
     cfg = nj.check(_tune(op))
-    st = nj.nnjit_last_tune_stats()
+    st = nj.nnjit_last_tune_stats_ex()
     lite, n, n_enum, _ = nj.nnjit_lite_space(kind_of(op.batch, op.M), dt, op.batch, op.M, op.N, op.K)
     print(f"{op.name}: cfg {cfg} {nj.nnjit_config_info(cfg).split()[2]} best {st['best_us']:.2f} us "
           f"(default {st['default_us']:.2f}), lite {st['n_lite']}/{n_enum}, timed {st['n_timed']}, "
@@ -44,7 +44,7 @@ def test_tune_returns_measured_lite_config_within_budget(name, index):
     assert st["wall_ms"] <= 1000.0, st
     # cache hit
     assert _tune(op) == cfg
-    st2 = nj.nnjit_last_tune_stats()
+    st2 = nj.nnjit_last_tune_stats_ex()
     assert st2["cache_hit"] == 1 and st2["wall_ms"] < 5.0
     assert nj.nnjit_cached_config(kind_of(op.batch, op.M), dt, op.batch, op.M, op.N, op.K) == cfg
 
@@ -59,13 +59,15 @@ def test_measured_resources_are_used():
 def test_failing_candidate_is_skipped(monkeypatch):
     op = workloads.workload("bart_base_layer_seq128_f32")[1]
     lite, _, _, _ = nj.nnjit_lite_space(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, op.M, op.N, op.K)
-    nj.nnjit_cache_clear()
     monkeypatch.setenv("NNJIT_FAULT_CONFIG", str(lite[0]))
-    cfg = nj.check(nj.nnjit_tune(op.M, op.N, op.K, nj.NNJIT_F32))
-    st = nj.nnjit_last_tune_stats()
-    assert cfg != lite[0] and cfg in lite and st["n_failed"] >= 1
-    monkeypatch.delenv("NNJIT_FAULT_CONFIG")
-    nj.nnjit_cache_clear()
+    nj.nnjit_cache_clear()   # the library reads its environment here
+    try:
+        cfg = nj.check(nj.nnjit_tune(op.M, op.N, op.K, nj.NNJIT_F32))
+        st = nj.nnjit_last_tune_stats_ex()
+        assert cfg != lite[0] and cfg in lite and st["n_failed"] >= 1
+    finally:
+        monkeypatch.delenv("NNJIT_FAULT_CONFIG")
+        nj.nnjit_cache_clear()
 
 
 
@@ -77,12 +79,20 @@ def test_graph_and_eager_timing_both_tune(monkeypatch, graph):
     and then computes the oracle's exact sums (small integers); a split-K
     GEMV shape exercises the scratch allocated before capture."""
     monkeypatch.setenv("NNJIT_TUNE_GRAPH", graph)
+    try:
+        _graph_and_eager_timing_both_tune(graph)
+    finally:
+        monkeypatch.delenv("NNJIT_TUNE_GRAPH")
+        nj.nnjit_cache_clear()
+
+
+def _graph_and_eager_timing_both_tune(graph):
     for name, index in (("bart_base_layer_seq128_f32", 4), ("llama2_7b_decode_f16", 1)):
         op = workloads.workload(name)[index]
         dt = dtype_code(op.dtype)
         nj.nnjit_cache_clear()
         cfg = nj.check(_tune(op))
-        st = nj.nnjit_last_tune_stats()
+        st = nj.nnjit_last_tune_stats_ex()
         lite, _, _, _ = nj.nnjit_lite_space(kind_of(op.batch, op.M), dt, op.batch, op.M, op.N, op.K)
         assert cfg in lite and st["n_timed"] >= 1 and st["n_failed"] == 0, st
         A, B = workloads.small_int_operands(8080, op.batch, op.M, op.K, op.N, op.dtype)
@@ -92,7 +102,6 @@ def test_graph_and_eager_timing_both_tune(monkeypatch, graph):
         else:
             C = nj.batched_matmul(dev(A), dev(B))
         assert np.array_equal(host(C).reshape(R.shape), R), f"{op.name} graph={graph}"
-    nj.nnjit_cache_clear()
 
 def test_dispatch_uses_tuned_config_and_matches_oracle():
     name, i = "bart_base_layer_seq128_f32", 3
@@ -211,7 +220,7 @@ def test_kernel_database_roundtrip(tmp_path):
     assert nj.check(nj.nnjit_cache_load(str(path))) == len([l for l in lines if not l.startswith("#")])
     assert nj.nnjit_cached_config(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, op.M, op.N, op.K) == cfg
     assert nj.check(nj.nnjit_tune(op.M, op.N, op.K, nj.NNJIT_F32)) == cfg
-    assert nj.nnjit_last_tune_stats()["cache_hit"] == 1
+    assert nj.nnjit_last_tune_stats_ex()["cache_hit"] == 1
     assert nj.nnjit_cache_load(str(tmp_path / "missing.txt")) == nj.NNJIT_EINVAL
 
 
@@ -222,7 +231,7 @@ def test_ranked_candidates_and_database_merge(tmp_path):
     nj.nnjit_cache_clear()
     cfg = nj.check(nj.nnjit_tune(op.M, op.N, op.K, nj.NNJIT_F32))
     ranked = nj.nnjit_cached_ranked(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, op.M, op.N, op.K)
-    st = nj.nnjit_last_tune_stats()
+    st = nj.nnjit_last_tune_stats_ex()
     assert ranked[0][0] == cfg and 1 <= len(ranked) <= 5
     assert len(ranked) == min(5, st["n_timed"])
     assert all(a[1] <= b[1] for a, b in zip(ranked[1:], ranked[2:]))     # the others by time
@@ -338,3 +347,148 @@ def test_concurrent_host_threads_on_own_streams():
         th.join(timeout=120)
     assert not errors, errors
     assert results == {0: True, 1: True, 2: True, 3: True}
+
+
+def test_graph_replay_after_scratch_growth():
+    """A graph captured on a stream keeps the split-K scratch it was captured
+    with: a larger split-K call on the same stream afterwards grows the
+    scratch (the old buffer is retired, not freed), and every replay of the
+    earlier graph, interleaved with further large calls, still gives the
+    oracle's exact sums."""
+    import torch
+    cfg = next(c for c in nj.configs()
+               if c["family"] == "gemm_f32" and c["vec"] == 16 and c["split"] == 4 and not c.get("direct"))
+    small = (64, 192, 512)
+    large = (256, 1024, 1024)
+    cases = {}
+    for tag, (M, N, K) in (("small", small), ("large", large)):
+        A, B = workloads.small_int_operands(5150 + M, 1, M, K, N, "f32")
+        cases[tag] = (M, N, K, dev(A), dev(B), oracle.matmul(A, B))
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        outs = {t: torch.full((v[0], v[1]), float("nan"), dtype=torch.float32, device="cuda:0")
+                for t, v in cases.items()}
+
+    def call(tag):
+        M, N, K, dA, dB, _ = cases[tag]
+        return nj.nnjit_matmul_config(cfg["id"], 1, M, N, K, dA, K, 0, dB, N, 0, outs[tag], N, 0, nj.NNJIT_F32,
+                                      side)
+
+    with torch.cuda.stream(side):
+        assert call("small") == nj.NNJIT_OK   # the stream's scratch sized for the small product
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        assert call("small") == nj.NNJIT_OK
+    with torch.cuda.stream(side):
+        assert call("large") == nj.NNJIT_OK   # grows the scratch past the captured buffer
+    torch.cuda.synchronize()
+    assert np.array_equal(host(outs["large"]), cases["large"][5])
+    for rep in range(4):
+        outs["small"].fill_(float("nan"))
+        outs["large"].fill_(float("nan"))
+        torch.cuda.synchronize()
+        with torch.cuda.stream(side):
+            g.replay()
+            assert call("large") == nj.NNJIT_OK
+        torch.cuda.synchronize()
+        assert np.array_equal(host(outs["small"]), cases["small"][5]), f"replay {rep}"
+        assert np.array_equal(host(outs["large"]), cases["large"][5]), f"large call {rep}"
+
+
+def test_product_served_from_loaded_database(tmp_path):
+    """A shape tuned in one session, saved to the kernel database, is served
+    after a cache clear and a load from that file: the dispatch runs the
+    stored configuration and its result meets the acceptance bar against
+    the oracle (workload values, every element)."""
+    name, index = "t5_large_layer_b4s256_f32", 5
+    op = workloads.workload(name)[index]
+    nj.nnjit_cache_clear()
+    cfg = nj.check(nj.nnjit_tune(op.M, op.N, op.K, nj.NNJIT_F32))
+    path = tmp_path / "db.txt"
+    assert nj.check(nj.nnjit_cache_save(str(path))) == 1
+    nj.nnjit_cache_clear()
+    assert nj.nnjit_cached_config(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, op.M, op.N, op.K) == nj.NNJIT_ENOCFG
+    assert nj.check(nj.nnjit_cache_load(str(path))) == 1
+    assert nj.nnjit_cached_config(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, op.M, op.N, op.K) == cfg
+    A, B = workloads.op_inputs(name, index)
+    dA, dB = dev(A), dev(B)
+    C = host(nj.matmul(dA, dB))
+    assert np.array_equal(C, host(nj.matmul(dA, dB, cfg=cfg)))     # the stored configuration ran
+    res = accept.check(C, oracle.matmul(A, B), A, B, "f32")
+    assert res["ok"], res
+    nj.nnjit_cache_clear()
+
+
+def test_online_failing_candidate_falls_back(monkeypatch):
+    """Online mode with a candidate that cannot launch: that call's product is
+    computed by the registered configuration (exact sums), the candidate is
+    never registered, and the shape still ends tuned."""
+    import torch
+    M, N, K = 96, 256, 384
+    lite, _, _, _ = nj.nnjit_lite_space(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, M, N, K)
+    bad = lite[1]
+    A, B = workloads.small_int_operands(4343, 1, M, K, N, "f32")
+    R = oracle.matmul(A, B)
+    dA, dB = dev(A), dev(B)
+    monkeypatch.setenv("NNJIT_FAULT_CONFIG", str(bad))
+    nj.nnjit_cache_clear()   # the library reads its environment here
+    prev = nj.nnjit_set_online(True)
+    try:
+        for calls in range(1, 400):
+            C = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda:0")
+            nj.matmul(dA, dB, C)
+            assert np.array_equal(host(C), R), f"call {calls}"
+            st = nj.nnjit_online_status(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, M, N, K)
+            if st["state"] == "tuned":
+                break
+        assert st["state"] == "tuned"
+        cfg = nj.nnjit_cached_config(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, M, N, K)
+        assert cfg != bad
+        assert bad not in [c for c, _ in nj.nnjit_cached_ranked(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, M, N, K)]
+    finally:
+        nj.nnjit_set_online(prev)
+        monkeypatch.delenv("NNJIT_FAULT_CONFIG")
+        nj.nnjit_cache_clear()
+
+
+def test_tune_does_not_block_dispatch_on_other_threads():
+    """While one thread tunes a large shape (hundreds of milliseconds),
+    another thread's calls return without waiting for it; their results are
+    exact."""
+    import threading
+    import torch
+    nj.nnjit_cache_clear()
+    M, N, K = 64, 128, 256
+    A, B = workloads.small_int_operands(4444, 1, M, K, N, "f32")
+    R = oracle.matmul(A, B)
+    dA, dB = dev(A), dev(B)
+    C = nj.matmul(dA, dB)                  # device state and this shape's default set up
+    torch.cuda.synchronize()
+    started, errors = threading.Event(), []
+
+    def tuner():
+        started.set()
+        try:
+            nj.check(nj.nnjit_tune(512, 32000, 4096, nj.NNJIT_F32))
+        except Exception as e:   # reported below
+            errors.append(repr(e))
+
+    th = threading.Thread(target=tuner)
+    th.start()
+    started.wait()
+    import time
+    time.sleep(0.05)                       # the tune is under way (scratch set-up, candidates)
+    alive_before = th.is_alive()
+    for _ in range(20):
+        nj.matmul(dA, dB, C)
+    alive_after = th.is_alive()
+    th.join(timeout=120)
+    assert not errors, errors
+    assert np.array_equal(host(C), R)
+    st_tuned = nj.nnjit_cached_config(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, 512, 32000, 4096)
+    assert st_tuned >= 0
+    if alive_before:
+        assert alive_after, "the calls waited for the tune to finish"
+    nj.nnjit_cache_clear()
