@@ -125,6 +125,27 @@ int nnjit_batched_matmul(int64_t batch, int64_t M, int64_t N, int64_t K,
                          void *C, int64_t ldc, int64_t strideC,
                          int dtype, void *stream);
 
+/* nnjit_batched_matmul for callers that cannot allocate device memory:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation.  Same arguments, results and dispatch (tuned, else default
+ * configuration; a shape being tuned online is served by its registered
+ * configuration without measuring), but split-K partials go to a fixed
+ * scratch array of 128 MiB that the library holds on each GPU for the life
+ * of the process, and the call makes no allocating HIP call
+ * (the first call on a device initialises it, which only takes that array's
+ * address).  A configuration that needs more split-K scratch than 128 MiB
+ * (S x batch x M x N x 4 bytes) is refused with NNJIT_ENOMEM before any
+ * launch.  All calls on one GPU share the array: calls that overlap in time
+ * on that GPU (on different streams, or replays of captured graphs that run
+ * concurrently) race on it and must be ordered by the caller.  Nothing in
+ * the scratch needs to start at zero: each call writes every partial it
+ * reads. */
+int nnjit_batched_matmul_noalloc(int64_t batch, int64_t M, int64_t N, int64_t K,
+                                 const void *A, int64_t lda, int64_t strideA,
+                                 const void *B, int64_t ldb, int64_t strideB,
+                                 void *C, int64_t ldc, int64_t strideC,
+                                 int dtype, void *stream);
+
 /* Just-in-time tuning of one shape (Sec. 3 JIT phase, Sec. 5.2 lite space;
  * the problem statement: one kernel per operator shape, Sec. 3):
  * builds the shape's lite space (enumerate the compiled configurations of

@@ -26,7 +26,7 @@ NNJIT_KIND_GEMM, NNJIT_KIND_BATCHED, NNJIT_KIND_GEMV, NNJIT_KIND_GEMV_Q4 = 0, 1,
 NNJIT_OK, NNJIT_EINVAL, NNJIT_EDTYPE, NNJIT_ENOCFG, NNJIT_EHIP, NNJIT_ENOMEM = 0, -1, -2, -3, -4, -5
 ERROR_NAMES = {-1: "NNJIT_EINVAL", -2: "NNJIT_EDTYPE", -3: "NNJIT_ENOCFG", -4: "NNJIT_EHIP", -5: "NNJIT_ENOMEM"}
 
-EXPORTED = ["nnjit_matmul", "nnjit_batched_matmul", "nnjit_tune", "nnjit_tune_batched", "nnjit_matmul_config",
+EXPORTED = ["nnjit_matmul", "nnjit_batched_matmul", "nnjit_batched_matmul_noalloc", "nnjit_tune", "nnjit_tune_batched", "nnjit_matmul_config",
             "nnjit_gemv_q4", "nnjit_tune_gemv_q4", "nnjit_gemv_q4_config",
             "nnjit_num_configs", "nnjit_config_info", "nnjit_config_resources", "nnjit_lite_space",
             "nnjit_last_tune_stats", "nnjit_last_tune_stats_ex", "nnjit_last_tune_trace", "nnjit_cached_config", "nnjit_cached_ranked",
@@ -84,6 +84,7 @@ def load(build_if_missing: bool = False) -> ctypes.CDLL:
         sig = {
             "nnjit_matmul": [i64, i64, i64, vp, i64, vp, i64, vp, i64, ci, vp],
             "nnjit_batched_matmul": [i64, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64, i64, ci, vp],
+            "nnjit_batched_matmul_noalloc": [i64, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64, i64, ci, vp],
             "nnjit_tune": [i64, i64, i64, ci],
             "nnjit_tune_batched": [i64, i64, i64, i64, ci],
             "nnjit_matmul_config": [ci, i64, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64, i64, ci, vp],
@@ -146,6 +147,12 @@ def nnjit_batched_matmul(batch, M, N, K, A, lda, strideA, B, ldb, strideB, C, ld
                          stream=None) -> int:
     return load().nnjit_batched_matmul(batch, M, N, K, _ptr(A), lda, strideA, _ptr(B), ldb, strideB,
                                        _ptr(C), ldc, strideC, dtype, _stream(stream))
+
+
+def nnjit_batched_matmul_noalloc(batch, M, N, K, A, lda, strideA, B, ldb, strideB, C, ldc, strideC, dtype,
+                                 stream=None) -> int:
+    return load().nnjit_batched_matmul_noalloc(batch, M, N, K, _ptr(A), lda, strideA, _ptr(B), ldb, strideB,
+                                               _ptr(C), ldc, strideC, dtype, _stream(stream))
 
 
 def nnjit_tune(M, N, K, dtype) -> int:

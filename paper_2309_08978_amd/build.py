@@ -25,7 +25,7 @@ LIB = os.path.join(HERE, "libnnjit.so")
 OBJDIR = os.path.join(HERE, "_build")
 ARCH = os.environ.get("NNJIT_ARCH", "gfx950")
 
-SOURCES = ["gemm_f32.hip", "gemm_f16.hip", "gemv.hip", "gemv_q4.hip", "space.cpp", "runtime.cpp"]
+SOURCES = ["gemm_f32.hip", "gemm_f16.hip", "gemv.hip", "gemv_q4.hip", "noalloc.hip", "space.cpp", "runtime.cpp"]
 
 COMMON = ["-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-function",
           "-I", CSRC, "-I", os.path.join(ROOT, "include")]

@@ -95,6 +95,12 @@ extern const int kNumGemvQ4Variants;
 hipError_t launch_splitk_reduce(const float *ws, int S, int batch, int M, int N, float *C, long long ldc,
                                 long long sC, hipStream_t stream);
 enum FillKind { FILL_F32 = 0, FILL_F16 = 1, FILL_WORDS = 2 };
+// Fixed device scratch of the allocation-free entry point (split-K partials).
+constexpr size_t kNoAllocScratchBytes = (size_t)128 << 20;
+// Device addresses of the library's static device arrays on the current
+// device: that scratch, and 256 bytes of zeros (the load address of
+// out-of-range GEMM elements).
+hipError_t static_buffer_addresses(void **scratch_ptr, void **zero_ptr);
 // Streaming-read reference kernel (bytes % 16 == 0, src 16-byte aligned,
 // sink: `workgroups` words).
 hipError_t launch_stream_read(const void *src, long long bytes, unsigned *sink, int workgroups, hipStream_t stream);

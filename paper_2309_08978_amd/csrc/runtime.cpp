@@ -98,6 +98,7 @@ struct Device {
     std::vector<int> regs;    // measured VGPR+AGPR per lane, per variant
     std::vector<int> spills;  // private segment (scratch) > 0, per variant
     void *zero = nullptr;     // 256 zero bytes: load address of out-of-range GEMM elements
+    float *fixed_ws = nullptr;  // the allocation-free entry point's split-K scratch (a static device array)
     std::map<hipStream_t, Workspace> workspaces;
     std::vector<float *> retired;   // outgrown split-K buffers (see Workspace)
 };
@@ -189,10 +190,12 @@ int device_ready(Device **out) {
             d.regs[gi] = attr.numRegs;
             d.spills[gi] = attr.localSizeBytes > 0 ? 1 : 0;
         }
-        e = hipMalloc(&d.zero, 256);
-        if (e != hipSuccess) return hip_fail(e, "hipMalloc");
-        e = hipMemset(d.zero, 0, 256);
-        if (e != hipSuccess) return hip_fail(e, "hipMemset");
+        // the zero block and the fixed scratch are static device arrays:
+        // their addresses on this device, taken once (nothing is allocated)
+        void *fixed = nullptr;
+        e = static_buffer_addresses(&fixed, &d.zero);
+        if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress");
+        d.fixed_ws = (float *)fixed;
         d.ready = true;
     }
     *out = &d;
@@ -593,6 +596,48 @@ int run(const Call &c, int forced) {
         }
     }
     return launch_on_stream(*d, *cfg, c);
+}
+
+// The allocation-free variant of run(): the configuration nnjit_matmul /
+// nnjit_batched_matmul would use (online shapes are served by their
+// registered configuration without measuring), with split-K partials in the
+// device's fixed static scratch.  Makes no allocating call once the device
+// is initialised (initialisation itself only takes the static arrays'
+// addresses).
+int run_noalloc(const Call &c) {
+    int rc = validate(c);
+    if (rc != NNJIT_OK) return rc;
+    if (is_noop(c)) return NNJIT_OK;
+    std::lock_guard<std::mutex> lk(g_mu);
+    Device *d = nullptr;
+    rc = device_ready(&d);
+    if (rc != NNJIT_OK) return rc;
+    const int kind = kind_of(c);
+    int id = -1;
+    const int env_force = g_set.force_config;
+    if (env_force >= 0 && env_force < (int)configs().size() && configs()[env_force].v->family == family_of(kind, c.dtype))
+        id = env_force;
+    if (id < 0) {
+        const ShapeKey key = key_of(d->ordinal, kind, c);
+        auto it = g_tuned.find(key);
+        auto on = g_online.find(key);
+        if (it != g_tuned.end()) id = it->second.cfg;
+        else if (on != g_online.end()) id = on->second.registered;
+        else id = default_config(*d, kind, c);
+        if (id < 0) return id;
+    }
+    const Config *cfg = &configs()[id];
+    if (cfg->v->vec_bytes == 16 && !aligned_for(kind, c)) {
+        cfg = fallback_config(family_of(kind, c.dtype), c, *d);
+        if (!cfg) return fail(NNJIT_ENOCFG, "no element-load fallback configuration");
+    }
+    const Geometry g = geometry_of(*cfg, c.batch, c.M, c.N, c.K);
+    if ((size_t)g.ws_floats * sizeof(float) > kNoAllocScratchBytes)
+        return fail(NNJIT_ENOMEM, "configuration %d (%s, split %d) needs %lld bytes of split-K scratch, above the "
+                                  "%zu bytes of the fixed scratch; use nnjit_batched_matmul",
+                    cfg->id, cfg->v->name, cfg->split, (long long)g.ws_floats * (long long)sizeof(float),
+                    kNoAllocScratchBytes);
+    return launch(*d, *cfg, c, d->fixed_ws, g_set);
 }
 
 // -------------------------------------------------------------------- tuner
@@ -998,6 +1043,14 @@ int nnjit_batched_matmul(int64_t batch, int64_t M, int64_t N, int64_t K, const v
     t_err.clear();
     Call c{batch, M, N, K, A, lda, strideA, B, ldb, strideB, C, ldc, strideC, dtype, (hipStream_t)stream};
     return run(c, -1);
+}
+
+int nnjit_batched_matmul_noalloc(int64_t batch, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
+                                 int64_t strideA, const void *B, int64_t ldb, int64_t strideB, void *C, int64_t ldc,
+                                 int64_t strideC, int dtype, void *stream) {
+    t_err.clear();
+    Call c{batch, M, N, K, A, lda, strideA, B, ldb, strideB, C, ldc, strideC, dtype, (hipStream_t)stream};
+    return run_noalloc(c);
 }
 
 int nnjit_matmul_config(int cfg, int64_t batch, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
