@@ -473,6 +473,8 @@ def main(argv=None):
     ap.add_argument("--profile-op", default=None,
                     help="counter-collection mode: tune, run the reference copy, then launch only this product "
                          "--kernel-reps times and print one metadata line")
+    ap.add_argument("--profile-config", default=None,
+                    help="with --profile-op: launch this configuration (name or name:split) instead of the tuned one")
     ap.add_argument("--online-steps", type=int, default=0,
                     help="after the measurement, clear the tuned cache and run this many eager steps with online "
                          "just-in-time tuning, reporting each step's time (the gradual speed-up curve)")
@@ -508,6 +510,32 @@ def main(argv=None):
         tunes = tune_all(runs)
         if args.tuned_cache:
             nj.check(nj.nnjit_cache_save(args.tuned_cache))
+        idx = next(i for i, r in enumerate(runs) if r.op.name == args.profile_op)
+        r = runs[idx]
+        t = tunes[idx]
+        cfg_name, cfg_split = t["config"].split()[0].split("=", 1)[1], int(t["config"].rsplit("split=", 1)[1])
+        call = r.call
+        if args.profile_config:
+            want, _, sp = args.profile_config.partition(":")
+            c = next(c for c in nj.configs() if c["name"] == want and (not sp or c["split"] == int(sp)))
+            cfg_name, cfg_split = c["name"], c["split"]
+            op = r.op
+
+            def call(i, c=c, op=op, r=r):
+                B = r.Bs[i % len(r.Bs)]
+                if op.batch > 1:
+                    nj.check(nj.nnjit_matmul_config(c["id"], op.batch, op.M, op.N, op.K, r.A, op.K, op.M * op.K, B,
+                                                    op.N, op.K * op.N, r.C, op.N, op.M * op.N, _dt(op), None))
+                else:
+                    nj.check(nj.nnjit_matmul_config(c["id"], 1, op.M, op.N, op.K, r.A, op.K, 0, B, op.N, 0, r.C,
+                                                    op.N, 0, _dt(op), None))
+        # warm-up launches of the product (about half a second), so that the
+        # measured ones below run at the clock the timed steps see
+        t_end = time.perf_counter() + 0.5
+        while time.perf_counter() < t_end:
+            for i in range(10):
+                call(i)
+            torch.cuda.synchronize()
         if args.copy_ref_mb > 0:
             src = torch.ones(args.copy_ref_mb << 18, dtype=torch.float32, device="cuda:0")
             dst = torch.empty_like(src)
@@ -515,14 +543,11 @@ def main(argv=None):
                 dst.copy_(src)
             torch.cuda.synchronize()
             del src, dst
-        idx = next(i for i, r in enumerate(runs) if r.op.name == args.profile_op)
-        r = runs[idx]
         for i in range(args.kernel_reps):
-            r.call(i)
+            call(i)
         torch.cuda.synchronize()
-        t = tunes[idx]
-        print(json.dumps({"workload": name, "op": r.op.name, "config": t["config"].split()[0].split("=", 1)[1],
-                          "split": int(t["config"].rsplit("split=", 1)[1]), "reps": args.kernel_reps,
+        print(json.dumps({"workload": name, "op": r.op.name, "config": cfg_name,
+                          "split": cfg_split, "reps": args.kernel_reps,
                           "copy_ref_mb": args.copy_ref_mb, "algorithmic_bytes": r.op.bytes,
                           "digest": nj.kernel_digest()}), flush=True)
         return 0

@@ -133,12 +133,31 @@ def traffic(fetch_dir, write_dir, meta):
             "write": out["write"], "reps": meta["reps"], "copy_ref_mb": meta["copy_ref_mb"]}
 
 
-def mfma_busy(pmc_dir, meta, simds: int = 1024):
+def kernel_duration_us(trace_dir):
+    """Mean start-to-end duration (us) of the library's dispatches after the
+    last reference copy in a --kernel-trace run of bench.py --profile-op
+    (the profiled product's launches), and their kernel names."""
+    path = sorted(glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True))
+    if not path:
+        raise SystemExit(f"no kernel_trace.csv under {trace_dir}")
+    rows = sorted(_rows(path[0]), key=lambda r: int(r["Start_Timestamp"]))
+    copies = [i for i, r in enumerate(rows) if "copyBuffer" in r["Kernel_Name"] or "copy_kernel" in r["Kernel_Name"]]
+    after = [r for r in rows[(copies[-1] + 1 if copies else 0):] if "nnjit" in r["Kernel_Name"]]
+    if not after:
+        return None, []
+    d = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in after]
+    return statistics.mean(d), sorted({_short(r["Kernel_Name"]) for r in after})
+
+
+def mfma_busy(pmc_dir, meta, simds: int = 1024, trace_dir=None, clock_ghz: float = 2.4):
     """Matrix-core busy fraction of the profiled product from one counter run
     of SQ_VALU_MFMA_BUSY_CYCLES (summed over all SIMDs, in cycles) and
-    GRBM_GUI_ACTIVE (GPU busy cycles, summed over the 8 XCDs): busy /
-    (simds x GRBM_GUI_ACTIVE / 8), over the product's dispatches after the
-    reference copy."""
+    GRBM_GUI_ACTIVE (GPU busy cycles, summed over the 8 XCDs), over the
+    product's dispatches after the reference copy: busy / (simds x
+    GRBM_GUI_ACTIVE / 8) -- which counts the gaps between dispatches under
+    the profiler as busy time -- and, given a kernel-trace run of the same
+    kernel, busy / (simds x kernel duration x clock), over the kernel's own
+    duration at the 2.4 GHz peak clock."""
     path = sorted(glob.glob(os.path.join(pmc_dir, "**", "*counter_collection.csv"), recursive=True))
     if not path:
         raise SystemExit(f"no counter_collection.csv under {pmc_dir}")
@@ -161,6 +180,12 @@ def mfma_busy(pmc_dir, meta, simds: int = 1024):
     out = {k: round(x / reps, 1) for k, x in sorted(tot.items())}
     out["mfma_busy_fraction"] = round(busy / (simds * gui / 8.0), 4) if gui > 0 else None
     out["kernels"] = sorted({_short(v["name"]) for v in mine})
+    if trace_dir:
+        dur, names = kernel_duration_us(trace_dir)
+        if dur:
+            out["kernel_duration_us"] = round(dur, 2)
+            out["trace_kernels"] = names
+            out["mfma_busy_of_kernel_duration"] = round(busy / (simds * dur * 1e-6 * clock_ghz * 1e9), 4)
     return out
 
 
@@ -173,6 +198,9 @@ def main(argv=None) -> int:
                     help="counter runs of bench.py --profile-op: record HBM bytes per launch")
     ap.add_argument("--meta", help="file holding the metadata line bench.py --profile-op printed")
     ap.add_argument("--db", help="traffic database (JSON) to add the entry to")
+    ap.add_argument("--trace", metavar="KT_DIR",
+                    help="with --mfma: a kernel-trace run of the same product (--profile-op), whose mean kernel "
+                         "duration normalises the busy cycles")
     ap.add_argument("--mfma", metavar="PMC_DIR",
                     help="counter run of bench.py --profile-op with SQ_VALU_MFMA_BUSY_CYCLES and GRBM_GUI_ACTIVE: "
                          "matrix-core busy fraction of the product")
@@ -181,7 +209,7 @@ def main(argv=None) -> int:
         import json
         with open(a.meta) as f:
             meta = next(json.loads(l) for l in f if l.startswith("{"))
-        print(json.dumps(mfma_busy(a.mfma, meta), indent=1))
+        print(json.dumps(mfma_busy(a.mfma, meta, trace_dir=a.trace), indent=1))
         return 0
     if a.traffic:
         import json
