@@ -611,7 +611,8 @@ constexpr int lds_f16(int mt, int nt, int st) { return st * (mt + nt) * 128; }
     {"gemm_f16_" #MT "x" #NT "x64_w" #WM "x" #WN "_m" #MF "_s" #ST "_p" #PF "_v" #VEC, FAM_GEMM_F16, MF,        \
      (MF == 32 ? 16 : 32), MT, NT, 64, WM, WN, ST, PF, 1, (VEC ? 16 : 2), 0, 0, WM * WN * 64,                 \
      lds_f16(MT, NT, ST), est_regs_f16(MT, NT, WM, WN, MF, PF),                                                \
-     (const void *)&gemm_f16_kernel<MT, NT, WM, WN, MF, ST, PF, VEC>, &launch_gemm_f16<MT, NT, WM, WN, MF, ST, PF, VEC>}
+     (const void *)&gemm_f16_kernel<MT, NT, WM, WN, MF, ST, PF, VEC>, &launch_gemm_f16<MT, NT, WM, WN, MF, ST, PF, VEC>, \
+     0, LAYOUT_SWIZZLE, 0}
 
 // The compiled fp16 configurations (K slab fixed at 64: 128-byte rows).
 #define NNJIT_F16_LIST(X) \
@@ -658,7 +659,7 @@ constexpr int lds_f16t(int mt, int nt, int kt, int st) { return st * (mt + nt) *
     {"gemm_f16t_" #MT "x" #NT "x" #KT "_w" #WM "x" #WN "_m" #MF "_s" #ST, FAM_GEMM_F16, MF, (MF == 32 ? 16 : 32), \
      MT, NT, KT, WM, WN, ST, ST - 1, 1, 16, 0, 0, WM * WN * 64, lds_f16t(MT, NT, KT, ST),                     \
      est_regs_f16t(MT, NT, KT, WM, WN, MF), (const void *)&gemm_f16t_kernel<MT, NT, KT, WM, WN, MF, ST>,      \
-     &launch_gemm_f16t<MT, NT, KT, WM, WN, MF, ST>, 1}
+     &launch_gemm_f16t<MT, NT, KT, WM, WN, MF, ST>, 1, LAYOUT_SWIZZLE, 0}
 
 // The compiled direct-copy configurations (16-byte aligned operands, Nt >= 128).
 #define NNJIT_F16T_LIST(X) \

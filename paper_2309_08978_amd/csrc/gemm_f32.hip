@@ -45,7 +45,13 @@ template <> struct Mfma32<16> {
 // through LDS (deterministic).  KS multiplies the waves and the loads in
 // flight per CU without a second kernel, which is what small-M products
 // (few tiles, long K) need.
-template <int MT, int NT, int KT, int WM, int WN, int MF, int ST, int PF, int KS, bool VEC>
+//
+// LAY (A slab layout) and ROLL (K steps of a slab as a loop) exist so that
+// the offline primitive benchmark can compare settings one at a time; the
+// default layout is the swizzle for 16-deep slabs and padding otherwise,
+// and the default is fully unrolled.
+template <int MT, int NT, int KT, int WM, int WN, int MF, int ST, int PF, int KS, bool VEC,
+          int LAY = (KT == 16 ? LAYOUT_SWIZZLE : LAYOUT_PAD), bool ROLL = false>
 __global__ void __launch_bounds__(KS * WM * WN * 64)
 gemm_f32_kernel(GemmParams p)
 {
@@ -60,8 +66,9 @@ gemm_f32_kernel(GemmParams p)
     // index XOR-swizzled by (row >> 2) & 3, deeper slabs are padded by 4
     // floats; both keep the 128-bit stores (8 lanes = 128 contiguous bytes)
     // and the fragment reads (16 consecutive rows) free of bank conflicts.
-    constexpr bool SWZ = (KT == 16);
-    constexpr int SA = SWZ ? KT : KT + 4;
+    constexpr bool SWZ = (LAY == LAYOUT_SWIZZLE);
+    constexpr int SA = (LAY == LAYOUT_PAD) ? KT + 4 : KT;
+    static_assert(!SWZ || KT % 16 == 0, "the swizzle permutes groups of four 16-byte chunks");
     constexpr int SB = NT + 4;           // B slab: [Kt][Nt + 4] floats
     constexpr int A4 = MT * KT / 4;      // 16-byte chunks of one A slab
     constexpr int B4 = KT * NT / 4;
@@ -191,8 +198,7 @@ gemm_f32_kernel(GemmParams p)
     auto compute = [&](int buf) {
         const float *as = As(buf);
         const float *bs = Bs(buf) + (lg * KL) * SB + wn * WTN + li;
-#pragma unroll
-        for (int q = 0; q < KL / 4; ++q) {
+        auto step = [&](int q) {
             f32x4 a[FM];
 #pragma unroll
             for (int i = 0; i < FM; ++i)
@@ -207,6 +213,13 @@ gemm_f32_kernel(GemmParams p)
 #pragma unroll
                     for (int j = 0; j < FN; ++j) acc[i][j] = I::mma(a[i][e], b[j], acc[i][j]);
             }
+        };
+        if constexpr (ROLL) {
+#pragma unroll 1
+            for (int q = 0; q < KL / 4; ++q) step(q);
+        } else {
+#pragma unroll
+            for (int q = 0; q < KL / 4; ++q) step(q);
         }
     };
 
@@ -292,11 +305,12 @@ gemm_f32_kernel(GemmParams p)
             }
 }
 
-template <int MT, int NT, int KT, int WM, int WN, int MF, int ST, int PF, int KS, bool VEC>
+template <int MT, int NT, int KT, int WM, int WN, int MF, int ST, int PF, int KS, bool VEC,
+          int LAY = (KT == 16 ? LAYOUT_SWIZZLE : LAYOUT_PAD), bool ROLL = false>
 static hipError_t launch_gemm_f32(const void *params, dim3 grid, hipStream_t stream)
 {
-    hipLaunchKernelGGL((gemm_f32_kernel<MT, NT, KT, WM, WN, MF, ST, PF, KS, VEC>), grid, dim3(KS * WM * WN * 64), 0,
-                       stream, *(const GemmParams *)params);
+    hipLaunchKernelGGL((gemm_f32_kernel<MT, NT, KT, WM, WN, MF, ST, PF, KS, VEC, LAY, ROLL>), grid,
+                       dim3(KS * WM * WN * 64), 0, stream, *(const GemmParams *)params);
     return hipGetLastError();
 }
 
@@ -887,18 +901,43 @@ static hipError_t launch_gemm_f32t(const void *params, dim3 grid, hipStream_t st
     return hipGetLastError();
 }
 
-constexpr int lds_f32(int mt, int nt, int kt, int st, int ks) {
-    return (ks * st * (mt * (kt == 16 ? kt : kt + 4) + kt * (nt + 4)) > (ks - 1) * mt * nt
-                ? ks * st * (mt * (kt == 16 ? kt : kt + 4) + kt * (nt + 4))
+constexpr int lds_f32(int mt, int nt, int kt, int st, int ks, int lay) {
+    return (ks * st * (mt * (lay == LAYOUT_PAD ? kt + 4 : kt) + kt * (nt + 4)) > (ks - 1) * mt * nt
+                ? ks * st * (mt * (lay == LAYOUT_PAD ? kt + 4 : kt) + kt * (nt + 4))
                 : (ks - 1) * mt * nt) * 4;
 }
+constexpr int default_layout_f32(int kt) { return kt == 16 ? LAYOUT_SWIZZLE : LAYOUT_PAD; }
 
 #define NNJIT_F32_VARIANT(MT, NT, KT, WM, WN, MF, ST, PF, KS, VEC)                                        \
     {"gemm_f32_" #MT "x" #NT "x" #KT "_w" #WM "x" #WN "_m" #MF "_s" #ST "_p" #PF "_k" #KS "_v" #VEC,             \
      FAM_GEMM_F32, MF, (MF == 32 ? 2 : 4), MT, NT, KT, WM, WN, ST, PF, KS, (VEC ? 16 : 4), 0, 0,               \
-     KS * WM * WN * 64, lds_f32(MT, NT, KT, ST, KS), est_regs_f32(MT, NT, KT, WM, WN, MF, PF),                 \
-     (const void *)&gemm_f32_kernel<MT, NT, KT, WM, WN, MF, ST, PF, KS, VEC>,                                 \
-     &launch_gemm_f32<MT, NT, KT, WM, WN, MF, ST, PF, KS, VEC>}
+     KS * WM * WN * 64, lds_f32(MT, NT, KT, ST, KS, default_layout_f32(KT)),                                  \
+     est_regs_f32(MT, NT, KT, WM, WN, MF, PF), (const void *)&gemm_f32_kernel<MT, NT, KT, WM, WN, MF, ST, PF, KS, VEC>, \
+     &launch_gemm_f32<MT, NT, KT, WM, WN, MF, ST, PF, KS, VEC>, 0, default_layout_f32(KT), 0}
+
+// Primitive-probe variants: a configuration of the list below with one
+// primitive changed -- the A slab layout (LAY) or a rolled K-step loop
+// (ROLL) -- for the offline one-variable-at-a-time benchmark.
+#define NNJIT_F32P_VARIANT(MT, NT, KT, WM, WN, MF, ST, PF, KS, LAY, ROLL, TAG)                               \
+    {"gemm_f32_" #MT "x" #NT "x" #KT "_w" #WM "x" #WN "_m" #MF "_s" #ST "_p" #PF "_k" #KS "_vtrue_" TAG,         \
+     FAM_GEMM_F32, MF, (MF == 32 ? 2 : 4), MT, NT, KT, WM, WN, ST, PF, KS, 16, 0, 0,                           \
+     KS * WM * WN * 64, lds_f32(MT, NT, KT, ST, KS, LAY), est_regs_f32(MT, NT, KT, WM, WN, MF, PF),            \
+     (const void *)&gemm_f32_kernel<MT, NT, KT, WM, WN, MF, ST, PF, KS, true, LAY, ROLL>,                     \
+     &launch_gemm_f32<MT, NT, KT, WM, WN, MF, ST, PF, KS, true, LAY, ROLL>, 0, LAY, ROLL}
+
+#define NNJIT_F32P_LIST(X) \
+    X(128, 128, 16, 2, 2, 32, 2, 2, 1, LAYOUT_PAD, false, "lpad") \
+    X(128, 128, 16, 2, 2, 32, 2, 2, 1, LAYOUT_PLAIN, false, "lplain") \
+    X(128, 128, 16, 2, 2, 32, 2, 2, 1, LAYOUT_SWIZZLE, true, "rolled") \
+    X(64, 64, 16, 2, 2, 32, 2, 2, 1, LAYOUT_PAD, false, "lpad") \
+    X(64, 64, 16, 2, 2, 32, 2, 2, 1, LAYOUT_PLAIN, false, "lplain") \
+    X(64, 64, 32, 2, 2, 32, 2, 2, 1, LAYOUT_SWIZZLE, false, "lswz") \
+    X(64, 64, 32, 2, 2, 32, 2, 2, 1, LAYOUT_PLAIN, false, "lplain") \
+    X(64, 64, 32, 2, 2, 32, 2, 2, 1, LAYOUT_PAD, true, "rolled") \
+    X(64, 64, 64, 2, 2, 32, 2, 2, 1, LAYOUT_SWIZZLE, false, "lswz") \
+    X(64, 64, 64, 2, 2, 32, 2, 2, 1, LAYOUT_PAD, true, "rolled") \
+    X(128, 128, 32, 2, 2, 32, 2, 2, 1, LAYOUT_SWIZZLE, false, "lswz") \
+    X(128, 128, 32, 2, 2, 32, 2, 2, 1, LAYOUT_PLAIN, false, "lplain")
 
 // Register estimate of the Table 1 formula Reg_thread = x0*r0 + r0*y0 + x0*y0
 // for one lane: the accumulator tile (x0*y0 over 64 lanes), the A and B
@@ -922,7 +961,7 @@ constexpr int lds_f32w(int mt, int nt, int ks, int st) {
 #define NNJIT_F32W_VARIANT(MT, NT, KS, ST)                                                                   \
     {"gemm_f32w_" #MT "x" #NT "x16_k" #KS "_s" #ST, FAM_GEMM_F32, 32, 2, MT, NT, 16, 1, 1, ST, ST - 1, KS, 16,  \
      0, 0, KS * 64, lds_f32w(MT, NT, KS, ST), est_regs_f32w(MT, NT), (const void *)&gemm_f32w_kernel<MT, NT, KS, ST>, \
-     &launch_gemm_f32w<MT, NT, KS, ST>, 1}
+     &launch_gemm_f32w<MT, NT, KS, ST>, 1, LAYOUT_SWIZZLE, 0}
 
 #define NNJIT_F32W_LIST(X) \
     X(64, 32, 4, 4) \
@@ -1031,7 +1070,7 @@ constexpr int lds_f32t(int mt, int nt, int st) { return st * (mt * 64 + 64 * nt)
 #define NNJIT_F32T_VARIANT(MT, NT, WM, WN, ST)                                                                \
     {"gemm_f32t_" #MT "x" #NT "x16_w" #WM "x" #WN "_s" #ST, FAM_GEMM_F32, 32, 2, MT, NT, 16, WM, WN, ST, ST - 1, \
      1, 16, 0, 0, WM * WN * 64, lds_f32t(MT, NT, ST), est_regs_f32t(MT, NT, WM, WN),                          \
-     (const void *)&gemm_f32t_kernel<MT, NT, WM, WN, ST>, &launch_gemm_f32t<MT, NT, WM, WN, ST>, 1}
+     (const void *)&gemm_f32t_kernel<MT, NT, WM, WN, ST>, &launch_gemm_f32t<MT, NT, WM, WN, ST>, 1, LAYOUT_SWIZZLE, 0}
 
 // The compiled shared-slab direct-copy configurations (16-byte aligned
 // operands, Nt >= 64).
@@ -1054,13 +1093,17 @@ NNJIT_F32T_LIST(NNJIT_F32T_INST)
 #define NNJIT_F32_INST(MT, NT, KT, WM, WN, MF, ST, PF, KS, VEC) \
     template __global__ void gemm_f32_kernel<MT, NT, KT, WM, WN, MF, ST, PF, KS, VEC>(GemmParams);
 NNJIT_F32_LIST(NNJIT_F32_INST)
+#define NNJIT_F32P_INST(MT, NT, KT, WM, WN, MF, ST, PF, KS, LAY, ROLL, TAG) \
+    template __global__ void gemm_f32_kernel<MT, NT, KT, WM, WN, MF, ST, PF, KS, true, LAY, ROLL>(GemmParams);
+NNJIT_F32P_LIST(NNJIT_F32P_INST)
 
 #if !defined(__HIP_DEVICE_COMPILE__)
 #define NNJIT_F32_ENTRY(...) NNJIT_F32_VARIANT(__VA_ARGS__),
 #define NNJIT_F32W_ENTRY(...) NNJIT_F32W_VARIANT(__VA_ARGS__),
 #define NNJIT_F32T_ENTRY(...) NNJIT_F32T_VARIANT(__VA_ARGS__),
+#define NNJIT_F32P_ENTRY(...) NNJIT_F32P_VARIANT(__VA_ARGS__),
 const Variant kGemmF32Variants[] = {NNJIT_F32_LIST(NNJIT_F32_ENTRY) NNJIT_F32W_LIST(NNJIT_F32W_ENTRY)
-                                        NNJIT_F32T_LIST(NNJIT_F32T_ENTRY)};
+                                        NNJIT_F32T_LIST(NNJIT_F32T_ENTRY) NNJIT_F32P_LIST(NNJIT_F32P_ENTRY)};
 const int kNumGemmF32Variants = sizeof(kGemmF32Variants) / sizeof(kGemmF32Variants[0]);
 #endif
 

@@ -166,7 +166,7 @@ constexpr int lds_gemv(int nthr, int l, int v) { return nthr > 64 ? (nthr / 64) 
 #define NNJIT_GEMV_VARIANT(T, FAMV, V, L, NTHR, U, VEC)                                                 \
     {"gemv_" #T "_L" #L "_t" #NTHR "_u" #U "_v" #VEC, FAMV, 0, 0, 1, L * V, NTHR / L, NTHR / 64, 1, 0, 0, 1, \
      (VEC ? 16 : (int)sizeof(T)), L, U, NTHR, lds_gemv(NTHR, L, V), est_regs_gemv(V, U),                \
-     (const void *)&gemv_kernel<T, L, NTHR, U, VEC>, &launch_gemv<T, L, NTHR, U, VEC>}
+     (const void *)&gemv_kernel<T, L, NTHR, U, VEC>, &launch_gemv<T, L, NTHR, U, VEC>, 0, -1, 0}
 
 
 // The compiled GEMV configurations of both dtypes.

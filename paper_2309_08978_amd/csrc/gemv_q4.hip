@@ -279,10 +279,10 @@ NNJIT_Q4_WORDS_LIST(NNJIT_Q4_WORDS_INST)
 #define NNJIT_Q4_ENTRY(RW, NTHR, KS, UB)                                                                            \
     {"gemv_q4_r" #RW "_t" #NTHR "_k" #KS "_u" #UB, FAM_GEMV_Q4, 0, 0, RW, RW * (NTHR / 64) / KS, kQ4Block,       \
      NTHR / 64, 1, 0, 0, KS, 16, 64, UB, NTHR, lds_q4(NTHR, RW, KS), est_regs_q4(RW, UB),                       \
-     (const void *)&gemv_q4_kernel<RW, NTHR, KS, UB>, &launch_gemv_q4<RW, NTHR, KS, UB>, 0},
+     (const void *)&gemv_q4_kernel<RW, NTHR, KS, UB>, &launch_gemv_q4<RW, NTHR, KS, UB>, 0, -1, 0},
 #define NNJIT_Q4_WORDS_ENTRY(RW, NTHR)                                                                               \
     {"gemv_q4_words_r" #RW "_t" #NTHR, FAM_GEMV_Q4, 0, 0, RW, RW * (NTHR / 64), 512, NTHR / 64, 1, 0, 0, 1, 4, 64, 1, \
-     NTHR, 0, 3 * RW + 40, (const void *)&gemv_q4_words_kernel<RW, NTHR>, &launch_gemv_q4_words<RW, NTHR>, 0},
+     NTHR, 0, 3 * RW + 40, (const void *)&gemv_q4_words_kernel<RW, NTHR>, &launch_gemv_q4_words<RW, NTHR>, 0, -1, 0},
 const Variant kGemvQ4Variants[] = {NNJIT_Q4_LIST(NNJIT_Q4_ENTRY) NNJIT_Q4_WORDS_LIST(NNJIT_Q4_WORDS_ENTRY)};
 const int kNumGemvQ4Variants = sizeof(kGemvQ4Variants) / sizeof(kGemvQ4Variants[0]);
 #endif

@@ -75,7 +75,13 @@ struct Variant {
     const void *kernel;   // device function (attribute queries)
     LaunchFn launch;
     int direct_copy;      // 1: slabs go global -> LDS by direct copies (staging in LDS, not registers)
+    int lds_layout;       // GEMM A slab in LDS: LAYOUT_SWIZZLE, LAYOUT_PAD or LAYOUT_PLAIN (GEMV: -1)
+    int rolled;           // GEMM: 1 if the K steps of a slab run as a loop instead of fully unrolled
 };
+
+// LDS layouts of a GEMM's A slab: 16-byte chunk index XOR-swizzled by row,
+// rows padded by 16 bytes, or plain rows.
+enum LdsLayout { LAYOUT_SWIZZLE = 0, LAYOUT_PAD = 1, LAYOUT_PLAIN = 2 };
 
 // Variant tables, one per family (defined in the kernel sources).
 extern const Variant kGemmF32Variants[];

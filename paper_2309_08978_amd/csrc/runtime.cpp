@@ -1114,10 +1114,11 @@ int nnjit_config_info(int cfg, char *buf, int64_t len) {
     else if (!family_is_gemv(v.family))
         n = snprintf(tmp, sizeof tmp,
                      "id=%d family=%s name=%s mfma=%dx%dx%d Mt=%d Nt=%d Kt=%d waves=%dx%d stages=%d prefetch=%d kslices=%d "
-                     "vec=%d split=%d threads=%d lds=%d est_regs=%d direct=%d",
+                     "vec=%d split=%d threads=%d lds=%d est_regs=%d direct=%d layout=%s unroll=%s",
                      c.id, family_name(v.family), v.name, v.mfma_m, v.mfma_m, v.mfma_k, v.mt, v.nt, v.kt, v.wm, v.wn,
                      v.stages, v.prefetch, v.kslices, v.vec_bytes, c.split, v.threads, v.lds_bytes, v.est_regs,
-                     v.direct_copy);
+                     v.direct_copy, v.lds_layout == LAYOUT_PAD ? "pad" : v.lds_layout == LAYOUT_PLAIN ? "plain" : "swz",
+                     v.rolled ? "rolled" : "full");
     else
         n = snprintf(tmp, sizeof tmp,
                      "id=%d family=%s name=%s cols=%d rows_per_pass=%d lanes_per_seg=%d unroll=%d vec=%d split=%d "

@@ -157,6 +157,56 @@ Geometry geometry_of(const Config &c, int64_t batch, int64_t M, int64_t N, int64
     return g;
 }
 
+const std::vector<ConsistentSetting> &consistent_settings() {
+    static const std::vector<ConsistentSetting> t = {
+#include "consistent.inc"
+    };
+    return t;
+}
+
+int primitive_value(const Variant &v, int primitive) {
+    switch (primitive) {
+    case PRIM_DIRECT: return v.direct_copy;
+    case PRIM_LAYOUT: return v.lds_layout;
+    case PRIM_UNROLL: return v.rolled;
+    case PRIM_STAGES: return v.stages;
+    case PRIM_PREFETCH: return v.prefetch;
+    case PRIM_KT: return v.kt;
+    case PRIM_MFMA: return v.mfma_m;
+    case PRIM_VEC: return v.vec_bytes;
+    default: return -1;
+    }
+}
+
+// Do u and v differ in nothing but `primitive` (for the staging primitive:
+// the same tile hierarchy, instruction shape and load width)?  The groups
+// the offline microbenchmark compares.
+static bool same_group(const Variant &u, const Variant &v, int primitive) {
+    if (u.family != v.family || u.mfma_m != v.mfma_m || u.mfma_k != v.mfma_k || u.mt != v.mt || u.nt != v.nt ||
+        u.kt != v.kt || u.wm != v.wm || u.wn != v.wn || u.vec_bytes != v.vec_bytes)
+        return false;
+    if (primitive == PRIM_DIRECT) return true;
+    for (int q : {PRIM_DIRECT, PRIM_LAYOUT, PRIM_UNROLL, PRIM_STAGES, PRIM_PREFETCH, PRIM_KT, PRIM_MFMA, PRIM_VEC})
+        if (q != primitive && primitive_value(u, q) != primitive_value(v, q)) return false;
+    return u.kslices == v.kslices;
+}
+
+// A variant is excluded when a fixed (consistent) setting differs from its
+// own and the compiled set holds its twin with the fixed setting: the
+// primitive is fixed where the choice exists, not for variants the
+// benchmark never compared.
+bool follows_consistent(const Variant &v) {
+    for (const ConsistentSetting &c : consistent_settings()) {
+        if (c.family != v.family) continue;
+        if (!(v.direct_copy ? c.direct_copy : c.reg_staged)) continue;
+        if (primitive_value(v, c.primitive) == c.value) continue;
+        for (const Config &u : configs())
+            if (u.split == 1 && primitive_value(*u.v, c.primitive) == c.value && same_group(*u.v, v, c.primitive))
+                return false;
+    }
+    return true;
+}
+
 namespace {
 struct Cand {
     int id;
@@ -188,11 +238,13 @@ LiteResult lite_space(const Shape &s, const nnjit_device_limits &d, const std::v
     }
 
     std::vector<Cand> cands, unfit;  // unfit: pass the resource heuristics, fail the shape fit (split 1 only)
+    std::vector<Cand> off_cands, off_unfit;  // the same, with a setting the consistent-primitive table excludes
     for (const Config &c : configs()) {
         const Variant &v = *c.v;
         if (v.family != fam) continue;
         ++out.n_enumerated;
         if ((v.vec_bytes == 16) != vec_ok) continue;  // vector loads only where the shape allows them
+        const bool consistent = follows_consistent(v);
         const int gi = variant_index(&v);
         if (spills && gi < (int)spills->size() && (*spills)[gi]) continue;
         const int mregs = (measured_regs && gi < (int)measured_regs->size()) ? (*measured_regs)[gi] : -1;
@@ -262,8 +314,15 @@ LiteResult lite_space(const Shape &s, const nnjit_device_limits &d, const std::v
                 if (wg_here * v.threads * (int64_t)v.unroll * 16 < 8192 && c.split != smax) continue;
             }
         }
-        if (fit) cands.push_back(cd);
-        else if (c.split == 1) unfit.push_back(cd);
+        if (fit) (consistent ? cands : off_cands).push_back(cd);
+        else if (c.split == 1) (consistent ? unfit : off_unfit).push_back(cd);
+    }
+    // settings fixed offline (consistent primitives) prune the rest, unless
+    // nothing would be left (e.g. element-load shapes when 16-byte loads are
+    // the fixed setting)
+    if (cands.empty() && unfit.empty()) {
+        cands.swap(off_cands);
+        unfit.swap(off_unfit);
     }
     // the shape fit never empties the space: tiny shapes fall back to the
     // unsplit configurations that passed the resource heuristics

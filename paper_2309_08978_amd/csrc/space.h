@@ -44,6 +44,23 @@ constexpr double kRelaxation = 0.9;  // share of the register file the estimate 
 constexpr int kMaxTimed = 96;        // size cap of a lite space (candidates timed per shape at most)
 constexpr int kMinSurvivors = 8;     // heuristic 7 is relaxed below this many
 
+// Primitives whose setting the offline microbenchmark may fix for a whole
+// family (the paper's consistent primitives, Sec. 5.1).
+enum Primitive { PRIM_DIRECT, PRIM_LAYOUT, PRIM_UNROLL, PRIM_STAGES, PRIM_PREFETCH, PRIM_KT, PRIM_MFMA, PRIM_VEC };
+struct ConsistentSetting {
+    int family;
+    int primitive;
+    int value;
+    int reg_staged;    // applies to register-staged variants
+    int direct_copy;   // applies to direct-copy variants
+};
+// The table generated from the microbenchmark's stored measurement.
+const std::vector<ConsistentSetting> &consistent_settings();
+// The setting of a primitive in a variant (the integer the table stores).
+int primitive_value(const Variant &v, int primitive);
+// false if the variant has another setting of a primitive the table fixes.
+bool follows_consistent(const Variant &v);
+
 struct Shape {
     int kind;
     int dtype;

@@ -249,20 +249,56 @@ def test_misaligned_shapes_get_element_load_configs(lib):
 
 
 def test_microbench_groups_vary_one_primitive(lib):
-    """The offline microbenchmark compares only configurations that differ in
-    exactly one primitive (besides derived fields)."""
-    from paper_2309_08978_amd.microbench import groups_for, PRIMITIVES, DERIVED
+    """The offline microbenchmark compares configurations that differ in
+    exactly one primitive (besides derived fields); staging groups compare
+    the two staging kinds on the same tile hierarchy, instruction shape and
+    load width.  Every primitive, the new ones included (staging, LDS layout,
+    unroll), has groups in the fp32 family."""
+    from paper_2309_08978_amd.microbench import groups_for, PRIMITIVES, DERIVED, DIRECT_KEY
     cfgs = [c for c in nj.configs() if c["family"] == "gemm_f32"]
-    total = 0
+    per_prim = {}
     for prim in PRIMITIVES:
+        per_prim[prim] = 0
         for grp in groups_for(cfgs, prim):
-            total += 1
-            assert len({c[prim] for c in grp}) >= 2
-            for c in grp:
+            per_prim[prim] += 1
+            assert len(grp) >= 2
+            members = [c for cs in grp.values() for c in cs]
+            assert all(c[prim] == v for v, cs in grp.items() for c in cs)
+            for c in members:
                 assert c["split"] == 1
-                rest = {k: v for k, v in c.items() if k not in DERIVED and k != prim}
-                assert rest == {k: v for k, v in grp[0].items() if k not in DERIVED and k != prim}
-    assert total >= 10
+                if prim == "direct":
+                    assert tuple(c[k] for k in DIRECT_KEY) == tuple(members[0][k] for k in DIRECT_KEY)
+                else:
+                    rest = {k: v for k, v in c.items() if k not in DERIVED and k != prim}
+                    assert rest == {k: v for k, v in members[0].items() if k not in DERIVED and k != prim}
+    for prim in ("direct", "layout", "unroll", "prefetch", "Kt", "vec"):
+        assert per_prim[prim] >= 1, (prim, per_prim)
+
+
+def test_consistent_table_is_generated_from_the_stored_measurement(lib):
+    """csrc/consistent.inc is exactly what the microbenchmark's rule makes of
+    the committed measurement, and no lite space of a workload shape holds a
+    configuration with another setting of a primitive the table fixes."""
+    from paper_2309_08978_amd import microbench as mb
+    if os.path.exists(mb.MEASUREMENT):
+        runs = json.load(open(mb.MEASUREMENT))["runs"]
+        assert open(mb.TABLE).read() == mb.table_text(runs)
+        fixed = mb.consistent_settings(runs)
+    else:
+        fixed = []
+    cfgs = nj.configs()
+    dev = nj.mi355x_limits()
+    for name in workloads.WORKLOADS:
+        for op in workloads.workload(name):
+            if op.dtype not in ("f32", "f16") or op.M == 1:
+                continue
+            kind = nj.NNJIT_KIND_GEMM if op.batch == 1 else nj.NNJIT_KIND_BATCHED
+            ids, _, _, _ = nj.nnjit_lite_space(kind, 1 if op.dtype == "f16" else 0, op.batch, op.M, op.N, op.K, dev)
+            for i in ids:
+                assert not mb.excluded_by(cfgs[i], fixed, cfgs), (name, op.name, cfgs[i]["name"])
+    # the rule excludes something (when the table fixes anything)
+    if fixed:
+        assert any(mb.excluded_by(c, fixed, cfgs) for c in cfgs)
 
 
 @pytest.mark.parametrize("N,K,G", [(4096, 4096, 128), (12288, 4096, 128), (4096, 11008, 128), (32000, 4096, 128),
