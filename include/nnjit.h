@@ -133,9 +133,9 @@ int nnjit_batched_matmul(int64_t batch, int64_t M, int64_t N, int64_t K,
  * scratch array of 128 MiB that the library holds on each GPU for the life
  * of the process, and the call makes no allocating HIP call
  * (the first call on a device initialises it, which only takes that array's
- * address).  A configuration that needs more split-K scratch than 128 MiB
- * (S x batch x M x N x 4 bytes) is refused with NNJIT_ENOMEM before any
- * launch.  All calls on one GPU share the array: calls that overlap in time
+ * address).  A configuration that needs more partials than 128 MiB
+ * (split-K: S x batch x M x N x 4 bytes; stream-K: 2 x workgroups x Mt x Nt
+ * x 4 bytes) is refused with NNJIT_ENOMEM before any launch.  All calls on one GPU share the array: calls that overlap in time
  * on that GPU (on different streams, or replays of captured graphs that run
  * concurrently) race on it and must be ordered by the caller.  Nothing in
  * the scratch needs to start at zero: each call writes every partial it
@@ -149,18 +149,23 @@ int nnjit_batched_matmul_noalloc(int64_t batch, int64_t M, int64_t N, int64_t K,
 /* Just-in-time tuning of one shape (Sec. 3 JIT phase, Sec. 5.2 lite space;
  * the problem statement: one kernel per operator shape, Sec. 3):
  * builds the shape's lite space (enumerate the compiled configurations of
- * the kind and dtype, compute each one's Table 1 resource use on this
- * device, prune by the heuristics, order by workgroups per CU, most first),
+ * the kind and dtype, drop those with another setting of a primitive fixed
+ * offline, compute each one's Table 1 resource use on this device, prune by
+ * the heuristics, order by workgroups per CU, most first, at most 96),
  * times every survivor on device scratch of this exact shape (1 untimed
  * warm-up, 1 single timed launch, then 3 timed bursts of back-to-back
- * launches whose per-launch median is the candidate's cost; the burst length
- * (8, 2 or 1) is set once per shape from the first candidate's single launch;
- * a candidate whose single launch is more than 1.5x the fastest single launch
- * so far is dropped; at most 96 candidates and about 900 ms of evaluation;
- * an M = 1 (GEMV) shape is timed on weights streamed from HBM: the weight
- * operand rotates over scratch copies of >= 512 MiB together), keeps the fastest in the per-shape cache and
- * returns its configuration id (>= 0).  Synchronous; uses its own stream and
- * a library-owned scratch buffer.  Re-tuning a cached shape replaces the
+ * launches, each captured as a HIP graph of about 500 us of device work,
+ * whose per-launch median is the candidate's cost; a candidate whose single
+ * launch is more than 1.5x the fastest single launch so far is dropped; the
+ * candidates within 15% of the best are timed again, in turns, and the best
+ * of that run-off is kept; about 900 ms of evaluation at most; an M = 1
+ * (GEMV) shape is timed on weights streamed from HBM: the weight operand
+ * rotates over scratch copies of >= 512 MiB together), keeps the fastest in
+ * the per-shape cache and returns its configuration id (>= 0).  The scratch
+ * operands hold near-normal values scaled like activations (A) and weights
+ * (B).  Synchronous; the stream and the scratch it times on are created and
+ * allocated by the call and released before it returns; other threads'
+ * calls are not held up meanwhile.  Re-tuning a cached shape replaces the
  * incumbent only if the new winner is at least 3% faster.  Wall time and
  * counts: nnjit_last_tune_stats().  Negative return: error code. */
 int nnjit_tune(int64_t M, int64_t N, int64_t K, int dtype);
@@ -169,7 +174,10 @@ int nnjit_tune(int64_t M, int64_t N, int64_t K, int dtype);
  * strideB = K*N, strideC = M*N).  batch == 1 is nnjit_tune. */
 int nnjit_tune_batched(int64_t batch, int64_t M, int64_t N, int64_t K, int dtype);
 
-/* Run one forced configuration `cfg` (test and report helper): any kind's
+/* Run one forced configuration `cfg` -- one point of the kernel space, a
+ * setting of each primitive of Table 2 (tiling, staging, unroll, vectorize)
+ * plus a split-K factor (split 0 = stream-K, see nnjit_config_info) -- (test
+ * and report helper; the candidates the tuner measures, Sec. 5.2): any kind's
  * configuration may be forced as long as it belongs to this dtype; GEMV
  * configurations additionally need batch == 1 and M == 1; a vector-load
  * configuration needs the 16-byte alignment described above.  A mismatch,
@@ -216,11 +224,18 @@ int nnjit_tune_gemv_q4(int64_t N, int64_t K, int64_t group);
 int nnjit_gemv_q4_config(int cfg, int64_t N, int64_t K, int64_t group, const void *x, const void *Wq, int64_t ldq,
                          const void *scales, int64_t lds, void *y, void *stream);
 
-/* Number of configurations (ids are 0 .. n-1, fixed for a build). */
+/* Number of compiled configurations (ids are 0 .. n-1, fixed for a build):
+ * the offline-compiled set from which every shape's lite space is drawn
+ * (Sec. 5.1: consistent primitives fixed offline; Sec. 5.2: the per-shape
+ * lite space). */
 int nnjit_num_configs(void);
 
-/* Writes a one-line description of configuration `cfg` into buf (at most
- * len bytes including the terminating NUL), e.g.
+/* Writes a one-line description of configuration `cfg` -- its primitive
+ * settings (Table 2: tile extents, K slab, staging, LDS layout, unroll,
+ * vector width) and its Table 1 inputs -- into buf (at most len bytes
+ * including the terminating NUL); split=0 marks a stream-K configuration
+ * (the tiles' K slabs cut evenly over one workgroup per resident slot,
+ * shared tiles summed by a fix-up kernel in workgroup order), e.g.
  * "id=12 family=gemm_f32 name=... mfma=32x32x2 Mt=128 Nt=64 Kt=16 waves=2x2
  *  stages=2 prefetch=2 vec=16 split=4 threads=256 lds=...".  Returns the full length of the
  * description, or NNJIT_EINVAL. */
@@ -340,7 +355,10 @@ int nnjit_set_online(int enable);
 int nnjit_online_status(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K, int *measured,
                         int *total, int *registered);
 
-/* Forget every tuned shape and release the tuner's scratch.  Returns NNJIT_OK. */
+/* Forget every tuned shape (the per-shape cache of Sec. 5.3), release the
+ * outgrown split-K buffers (after a device synchronisation; graphs captured
+ * before must be captured again) and read the environment overrides again.
+ * Returns NNJIT_OK. */
 int nnjit_cache_clear(void);
 
 /* Persistent kernel database (the paper's kernel database keyed by kernel

@@ -643,7 +643,7 @@ static hipError_t launch_gemm_f32w(const void *params, dim3 grid, hipStream_t st
 // sit on opposite halves of the 64 banks.  A copy writes 1 KiB contiguously
 // at a wave-uniform LDS base (lane l at base + 16 l), so both swizzles are
 // made by choosing which global piece each lane fetches.
-template <int MT, int NT, int WM, int WN, int ST>
+template <int MT, int NT, int WM, int WN, int ST, bool SK = false>
 __global__ void __launch_bounds__(WM * WN * 64)
 gemm_f32t_kernel(GemmParams p)
 {
@@ -667,33 +667,64 @@ gemm_f32t_kernel(GemmParams p)
     __shared__ __attribute__((aligned(1024))) char smem[ST * STAGE];
     typedef __attribute__((address_space(3))) char lds_char;
 
-    const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
-    const int wm = wave / WN, wn = wave % WN;
-    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
-    const int li = lane & 31, lg = lane >> 5;
-
     const int tiles = p.tiles_m * p.tiles_n;
     const int gx = gridDim.x;
     const int logical = xcd_remap(blockIdx.x + gx * blockIdx.z, gx * gridDim.z);
-    const int z = logical / gx;
-    const int rest = logical - z * gx;
-    const int s = rest / tiles;
-    const int tile = rest - s * tiles;
-    int tm, tn;
-    tile_of(tile, p.tiles_m, p.tiles_n, p.group_m, tm, tn);
-    const int m0 = tm * MT, n0 = tn * NT;
-    const int kbeg = s * p.kchunk;
-    const int kend = min(p.K, kbeg + p.kchunk);
-    const int nk = kend > kbeg ? (kend - kbeg + KT - 1) / KT : 0;
-
-    const float *A = (const float *)p.A + (long long)z * p.sA;
-    const float *B = (const float *)p.B + (long long)z * p.sB;
-    float *C = p.C + (long long)z * p.sC;
     const int M = p.M, N = p.N;
     const long long lda = p.lda, ldb = p.ldb;
     const float *zero = (const float *)p.zero;
     auto stage_base = [&](int u) -> lds_char * { return (lds_char *)smem + u * STAGE; };
+
+    // The workgroup's pieces of work: one (tile, split) in the tiled mode;
+    // consecutive (tile, K-slab range) segments of its share of units in the
+    // stream-K mode (at most one tile is begun and one ended mid-K).
+    long long su = 0, su_end = 1;
+    if constexpr (SK) {
+        su = (long long)logical * p.units / p.sk_wgs;
+        su_end = (long long)(logical + 1) * p.units / p.sk_wgs;
+    }
+    for (bool first = true; su < su_end; first = false) {
+    int z, s, tile, kbeg, kend;
+    bool partial = false;
+    if constexpr (SK) {
+        z = 0;
+        s = 0;
+        tile = (int)(su / p.nslab);
+        const int ks = (int)(su - (long long)tile * p.nslab);
+        const int ke = (int)min((long long)p.nslab, ks + (su_end - su));
+        kbeg = ks * KT;
+        kend = min(p.K, ke * KT);
+        partial = ks > 0 || ke < p.nslab;
+        su += ke - ks;
+    } else {
+        z = logical / gx;
+        const int rest = logical - z * gx;
+        s = rest / tiles;
+        tile = rest - s * tiles;
+        kbeg = s * p.kchunk;
+        kend = min(p.K, kbeg + p.kchunk);
+        su = su_end;
+    }
+    int tm, tn;
+    tile_of(tile, p.tiles_m, p.tiles_n, p.group_m, tm, tn);
+    const int m0 = tm * MT, n0 = tn * NT;
+    const int nk = kend > kbeg ? (kend - kbeg + KT - 1) / KT : 0;
+    const float *A = (const float *)p.A + (long long)z * p.sA;
+    const float *B = (const float *)p.B + (long long)z * p.sB;
+    float *C = p.C + (long long)z * p.sC;
+    // the LDS stages are reused: every wave must be done reading the previous
+    // segment's slabs before this one's copies land
+    if (SK && !first) lds_barrier();
+    // The lane's indices are taken afresh in every segment through an opaque
+    // copy of the thread id: the lane-dependent addresses derived from them
+    // are then computed per segment instead of being held in registers
+    // across the segment loop.
+    int tid = threadIdx.x;
+    if constexpr (SK) asm volatile("v_mov_b32 %0, %0" : "+v"(tid));
+    const int lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / WN, wn = wave % WN;
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+    const int li = lane & 31, lg = lane >> 5;
 
     // per-lane sources of this wave's copies for the split's first slab; copy
     // j of the wave fills 1 KiB chunk c = wave + j NW of the A or B slab
@@ -873,31 +904,50 @@ gemm_f32t_kernel(GemmParams p)
             if (it < nk) compute(u);
         }
     }
-    wait_vmcnt<0>();   // no copy may still target LDS when the workgroup ends
+    wait_vmcnt<0>();   // no copy may still target LDS when the workgroup (or segment) ends
 
     const int rbase = m0 + wm * WTM, cbase = n0 + wn * WTN + li;
-    float *out = C;
-    long long ldo = p.ldc;
-    if (p.S > 1) {
-        out = p.ws + ((long long)s * p.batch + z) * (long long)M * N;
-        ldo = N;
+    if (SK && partial) {
+        // a piece of a tile several workgroups share: the whole Mt x Nt
+        // partial tile to this workgroup's slot (first piece 2w, last 2w + 1)
+        float *slot = p.ws + (long long)(2 * logical + (first ? 0 : 1)) * (MT * NT);
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int r = 0; r < I::NR; ++r) {
+                    const int row = wm * WTM + 32 * i + I::row_of(r, lg), col = wn * WTN + li + 32 * j;
+                    slot[row * NT + col] = acc[i][j][r];
+                }
+    } else {
+        float *out = C;
+        long long ldo = p.ldc;
+        if (p.S > 1) {
+            out = p.ws + ((long long)s * p.batch + z) * (long long)M * N;
+            ldo = N;
+        }
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int r = 0; r < I::NR; ++r) {
+                    const int row = rbase + 32 * i + I::row_of(r, lg), col = cbase + 32 * j;
+                    if (row < M && col < N) out[(long long)row * ldo + col] = acc[i][j][r];
+                }
     }
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-#pragma unroll
-            for (int r = 0; r < I::NR; ++r) {
-                const int row = rbase + 32 * i + I::row_of(r, lg), col = cbase + 32 * j;
-                if (row < M && col < N) out[(long long)row * ldo + col] = acc[i][j][r];
-            }
+    }   // segments
 }
 
 template <int MT, int NT, int WM, int WN, int ST>
 static hipError_t launch_gemm_f32t(const void *params, dim3 grid, hipStream_t stream)
 {
-    hipLaunchKernelGGL((gemm_f32t_kernel<MT, NT, WM, WN, ST>), grid, dim3(WM * WN * 64), 0, stream,
-                       *(const GemmParams *)params);
+    const GemmParams &p = *(const GemmParams *)params;
+    if (p.sk_wgs > 0)
+        hipLaunchKernelGGL((gemm_f32t_kernel<MT, NT, WM, WN, ST, true>), grid, dim3(WM * WN * 64), 0, stream, p);
+    else
+        hipLaunchKernelGGL((gemm_f32t_kernel<MT, NT, WM, WN, ST, false>), grid, dim3(WM * WN * 64), 0, stream, p);
     return hipGetLastError();
 }
 
@@ -1087,7 +1137,9 @@ constexpr int lds_f32t(int mt, int nt, int st) { return st * (mt * 64 + 64 * nt)
     X(64, 128, 1, 2, 4) \
     X(64, 64, 2, 2, 4)
 
-#define NNJIT_F32T_INST(MT, NT, WM, WN, ST) template __global__ void gemm_f32t_kernel<MT, NT, WM, WN, ST>(GemmParams);
+#define NNJIT_F32T_INST(MT, NT, WM, WN, ST)                                           \
+    template __global__ void gemm_f32t_kernel<MT, NT, WM, WN, ST, false>(GemmParams); \
+    template __global__ void gemm_f32t_kernel<MT, NT, WM, WN, ST, true>(GemmParams);
 NNJIT_F32T_LIST(NNJIT_F32T_INST)
 
 #define NNJIT_F32_INST(MT, NT, KT, WM, WN, MF, ST, PF, KS, VEC) \

@@ -303,6 +303,51 @@ hipError_t launch_splitk_reduce(const float *ws, int S, int batch, int M, int N,
 }
 
 // ------------------------------------------------------------------------
+// Stream-K fix-up.  Workgroup w of the GEMM took units [u0(w), u0(w + 1)),
+// u0(w) = w units / G.  A tile is shared when a boundary u0(b) (b = 1 .. G-1)
+// falls strictly inside it; workgroup b - 1 then holds its first units.
+// One workgroup here per boundary: the first boundary inside a tile sums the
+// tile's pieces over the sharing workgroups, in workgroup (= K) order, and
+// writes the tile of C; a piece is in slot 2w if the tile is workgroup w's
+// first segment (u0(w) >= the tile's first unit), else in slot 2w + 1.
+__global__ void __launch_bounds__(256)
+streamk_fixup_kernel(GemmParams p, int mt, int nt)
+{
+    const long long G = p.sk_wgs;
+    const int b = blockIdx.x + 1;
+    auto u0 = [&](long long w) { return w * p.units / G; };
+    const long long ub = u0(b);
+    const long long t = ub / p.nslab;
+    const long long tstart = t * p.nslab, tend = tstart + p.nslab;
+    if (ub == tstart || u0(b - 1) > tstart) return;   // no shared tile here, or an earlier boundary's
+    int tm, tn;
+    tile_of((int)t, p.tiles_m, p.tiles_n, p.group_m, tm, tn);
+    const int m0 = tm * mt, n0 = tn * nt;
+    const long long tile_elems = (long long)mt * nt;
+    for (int e = 4 * threadIdx.x; e < mt * nt; e += 4 * 256) {
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        for (long long w = b - 1; w < G && u0(w) < tend; ++w) {
+            const long long slot = 2 * w + (u0(w) >= tstart ? 0 : 1);
+            const f32x4 v = *(const f32x4 *)(p.ws + slot * tile_elems + e);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) acc[q] += v[q];
+        }
+        const int row = m0 + e / nt, col = n0 + e % nt;
+        if (row < p.M)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                if (col + q < p.N) p.C[(long long)row * p.ldc + col + q] = acc[q];
+    }
+}
+
+hipError_t launch_streamk_fixup(const GemmParams &p, int mt, int nt, hipStream_t stream)
+{
+    if (p.sk_wgs < 2) return hipSuccess;
+    hipLaunchKernelGGL(streamk_fixup_kernel, dim3((unsigned)(p.sk_wgs - 1)), dim3(256), 0, stream, p, mt, nt);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------
 // Streaming-read reference: every 16-byte chunk of src read once (four loads
 // in flight per lane, consecutive lanes on consecutive chunks), combined by
 // XOR so the loads cannot be dropped; a workgroup stores only if its value

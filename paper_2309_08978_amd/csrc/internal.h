@@ -24,8 +24,19 @@ struct GemmParams {
     int kchunk;            // K range of one split, a multiple of the K-slab
     int tiles_m, tiles_n;
     int group_m;           // tile rows per group of the tile order (1 .. tiles_m)
-    float *ws;             // S > 1: partial products, row-major [S][batch][M][N]
+    float *ws;             // S > 1: partial products, row-major [S][batch][M][N];
+                           // stream-K: partial tiles, [2 * sk_wgs][Mt][Nt]
     const void *zero;      // >= 64 bytes of zeros: the load address of out-of-range elements
+    // Stream-K (sk_wgs > 0, batch 1, S 1): the tiles' K slabs form one
+    // sequence of `units` = tiles x nslab units, cut evenly over sk_wgs
+    // workgroups; workgroup w takes units [w units / sk_wgs, (w + 1) units /
+    // sk_wgs).  A tile covered by one workgroup is stored to C; the pieces of
+    // a tile covered by several go to partial slots (the workgroup's first
+    // piece to slot 2w, its last to 2w + 1) and a fix-up kernel adds them in
+    // workgroup order.
+    int sk_wgs;
+    int nslab;             // K slabs per tile
+    long long units;
 };
 
 // Arguments of the M == 1 kernels: y[N] = x[K] . W[K][N].
@@ -100,6 +111,9 @@ extern const int kNumGemvQ4Variants;
 // or fp16, or n random 32-bit words.
 hipError_t launch_splitk_reduce(const float *ws, int S, int batch, int M, int N, float *C, long long ldc,
                                 long long sC, hipStream_t stream);
+// Stream-K fix-up: C tile = sum, in workgroup order, of the partial slots
+// of every tile that several workgroups share (see GemmParams).
+hipError_t launch_streamk_fixup(const GemmParams &p, int mt, int nt, hipStream_t stream);
 enum FillKind { FILL_F32 = 0, FILL_F16 = 1, FILL_WORDS = 2 };
 // Fixed device scratch of the allocation-free entry point (split-K partials).
 constexpr size_t kNoAllocScratchBytes = (size_t)128 << 20;

@@ -329,6 +329,18 @@ int tile_group_rows(int tiles_m, int tiles_n, int override_rows) {
     return std::max(1, std::min(G, tiles_m));
 }
 
+// Launch geometry of a configuration on this device (a stream-K
+// configuration launches one workgroup per resident slot).
+Geometry geom(const Device &d, const Config &cfg, int64_t batch, int64_t M, int64_t N, int64_t K) {
+    int64_t sk = 0;
+    if (cfg.split == kStreamK && !family_is_gemv(cfg.v->family) && !family_is_q4(cfg.v->family)) {
+        const int gi = variant_index(cfg.v);
+        const int regs = gi < (int)d.regs.size() ? d.regs[gi] : -1;
+        sk = (int64_t)d.limits.num_cus * std::max(1, resources_of(*cfg.v, d.limits, regs).wg_per_cu);
+    }
+    return geometry_of(cfg, batch, M, N, K, sk);
+}
+
 // Launch one configuration on c.stream.  ws: split-K partial storage of at
 // least the geometry's ws_floats floats (unused when the split is 1).  Needs
 // no lock: it reads only the device's constant zero buffer.
@@ -336,7 +348,7 @@ int launch(const Device &d, const Config &cfg, const Call &c, float *ws, const S
     if (s.fault_config >= 0 && s.fault_config == cfg.id)
         return fail(NNJIT_EHIP, "config %d: launch failure injected by NNJIT_FAULT_CONFIG", cfg.id);
     const Variant &v = *cfg.v;
-    const Geometry g = geometry_of(cfg, c.batch, c.M, c.N, c.K);
+    const Geometry g = geom(d, cfg, c.batch, c.M, c.N, c.K);
     if (g.ws_floats > 0 && !ws) return fail(NNJIT_EINVAL, "config %d needs split-K scratch", cfg.id);
     hipError_t e = hipSuccess;
     if (family_is_q4(v.family)) {
@@ -362,14 +374,27 @@ int launch(const Device &d, const Config &cfg, const Call &c, float *ws, const S
         p.M = (int)c.M;
         p.N = (int)c.N;
         p.K = (int)c.K;
-        p.S = cfg.split;
+        p.S = g.split;
         p.kchunk = g.kchunk;
         p.tiles_m = g.tiles_m;
         p.tiles_n = g.tiles_n;
         p.group_m = tile_group_rows(g.tiles_m, g.tiles_n, s.group_m);
         p.ws = ws;
         p.zero = d.zero;
-        const int64_t gx = (int64_t)g.tiles_m * g.tiles_n * cfg.split;
+        if (g.stream_k) {
+            p.A = c.A;
+            p.B = c.B;
+            p.C = (float *)c.C;
+            p.batch = 1;
+            p.sk_wgs = (int)g.wgs;
+            p.nslab = g.nslab;
+            p.units = g.units;
+            e = v.launch(&p, dim3((unsigned)g.wgs), c.stream);
+            if (e == hipSuccess) e = launch_streamk_fixup(p, v.mt, v.nt, c.stream);
+            if (e != hipSuccess) return hip_fail(e, v.name);
+            return NNJIT_OK;
+        }
+        const int64_t gx = (int64_t)g.tiles_m * g.tiles_n * g.split;
         // the kernels number workgroups (x + gx * z) in 32-bit integers
         if (gx * std::min<int64_t>(c.batch, 65535) > INT32_MAX)
             return fail(NNJIT_EINVAL, "%lld workgroups per launch exceed 2^31-1; split the batch or the matrix",
@@ -382,8 +407,8 @@ int launch(const Device &d, const Config &cfg, const Call &c, float *ws, const S
             p.C = (float *)c.C + b0 * c.sC;
             p.batch = (int)nb;
             e = v.launch(&p, dim3((unsigned)gx, 1, (unsigned)nb), c.stream);
-            if (e == hipSuccess && cfg.split > 1)
-                e = launch_splitk_reduce(p.ws, cfg.split, (int)nb, p.M, p.N, p.C, c.ldc, c.sC, c.stream);
+            if (e == hipSuccess && g.split > 1)
+                e = launch_splitk_reduce(p.ws, g.split, (int)nb, p.M, p.N, p.C, c.ldc, c.sC, c.stream);
         }
     } else {
         GemvParams p{};
@@ -406,7 +431,7 @@ int launch(const Device &d, const Config &cfg, const Call &c, float *ws, const S
 
 // Launch on the caller's stream with that stream's split-K scratch (under g_mu).
 int launch_on_stream(Device &d, const Config &cfg, const Call &c) {
-    const Geometry g = geometry_of(cfg, c.batch, c.M, c.N, c.K);
+    const Geometry g = geom(d, cfg, c.batch, c.M, c.N, c.K);
     float *ws = nullptr;
     if (g.ws_floats > 0) {
         const int rc = workspace_for(d, c.stream, g.ws_floats, &ws);
@@ -631,7 +656,7 @@ int run_noalloc(const Call &c) {
         cfg = fallback_config(family_of(kind, c.dtype), c, *d);
         if (!cfg) return fail(NNJIT_ENOCFG, "no element-load fallback configuration");
     }
-    const Geometry g = geometry_of(*cfg, c.batch, c.M, c.N, c.K);
+    const Geometry g = geom(*d, *cfg, c.batch, c.M, c.N, c.K);
     if ((size_t)g.ws_floats * sizeof(float) > kNoAllocScratchBytes)
         return fail(NNJIT_ENOMEM, "configuration %d (%s, split %d) needs %lld bytes of split-K scratch, above the "
                                   "%zu bytes of the fixed scratch; use nnjit_batched_matmul",
@@ -753,7 +778,7 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
     const size_t need = up(a_bytes) + (size_t)b_copies * up(b_bytes) + up(c_bytes);
     int64_t ws_floats = 0;
     for (int i = 0; i < limit; ++i)
-        ws_floats = std::max(ws_floats, geometry_of(configs()[lr.ids[i]], batch, M, N, K).ws_floats);
+        ws_floats = std::max(ws_floats, geom(*d, configs()[lr.ids[i]], batch, M, N, K).ws_floats);
 
     TuneResources res;
     hipError_t e = hipStreamCreateWithFlags(&res.stream, hipStreamNonBlocking);

@@ -71,6 +71,7 @@ const std::vector<Config> &configs() {
             const std::vector<int> &splits =
                 family_is_q4(v->family) ? no_split : family_is_gemv(v->family) ? gemv_splits() : gemm_splits();
             for (int s : splits) out.push_back(Config{(int)out.size(), v, s});
+            if (has_stream_k(*v)) out.push_back(Config{(int)out.size(), v, kStreamK});
         }
         return out;
     }();
@@ -124,10 +125,23 @@ static int64_t pow2ceil(int64_t x) {
     return p;
 }
 
-Geometry geometry_of(const Config &c, int64_t batch, int64_t M, int64_t N, int64_t K) {
+bool has_stream_k(const Variant &v) { return v.family == FAM_GEMM_F32 && v.direct_copy && v.kslices == 1; }
+
+Geometry geometry_of(const Config &c, int64_t batch, int64_t M, int64_t N, int64_t K, int64_t sk_wgs) {
     Geometry g;
     const Variant &v = *c.v;
-    g.split = c.split;
+    g.split = c.split == kStreamK ? 1 : c.split;
+    if (c.split == kStreamK && batch == 1 && K > 0 && sk_wgs > 0) {
+        g.stream_k = true;
+        g.tiles_m = (int)ceil_div(std::max<int64_t>(M, 1), v.mt);
+        g.tiles_n = (int)ceil_div(std::max<int64_t>(N, 1), v.nt);
+        g.nslab = (int)ceil_div(K, v.kt);
+        g.units = (int64_t)g.tiles_m * g.tiles_n * g.nslab;
+        g.kchunk = (int)(g.nslab * (int64_t)v.kt);
+        g.wgs = std::max<int64_t>(1, std::min<int64_t>(sk_wgs, g.units));
+        g.ws_floats = 2 * g.wgs * (int64_t)v.mt * v.nt;
+        return g;
+    }
     if (family_is_q4(v.family)) {
         // one workgroup per nt output rows, no split (batch carries the group size)
         g.group = std::max<int64_t>(1, batch);
@@ -142,11 +156,11 @@ Geometry geometry_of(const Config &c, int64_t batch, int64_t M, int64_t N, int64
     if (!family_is_gemv(v.family)) {
         g.tiles_m = (int)ceil_div(std::max<int64_t>(M, 1), v.mt);
         g.tiles_n = (int)ceil_div(std::max<int64_t>(N, 1), v.nt);
-        const int64_t per = ceil_div(std::max<int64_t>(K, 1), c.split);
+        const int64_t per = ceil_div(std::max<int64_t>(K, 1), g.split);
         g.kchunk = (int)(ceil_div(per, v.kt) * v.kt);
         const int64_t tiles = batch * g.tiles_m * (int64_t)g.tiles_n;
-        g.wgs = tiles * c.split;
-        g.ws_floats = c.split > 1 ? (int64_t)c.split * batch * std::max<int64_t>(M, 1) * std::max<int64_t>(N, 1) : 0;
+        g.wgs = tiles * g.split;
+        g.ws_floats = g.split > 1 ? (int64_t)g.split * batch * std::max<int64_t>(M, 1) * std::max<int64_t>(N, 1) : 0;
     } else {
         g.tiles_m = 1;
         g.tiles_n = (int)ceil_div(std::max<int64_t>(N, 1), v.nt);
@@ -253,8 +267,8 @@ LiteResult lite_space(const Shape &s, const nnjit_device_limits &d, const std::v
         if (r.lds_per_wg > d.lds_per_wg) continue;                            // heuristic 6
         if (r.wg_per_cu < 1) continue;
 
-        const Geometry g = geometry_of(c, s.batch, s.M, s.N, s.K);
         const int64_t slots = (int64_t)d.num_cus * r.wg_per_cu;
+        const Geometry g = geometry_of(c, s.batch, s.M, s.N, s.K, slots);
         Cand cd;
         cd.id = c.id;
         cd.r = r;
@@ -274,6 +288,14 @@ LiteResult lite_space(const Shape &s, const nnjit_device_limits &d, const std::v
             // shape fit: no macro tile wider than the (power-of-two rounded) matrix
             if (v.mt > std::max<int64_t>(16, pow2ceil(s.M)) || v.nt > std::max<int64_t>(16, pow2ceil(s.N))) fit = false;
             const int64_t tiles = s.batch * g.tiles_m * (int64_t)g.tiles_n;
+            if (c.split == kStreamK) {
+                // stream-K: only where the tiles leave the last wave of
+                // workgroups short, with at least four K slabs per workgroup
+                if (!g.stream_k || g.units < 4 * g.wgs) continue;
+                const int64_t tw = ceil_div(tiles, slots);
+                if ((double)tiles / (double)(tw * slots) >= 0.95) continue;
+                cd.eff = 1.0;
+            }
             // K groups inside a workgroup pay off only while the chip has
             // few workgroups (fewer than two per CU)
             if (v.kslices > 1 && tiles * c.split >= 2LL * d.num_cus) continue;

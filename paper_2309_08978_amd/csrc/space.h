@@ -78,16 +78,28 @@ struct LiteResult {
 LiteResult lite_space(const Shape &s, const nnjit_device_limits &d, const std::vector<int> *measured_regs,
                       const std::vector<int> *spills);
 
+// The split value of a stream-K configuration (see GemmParams): the K slabs
+// of all tiles cut evenly over one workgroup per resident slot.
+constexpr int kStreamK = 0;
+// Variants that have a stream-K configuration (fp32 shared-slab direct copy).
+bool has_stream_k(const Variant &v);
+
 // Launch geometry of a configuration for a shape.
 struct Geometry {
     int tiles_m = 0, tiles_n = 0;  // GEMM tiles per batch slice (GEMV: segs in tiles_n)
-    int split = 1;
+    int split = 1;                 // split-K factor of the launch (1 for stream-K)
     int kchunk = 0;
     int64_t wgs = 0;               // workgroups over the whole launch
-    int64_t ws_floats = 0;         // split-K partial storage (S x batch x M x N floats)
+    int64_t ws_floats = 0;         // split-K partial storage (S x batch x M x N floats; stream-K 2 x wgs x Mt x Nt)
     int64_t group = 0;             // 4-bit GEMV: the group size
+    bool stream_k = false;
+    int nslab = 0;                 // stream-K: K slabs per tile
+    int64_t units = 0;             // stream-K: tiles x nslab
 };
-Geometry geometry_of(const Config &c, int64_t batch, int64_t M, int64_t N, int64_t K);
+// sk_wgs: the workgroups a stream-K configuration launches (resident slots of
+// the device, CUs x workgroups per CU); unused by other configurations.  A
+// stream-K configuration on a batch > 1 or K == 0 shape runs tiled (split 1).
+Geometry geometry_of(const Config &c, int64_t batch, int64_t M, int64_t N, int64_t K, int64_t sk_wgs = 0);
 
 // Index of a variant inside its family table (used to look up measured data).
 int variant_index(const Variant *v);

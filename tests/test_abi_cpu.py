@@ -142,7 +142,7 @@ def test_config_table(lib):
     p2 = lambda x: x > 0 and (x & (x - 1)) == 0
     for c in cfgs:
         assert c["vec"] <= 16                     # heuristic 1: at most 128-bit accesses
-        assert p2(c["split"])
+        assert p2(c["split"]) or (c["split"] == 0 and c["family"] == "gemm_f32" and c["direct"] == 1)   # 0: stream-K
         if c["family"].startswith("gemm"):
             for k in ("Mt", "Nt", "Kt"):
                 assert p2(c[k]), (c, k)           # heuristic 2: power-of-two tiles
@@ -328,3 +328,64 @@ def test_q4_lite_space(lib, N, K, G):
     assert nj.nnjit_lite_space(nj.NNJIT_KIND_GEMV_Q4, nj.NNJIT_F16, G, 1, N, K, d)[0] == ids
     with pytest.raises(nj.NnjitError):
         nj.nnjit_lite_space(nj.NNJIT_KIND_GEMV_Q4, nj.NNJIT_F32, G, 1, N, K, d)
+
+
+def _streamk_model(tiles, nslab, G):
+    """The stream-K work split written out plainly (the GEMM kernel's segment
+    loop and the fix-up kernel's contributor walk, as GemmParams documents
+    them): returns (full tiles -> writer, partial slot writes, fix-up reads)."""
+    units = tiles * nslab
+    u0 = lambda w: w * units // G
+    full, writes = {}, {}
+    for w in range(G):
+        su, end, first = u0(w), u0(w + 1), True
+        while su < end:
+            t = su // nslab
+            ks = su - t * nslab
+            ke = min(nslab, ks + (end - su))
+            if ks == 0 and ke == nslab:
+                assert t not in full
+                full[t] = w
+            else:
+                slot = 2 * w + (0 if first else 1)
+                assert slot not in writes, "a slot is written twice"
+                writes[slot] = (t, ks, ke)
+            su += ke - ks
+            first = False
+    reads = {}
+    for b in range(1, G):
+        ub = u0(b)
+        t = ub // nslab
+        tstart, tend = t * nslab, t * nslab + nslab
+        if ub == tstart or u0(b - 1) > tstart:
+            continue
+        assert t not in reads, "two fix-up workgroups for one tile"
+        w, slots = b - 1, []
+        while w < G and u0(w) < tend:
+            slots.append(2 * w + (0 if u0(w) >= tstart else 1))
+            w += 1
+        reads[t] = slots
+    return full, writes, reads
+
+
+@pytest.mark.parametrize("tiles,nslab,G", [(172, 256, 256), (192, 256, 256), (500, 256, 256), (64, 64, 256),
+                                           (3, 5, 256), (1, 700, 256), (300, 7, 256), (256, 256, 256),
+                                           (257, 100, 512), (40, 1024, 37)])
+def test_streamk_split_covers_every_unit_once(tiles, nslab, G):
+    """Every tile is either stored whole by one workgroup or summed by exactly
+    one fix-up workgroup from partial slots that cover its K slabs exactly
+    once, in K order; no slot is written twice and none lies outside the
+    2 x G slots of the workspace."""
+    G = min(G, tiles * nslab)
+    full, writes, reads = _streamk_model(tiles, nslab, G)
+    for t in range(tiles):
+        assert (t in full) != (t in reads), t
+        if t in reads:
+            pieces = [writes[s] for s in reads[t]]
+            assert all(p[0] == t for p in pieces)
+            ranges = [(p[1], p[2]) for p in pieces]
+            assert ranges[0][0] == 0 and ranges[-1][1] == nslab
+            assert all(a[1] == b[0] for a, b in zip(ranges, ranges[1:])), "pieces out of K order or overlapping"
+            assert len(reads[t]) >= 2
+    assert sorted(s for ss in reads.values() for s in ss) == sorted(writes)
+    assert all(0 <= s < 2 * G for s in writes)

@@ -472,3 +472,31 @@ def test_random_gemv_shapes_bit_exact(all_configs, dt):
             assert np.array_equal(host(C), R), f"{c['name']} split={c['split']}: N={N} K={K}"
             n += 1
     print(f"{dt}: {n} forced random GEMV runs bit-exact", flush=True)
+
+
+@pytest.mark.parametrize("shape", [(300, 520, 1000), (512, 1024, 2048), (64, 128, 4100), (1000, 264, 72),
+                                   (130, 64, 16), (257, 1032, 520)])
+def test_stream_k_configs_bit_exact(all_configs, shape):
+    """Every stream-K configuration (the tiles' K slabs cut evenly over one
+    workgroup per resident slot; shared tiles summed by the fix-up kernel)
+    on ragged shapes -- tiles shared by two or more workgroups, workgroups
+    spanning several tiles, K not a multiple of the slab -- gives the
+    oracle's exact sums (small integers), twice in a row; a batched call
+    forced onto it runs tiled."""
+    import torch
+    M, N, K = shape
+    A, B = workloads.small_int_operands(7700 + M + K, 1, M, K, N, "f32")
+    R = oracle.matmul(A, B)
+    dA, dB = dev(A), dev(B)
+    sk = [c for c in all_configs if c["family"] == "gemm_f32" and c["split"] == 0]
+    assert sk
+    for c in sk:
+        for rep in range(2):
+            C = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda:0")
+            nj.matmul(dA, dB, C, cfg=c["id"])
+            assert np.array_equal(host(C), R), f"{c['name']} stream-K {shape} rep {rep}"
+    c = sk[0]
+    A3, B3 = workloads.small_int_operands(7800, 3, 40, 96, 136, "f32")
+    C3 = torch.full((3, 40, 136), float("nan"), dtype=torch.float32, device="cuda:0")
+    nj.batched_matmul(dev(A3), dev(B3), C3, cfg=c["id"])
+    assert np.array_equal(host(C3), oracle.matmul(A3, B3))
