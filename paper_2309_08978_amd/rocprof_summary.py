@@ -133,20 +133,30 @@ def traffic(fetch_dir, write_dir, meta):
             "write": out["write"], "reps": meta["reps"], "copy_ref_mb": meta["copy_ref_mb"]}
 
 
-def kernel_duration_us(trace_dir):
-    """Mean start-to-end duration (us) of the library's dispatches after the
-    last reference copy in a --kernel-trace run of bench.py --profile-op
-    (the profiled product's launches), and their kernel names."""
+def kernel_duration_us(trace_dir, steady_n: int = 20):
+    """Durations (us) of the profiled product's dispatches in a --kernel-trace
+    run of bench.py --profile-op: the mean over the library's dispatches
+    after the last reference copy (the counted launches), the mean over the
+    last `steady_n` dispatches of the same kernels before the copies (the
+    half-second warm-up: the clock and caches of the timed steps; the copies
+    themselves disturb the first launches after them), and the kernel names."""
     path = sorted(glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True))
     if not path:
         raise SystemExit(f"no kernel_trace.csv under {trace_dir}")
     rows = sorted(_rows(path[0]), key=lambda r: int(r["Start_Timestamp"]))
-    copies = [i for i, r in enumerate(rows) if "copyBuffer" in r["Kernel_Name"] or "copy_kernel" in r["Kernel_Name"]]
-    after = [r for r in rows[(copies[-1] + 1 if copies else 0):] if "nnjit" in r["Kernel_Name"]]
+    is_copy = lambda r: "copyBuffer" in r["Kernel_Name"] or "copy_kernel" in r["Kernel_Name"]
+    copies = [i for i, r in enumerate(rows) if is_copy(r)]
+    last = copies[-1] if copies else -1
+    after = [r for r in rows[last + 1:] if "nnjit" in r["Kernel_Name"]]
     if not after:
-        return None, []
-    d = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in after]
-    return statistics.mean(d), sorted({_short(r["Kernel_Name"]) for r in after})
+        return None, None, []
+    names = {r["Kernel_Name"] for r in after}
+    first_ref = last
+    while first_ref > 0 and is_copy(rows[first_ref - 1]):
+        first_ref -= 1
+    before = [r for r in rows[:max(first_ref, 0)] if r["Kernel_Name"] in names][-steady_n:]
+    dur = lambda rs: statistics.mean((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in rs)
+    return dur(after), (dur(before) if before else None), sorted({_short(n) for n in names})
 
 
 def mfma_busy(pmc_dir, meta, simds: int = 1024, trace_dir=None, clock_ghz: float = 2.4):
@@ -156,8 +166,10 @@ def mfma_busy(pmc_dir, meta, simds: int = 1024, trace_dir=None, clock_ghz: float
     product's dispatches after the reference copy: busy / (simds x
     GRBM_GUI_ACTIVE / 8) -- which counts the gaps between dispatches under
     the profiler as busy time -- and, given a kernel-trace run of the same
-    kernel, busy / (simds x kernel duration x clock), over the kernel's own
-    duration at the 2.4 GHz peak clock."""
+    command, busy / (simds x kernel duration x clock), over the kernel's own
+    duration at the 2.4 GHz peak clock (SQ_VALU_MFMA_BUSY_CYCLES counts the
+    instructions' issue cycles, the same for every launch, so the steady
+    warm-up launches' duration gives the timed steps' share).""" 
     path = sorted(glob.glob(os.path.join(pmc_dir, "**", "*counter_collection.csv"), recursive=True))
     if not path:
         raise SystemExit(f"no counter_collection.csv under {pmc_dir}")
@@ -181,11 +193,14 @@ def mfma_busy(pmc_dir, meta, simds: int = 1024, trace_dir=None, clock_ghz: float
     out["mfma_busy_fraction"] = round(busy / (simds * gui / 8.0), 4) if gui > 0 else None
     out["kernels"] = sorted({_short(v["name"]) for v in mine})
     if trace_dir:
-        dur, names = kernel_duration_us(trace_dir)
+        dur, steady, names = kernel_duration_us(trace_dir)
         if dur:
-            out["kernel_duration_us"] = round(dur, 2)
             out["trace_kernels"] = names
-            out["mfma_busy_of_kernel_duration"] = round(busy / (simds * dur * 1e-6 * clock_ghz * 1e9), 4)
+            out["kernel_duration_us_after_copy"] = round(dur, 2)
+            out["mfma_busy_of_kernel_duration_after_copy"] = round(busy / (simds * dur * 1e-6 * clock_ghz * 1e9), 4)
+        if steady:
+            out["kernel_duration_us_steady"] = round(steady, 2)
+            out["mfma_busy_of_kernel_duration"] = round(busy / (simds * steady * 1e-6 * clock_ghz * 1e9), 4)
     return out
 
 
