@@ -110,3 +110,45 @@ def all_split_configs():
     cf = nj.configs()
     return {"f32": next(c["id"] for c in cf if c["family"] == "gemm_f32" and c["vec"] == 16 and c["split"] == 4),
             "f16": next(c["id"] for c in cf if c["family"] == "gemm_f16" and c["vec"] == 16 and c["split"] == 4)}
+
+
+def test_noalloc_captured_in_a_graph(all_split_configs, monkeypatch):
+    """The use the entry point exists for: calls recorded into a HIP graph on a
+    stream no call has used before (no scratch of its own) -- a split-K
+    configuration, whose partials go to the fixed scratch -- replay correctly
+    several times, with eager work between the replays, every replay equal
+    to the eager result and to the oracle."""
+    import torch
+    cfg = all_split_configs["f32"]
+    monkeypatch.setenv("NNJIT_FORCE_CONFIG", str(cfg))
+    nj.nnjit_cache_clear()   # the library reads its environment here
+    try:
+        M, N, K = 96, 200, 520
+        A, B = workloads.small_int_operands(7400, 1, M, K, N, "f32")
+        R = oracle.matmul(A, B)
+        dA, dB = dev(A.reshape(1, M, K)), dev(B.reshape(1, K, N))
+        eager = torch.full((1, M, N), float("nan"), dtype=torch.float32, device="cuda:0")
+        assert _noalloc(dA, dB, eager, nj.NNJIT_F32) == nj.NNJIT_OK, nj.nnjit_last_error()
+        torch.cuda.synchronize()
+        assert np.array_equal(host(eager)[0], R)
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            C = torch.full((1, M, N), float("nan"), dtype=torch.float32, device="cuda:0")
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=side):
+            rc = _noalloc(dA, dB, C, nj.NNJIT_F32, side)
+        assert rc == nj.NNJIT_OK, nj.nnjit_last_error()
+        other = torch.full((1, M, N), float("nan"), dtype=torch.float32, device="cuda:0")
+        for rep in range(4):
+            C.fill_(float("nan"))
+            assert _noalloc(dA, dB, other, nj.NNJIT_F32) == nj.NNJIT_OK   # eager use of the same scratch
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            assert np.array_equal(host(C)[0], R), f"replay {rep}"
+            assert np.array_equal(host(other)[0], R)
+    finally:
+        monkeypatch.delenv("NNJIT_FORCE_CONFIG")
+        nj.nnjit_cache_clear()
