@@ -308,42 +308,78 @@ hipError_t launch_splitk_reduce(const float *ws, int S, int batch, int M, int N,
 // falls strictly inside it; workgroup b - 1 then holds its first units.
 // One workgroup here per boundary: the first boundary inside a tile sums the
 // tile's pieces over the sharing workgroups, in workgroup (= K) order, and
-// writes the tile of C; a piece is in slot 2w if the tile is workgroup w's
-// first segment (u0(w) >= the tile's first unit), else in slot 2w + 1.
-__global__ void __launch_bounds__(256)
+// writes the tile of C.  A piece is in slot 2w if the tile is workgroup w's
+// first segment, else in slot 2w + 1: every sharing workgroup after b - 1
+// starts inside the tile (slot 2w); b - 1 starts at the tile's first unit
+// (slot 2(b - 1)) or before it (2(b - 1) + 1).  Each thread keeps QB quads
+// times up to 4 pieces of loads in flight before it stores.
+constexpr int kFixupThreads = 512;
+__global__ void __launch_bounds__(kFixupThreads)
 streamk_fixup_kernel(GemmParams p, int mt, int nt)
 {
+    constexpr int QB = 4;
     const long long G = p.sk_wgs;
     const int b = blockIdx.x + 1;
-    auto u0 = [&](long long w) { return w * p.units / G; };
-    const long long ub = u0(b);
+    const long long ua = (long long)(b - 1) * p.units / G, ub = (long long)b * p.units / G;
     const long long t = ub / p.nslab;
     const long long tstart = t * p.nslab, tend = tstart + p.nslab;
-    if (ub == tstart || u0(b - 1) > tstart) return;   // no shared tile here, or an earlier boundary's
+    if (ub == tstart || ua > tstart) return;   // no shared tile here, or an earlier boundary's
+    int nw = 2;                                // sharing workgroups b - 1, b, ...
+    while (b - 1 + nw < G && (long long)(b - 1 + nw) * p.units / G < tend) ++nw;
+    const long long slot0 = 2LL * (b - 1) + (ua == tstart ? 0 : 1);
     int tm, tn;
     tile_of((int)t, p.tiles_m, p.tiles_n, p.group_m, tm, tn);
     const int m0 = tm * mt, n0 = tn * nt;
     const long long tile_elems = (long long)mt * nt;
-    for (int e = 4 * threadIdx.x; e < mt * nt; e += 4 * 256) {
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-        for (long long w = b - 1; w < G && u0(w) < tend; ++w) {
-            const long long slot = 2 * w + (u0(w) >= tstart ? 0 : 1);
-            const f32x4 v = *(const f32x4 *)(p.ws + slot * tile_elems + e);
+    const int quads = mt * nt / 4, nq = nt / 4;
+    const float *__restrict__ ws = p.ws;
+    float *__restrict__ C = p.C;
+    const bool vec_c = (p.ldc & 3) == 0 && ((unsigned long long)C & 15) == 0;
+    for (int q0 = threadIdx.x; q0 < quads; q0 += QB * kFixupThreads) {
+        f32x4 acc[QB];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) acc[q] += v[q];
+        for (int i = 0; i < QB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int w0 = 0; w0 < nw; w0 += 4) {
+            f32x4 v[QB][4];   // indices clamped: the loads are unconditional
+#pragma unroll
+            for (int i = 0; i < QB; ++i)
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int q = min(q0 + i * kFixupThreads, quads - 1), k = min(w0 + u, nw - 1);
+                    const long long slot = k == 0 ? slot0 : 2LL * (b - 1 + k);
+                    v[i][u] = *(const f32x4 *)(ws + slot * tile_elems + 4LL * q);
+                }
+#pragma unroll
+            for (int i = 0; i < QB; ++i)
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    if (w0 + u < nw)
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) acc[i][e] += v[i][u][e];
         }
-        const int row = m0 + e / nt, col = n0 + e % nt;
-        if (row < p.M)
 #pragma unroll
-            for (int q = 0; q < 4; ++q)
-                if (col + q < p.N) p.C[(long long)row * p.ldc + col + q] = acc[q];
+        for (int i = 0; i < QB; ++i) {
+            const int q = q0 + i * kFixupThreads;
+            if (q >= quads) break;
+            const int row = m0 + q / nq, col = n0 + (q % nq) * 4;
+            if (row >= p.M) continue;
+            float *d = C + (long long)row * p.ldc + col;
+            if (vec_c && col + 4 <= p.N) {
+                *(f32x4 *)d = acc[i];
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (col + e < p.N) d[e] = acc[i][e];
+            }
+        }
     }
 }
 
 hipError_t launch_streamk_fixup(const GemmParams &p, int mt, int nt, hipStream_t stream)
 {
     if (p.sk_wgs < 2) return hipSuccess;
-    hipLaunchKernelGGL(streamk_fixup_kernel, dim3((unsigned)(p.sk_wgs - 1)), dim3(256), 0, stream, p, mt, nt);
+    hipLaunchKernelGGL(streamk_fixup_kernel, dim3((unsigned)(p.sk_wgs - 1)), dim3(kFixupThreads), 0, stream, p, mt,
+                       nt);
     return hipGetLastError();
 }
 
