@@ -311,15 +311,16 @@ hipError_t launch_splitk_reduce(const float *ws, int S, int batch, int M, int N,
 // writes the tile of C.  A piece is in slot 2w if the tile is workgroup w's
 // first segment, else in slot 2w + 1: every sharing workgroup after b - 1
 // starts inside the tile (slot 2w); b - 1 starts at the tile's first unit
-// (slot 2(b - 1)) or before it (2(b - 1) + 1).  Each thread keeps QB quads
-// times up to 4 pieces of loads in flight before it stores.
-constexpr int kFixupThreads = 512;
+// (slot 2(b - 1)) or before it (2(b - 1) + 1).  kFixupParts workgroups per
+// boundary share the tile's element quads; each thread keeps QB quads times
+// up to 4 pieces of loads in flight before it stores.
+constexpr int kFixupThreads = 512, kFixupParts = 4;
 __global__ void __launch_bounds__(kFixupThreads)
 streamk_fixup_kernel(GemmParams p, int mt, int nt)
 {
     constexpr int QB = 4;
     const long long G = p.sk_wgs;
-    const int b = blockIdx.x + 1;
+    const int b = blockIdx.x / kFixupParts + 1, part = blockIdx.x % kFixupParts;
     const long long ua = (long long)(b - 1) * p.units / G, ub = (long long)b * p.units / G;
     const long long t = ub / p.nslab;
     const long long tstart = t * p.nslab, tend = tstart + p.nslab;
@@ -332,10 +333,12 @@ streamk_fixup_kernel(GemmParams p, int mt, int nt)
     const int m0 = tm * mt, n0 = tn * nt;
     const long long tile_elems = (long long)mt * nt;
     const int quads = mt * nt / 4, nq = nt / 4;
+    const int qbeg = (int)((long long)quads * part / kFixupParts);
+    const int qend = (int)((long long)quads * (part + 1) / kFixupParts);
     const float *__restrict__ ws = p.ws;
     float *__restrict__ C = p.C;
     const bool vec_c = (p.ldc & 3) == 0 && ((unsigned long long)C & 15) == 0;
-    for (int q0 = threadIdx.x; q0 < quads; q0 += QB * kFixupThreads) {
+    for (int q0 = qbeg + threadIdx.x; q0 < qend; q0 += QB * kFixupThreads) {
         f32x4 acc[QB];
 #pragma unroll
         for (int i = 0; i < QB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -345,7 +348,7 @@ streamk_fixup_kernel(GemmParams p, int mt, int nt)
             for (int i = 0; i < QB; ++i)
 #pragma unroll
                 for (int u = 0; u < 4; ++u) {
-                    const int q = min(q0 + i * kFixupThreads, quads - 1), k = min(w0 + u, nw - 1);
+                    const int q = min(q0 + i * kFixupThreads, qend - 1), k = min(w0 + u, nw - 1);
                     const long long slot = k == 0 ? slot0 : 2LL * (b - 1 + k);
                     v[i][u] = *(const f32x4 *)(ws + slot * tile_elems + 4LL * q);
                 }
@@ -360,7 +363,7 @@ streamk_fixup_kernel(GemmParams p, int mt, int nt)
 #pragma unroll
         for (int i = 0; i < QB; ++i) {
             const int q = q0 + i * kFixupThreads;
-            if (q >= quads) break;
+            if (q >= qend) break;
             const int row = m0 + q / nq, col = n0 + (q % nq) * 4;
             if (row >= p.M) continue;
             float *d = C + (long long)row * p.ldc + col;
@@ -378,8 +381,8 @@ streamk_fixup_kernel(GemmParams p, int mt, int nt)
 hipError_t launch_streamk_fixup(const GemmParams &p, int mt, int nt, hipStream_t stream)
 {
     if (p.sk_wgs < 2) return hipSuccess;
-    hipLaunchKernelGGL(streamk_fixup_kernel, dim3((unsigned)(p.sk_wgs - 1)), dim3(kFixupThreads), 0, stream, p, mt,
-                       nt);
+    hipLaunchKernelGGL(streamk_fixup_kernel, dim3((unsigned)((p.sk_wgs - 1) * kFixupParts)), dim3(kFixupThreads), 0,
+                       stream, p, mt, nt);
     return hipGetLastError();
 }
 
