@@ -76,7 +76,8 @@ gemv_kernel(GemvParams p)
     auto wload = [&](int k) -> u32x4 {
         const T *src = W + (long long)k * p.ldw + n;
         if constexpr (VEC) {
-            return *(const u32x4 *)src;
+            // W is read exactly once: a non-temporal load
+            return __builtin_nontemporal_load((const u32x4 *)src);
         } else {
             // element loads, columns at or beyond N read as +0
             u32x4 v = {0u, 0u, 0u, 0u};
@@ -399,11 +400,12 @@ stream_read_kernel(const u32x4 *__restrict__ src, long long n16, unsigned *sink)
     long long i = (long long)blockIdx.x * 256 + threadIdx.x;
     unsigned acc = 0;
     for (; i + 3 * stride < n16; i += 4 * stride) {
-        const u32x4 a = src[i], b = src[i + stride], c = src[i + 2 * stride], d = src[i + 3 * stride];
+        const u32x4 a = __builtin_nontemporal_load(src + i), b = __builtin_nontemporal_load(src + i + stride),
+                    c = __builtin_nontemporal_load(src + i + 2 * stride), d = __builtin_nontemporal_load(src + i + 3 * stride);
         acc ^= (a.x ^ a.y ^ a.z ^ a.w) ^ (b.x ^ b.y ^ b.z ^ b.w) ^ (c.x ^ c.y ^ c.z ^ c.w) ^ (d.x ^ d.y ^ d.z ^ d.w);
     }
     for (; i < n16; i += stride) {
-        const u32x4 a = src[i];
+        const u32x4 a = __builtin_nontemporal_load(src + i);
         acc ^= a.x ^ a.y ^ a.z ^ a.w;
     }
     if (acc == 0x9e3779b9u) sink[blockIdx.x] = acc;

@@ -89,7 +89,7 @@ gemv_q4_kernel(GemvQ4Params p)
             const int kc = min(k0, klast);
 #pragma unroll
             for (int r = 0; r < RW; ++r) {
-                wv[b][r] = *(const u32x4 *)(wrow[r] + (kc >> 3));
+                wv[b][r] = __builtin_nontemporal_load((const u32x4 *)(wrow[r] + (kc >> 3)));
                 sv[b][r] = srow[r][kc / G];
             }
             if (live && k0 + 32 <= K) {
