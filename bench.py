@@ -340,7 +340,7 @@ def burst_us(fn, reps, stream, side):
 
 
 def stream_ceiling_us(nbytes, copies, reps, stream, side):
-    """What one launch can stream: a plain 16-byte-load read (nnjit_stream_read)
+    """What one launch can stream: a non-temporal 16-byte-load read (nnjit_stream_read)
     of the same byte count, rotating over the same number of replicas (cold),
     timed like the products; the best of several grid sizes."""
     import torch
@@ -464,7 +464,7 @@ def main(argv=None):
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-stream-ceiling", action="store_true",
-                    help="skip the plain streaming-read reference of bandwidth-bound products")
+                    help="skip the streaming-read reference of bandwidth-bound products")
     ap.add_argument("--eager", action="store_true", help="time eager ABI calls instead of the graph replay")
     ap.add_argument("--tuned-cache", default=None,
                     help="kernel database file: loaded before tuning if it exists, written after")

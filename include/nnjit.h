@@ -382,7 +382,8 @@ int nnjit_cache_save(const char *path);
 int nnjit_cache_load(const char *path);
 
 /* Measurement helper: reads `bytes` of device memory at `src` once, with
- * 16-byte loads from `workgroups` workgroups of 256 threads, and writes
+ * 16-byte non-temporal loads (the GEMVs read their weights the same way)
+ * from `workgroups` workgroups of 256 threads, and writes
  * (practically) nothing -- at most one word per workgroup into `sink`
  * (device memory of `workgroups` 32-bit words).  Timed around it, this is
  * what one launch can stream from HBM, the reference against which the
