@@ -65,6 +65,15 @@ def test_validation_without_gpu(lib):
     # a 4-bit configuration is not a MatMul configuration, and the other way round
     assert nj.nnjit_matmul_config(q4, 1, 4, 8, 8, 1, 8, 0, 2, 8, 0, 3, 8, 0, 1, None) == nj.NNJIT_EINVAL
     assert nj.nnjit_gemv_q4_config(f16, 64, 64, 32, 1, 2, 8, 3, 2, 4, None) == nj.NNJIT_EINVAL
+    # streaming-read reference: (src, bytes, sink, workgroups, stream)
+    assert nj.nnjit_stream_read(16, 24, 32, 8, None) == nj.NNJIT_EINVAL                 # bytes not a multiple of 16
+    assert nj.nnjit_stream_read(16, -16, 32, 8, None) == nj.NNJIT_EINVAL
+    assert nj.nnjit_stream_read(16, 64, 32, 0, None) == nj.NNJIT_EINVAL                 # no workgroup
+    assert nj.nnjit_stream_read(16, 64, 32, (1 << 20) + 1, None) == nj.NNJIT_EINVAL
+    assert nj.nnjit_stream_read(8, 64, 32, 8, None) == nj.NNJIT_EINVAL                  # src not 16-byte aligned
+    assert nj.nnjit_stream_read(None, 64, 32, 8, None) == nj.NNJIT_EINVAL
+    assert nj.nnjit_stream_read(16, 64, None, 8, None) == nj.NNJIT_EINVAL               # no sink
+    assert nj.nnjit_stream_read(None, 0, 32, 8, None) == nj.NNJIT_OK                    # nothing to read
 
 
 def test_tune_stats_forms(lib):
