@@ -910,6 +910,7 @@ int tune(int kind, int dtype, int64_t batch, int64_t M, int64_t N, int64_t K) {
         }
         if (!ok) {
             ++t_stats.n_failed;
+            t_trace.emplace_back(cfg.id, -1.0, ms_since(t0));
             (void)hipGetLastError();
             (void)hipStreamSynchronize(c.stream);
             drop_graphs();

@@ -492,3 +492,33 @@ def test_tune_does_not_block_dispatch_on_other_threads():
     if alive_before:
         assert alive_after, "the calls waited for the tune to finish"
     nj.nnjit_cache_clear()
+
+
+def test_tune_trace_agrees_with_stats_and_lite_space():
+    """The evaluation trace of a tune -- one entry per first-pass candidate,
+    in the lite space's order: its id, its per-launch time (-1 when aborted
+    or failed) and the milliseconds since the call began -- agrees with the
+    call's statistics; the returned count is the full length whatever the
+    cap; a cache hit evaluates nothing."""
+    import ctypes
+    nj.nnjit_cache_clear()
+    M, N, K = 256, 1024, 512
+    cfg = nj.nnjit_tune(M, N, K, nj.NNJIT_F32)
+    assert cfg >= 0, nj.nnjit_last_error()
+    st = nj.nnjit_last_tune_stats_ex()
+    tr = nj.nnjit_last_tune_trace(4096)
+    assert len(tr) >= 2
+    assert len(tr) == st["n_timed"] + st["n_aborted"] + st["n_failed"]
+    ids = nj.nnjit_lite_space(nj.NNJIT_KIND_GEMM, nj.NNJIT_F32, 1, M, N, K)[0]
+    assert [t[0] for t in tr] == ids[:len(tr)]
+    timed = [t for t in tr if t[1] >= 0]
+    assert len(timed) == st["n_timed"] and all(t[1] > 0 for t in timed)
+    at = [t[2] for t in tr]
+    assert at == sorted(at) and 0 <= at[0] and at[-1] <= st["wall_ms"]
+    assert st["chosen"] == cfg and cfg in {t[0] for t in timed}
+    a, u, m = (ctypes.c_int * 2)(), (ctypes.c_double * 2)(), (ctypes.c_double * 2)()
+    assert nj.load().nnjit_last_tune_trace(a, u, m, 2) == len(tr)
+    assert [(a[i], u[i], m[i]) for i in range(2)] == tr[:2]
+    assert nj.nnjit_tune(M, N, K, nj.NNJIT_F32) == cfg
+    assert nj.nnjit_last_tune_trace() == []
+    assert nj.nnjit_last_tune_stats_ex()["cache_hit"] == 1
