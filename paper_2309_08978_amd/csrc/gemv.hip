@@ -307,14 +307,14 @@ hipError_t launch_splitk_reduce(const float *ws, int S, int batch, int M, int N,
 // Stream-K fix-up.  Workgroup w of the GEMM took units [u0(w), u0(w + 1)),
 // u0(w) = w units / G.  A tile is shared when a boundary u0(b) (b = 1 .. G-1)
 // falls strictly inside it; workgroup b - 1 then holds its first units.
-// One workgroup here per boundary: the first boundary inside a tile sums the
+// kFixupParts workgroups here per boundary, each taking a quarter of the
+// tile's element quads: those of the first boundary inside a tile sum the
 // tile's pieces over the sharing workgroups, in workgroup (= K) order, and
-// writes the tile of C.  A piece is in slot 2w if the tile is workgroup w's
+// write the tile of C.  A piece is in slot 2w if the tile is workgroup w's
 // first segment, else in slot 2w + 1: every sharing workgroup after b - 1
 // starts inside the tile (slot 2w); b - 1 starts at the tile's first unit
-// (slot 2(b - 1)) or before it (2(b - 1) + 1).  kFixupParts workgroups per
-// boundary share the tile's element quads; each thread keeps QB quads times
-// up to 4 pieces of loads in flight before it stores.
+// (slot 2(b - 1)) or before it (2(b - 1) + 1).  Each thread keeps QB quads
+// times up to 4 pieces of loads in flight before it stores.
 constexpr int kFixupThreads = 512, kFixupParts = 4;
 __global__ void __launch_bounds__(kFixupThreads)
 streamk_fixup_kernel(GemmParams p, int mt, int nt)
